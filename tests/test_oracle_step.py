@@ -1,0 +1,229 @@
+"""Pins of the oracle's optimizer step.
+
+Eq. 1 (Momentum) and Eq. 2 (Adam) with the textbook bias correction the paper
+omits ("without damping and scaling constants"); AdamW as decoupled weight
+decay.  With quantization bypassed the step must equal torch.optim's CPU
+implementations (a library routine, independent of the oracle); the 8-bit step
+must equal dequantize -> torch.optim update -> exact requantize (Section 3,
+Fig. 1), and the first step has closed forms.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2110_02861_amd import workloads
+from tests.test_oracle_quant import exact_quantize_blockwise
+
+HP = dict(lr=1e-3, beta1=0.9, beta2=0.995, eps=1e-8)
+
+
+def torch_opt(name, p, lr, beta1, beta2, eps, wd):
+    if name == oracle.ADAM:
+        return torch.optim.Adam([p], lr=lr, betas=(beta1, beta2), eps=eps, weight_decay=wd,
+                                foreach=False)
+    if name == oracle.ADAMW:
+        return torch.optim.AdamW([p], lr=lr, betas=(beta1, beta2), eps=eps, weight_decay=wd,
+                                 foreach=False)
+    return torch.optim.SGD([p], lr=lr, momentum=beta1, dampening=0.0, weight_decay=wd,
+                           foreach=False)
+
+
+def close(a, b, lr):
+    """Param tolerance: |d| <= 1e-6 |ref| + 2^-20 lr."""
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return np.all(np.abs(a - b) <= 1e-6 * np.abs(b) + 2.0 ** -20 * lr)
+
+
+@pytest.mark.parametrize("opt,wd,gdt", [
+    (oracle.ADAM, 0.0, np.float32), (oracle.ADAM, 0.0, np.float16),
+    (oracle.ADAM, 1e-2, np.float32), (oracle.ADAMW, 1e-2, np.float16),
+    (oracle.MOMENTUM, 0.0, np.float32), (oracle.MOMENTUM, 1e-4, np.float32),
+])
+def test_step32_equals_torch_optim(opt, wd, gdt):
+    rng = np.random.default_rng(10)
+    n = 5000
+    lr = 0.1 if opt == oracle.MOMENTUM else HP["lr"]
+    w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    m = np.zeros(n, np.float32)
+    v = np.zeros(n, np.float32)
+    p = torch.nn.Parameter(torch.from_numpy(w.copy()))
+    o = torch_opt(opt, p, lr, HP["beta1"], HP["beta2"], HP["eps"], wd)
+    for t in range(1, 8):
+        g = (rng.standard_normal(n) * 1e-3).astype(gdt)
+        oracle.step32(opt, w, g, m, v, lr, HP["beta1"], HP["beta2"], HP["eps"], wd, t)
+        p.grad = torch.from_numpy(g.astype(np.float32))
+        o.step()
+        assert close(w, p.detach().numpy(), lr), (opt, t)
+        st = o.state[p]
+        key = "momentum_buffer" if opt == oracle.MOMENTUM else "exp_avg"
+        # torch orders the state arithmetic differently (lerp for exp_avg, addcmul
+        # for exp_avg_sq), so states agree to a few roundings per step, measured
+        # against the state's scale where b1*m and g cancel
+        mr = st[key].numpy()
+        np.testing.assert_allclose(m, mr, rtol=8e-6, atol=1e-6 * np.abs(mr).max())
+        if opt != oracle.MOMENTUM:
+            vr = st["exp_avg_sq"].numpy()
+            np.testing.assert_allclose(v, vr, rtol=8e-6, atol=1e-6 * np.abs(vr).max())
+
+
+def zero_state(n, B, opt):
+    nb = (n + B - 1) // B
+    c1 = np.full(n, 127, np.uint8)          # index of 0.0 in the signed map
+    a1 = np.zeros(nb, np.float32)
+    c2 = np.zeros(n, np.uint8)              # index of 0.0 in the unsigned map
+    a2 = np.zeros(nb, np.float32)
+    return c1, a1, c2, a2
+
+
+@pytest.fixture(scope="module")
+def maps():
+    return oracle.dynamic_codebook(0), oracle.dynamic_codebook(1)
+
+
+def test_step8_first_step_closed_form_adam(maps):
+    """t = 1 from zero state: mhat = g, vhat = g^2, so w1 = w0 - lr * g / (|g| + eps)."""
+    qs, qu = maps
+    rng = np.random.default_rng(11)
+    n, B = 5000, 256
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float16)
+    w = w0.copy()
+    c1, a1, c2, a2 = zero_state(n, B, oracle.ADAM)
+    oracle.step8(oracle.ADAM, B, w, g, c1, a1, qs, c2, a2, qu, **HP, wd=0.0, step=1)
+    g64 = g.astype(np.float64)
+    ref = w0 - HP["lr"] * g64 / (np.abs(g64) + HP["eps"])
+    assert close(w, ref, HP["lr"])
+    # the stored states are the block-wise quantization of (1-b1) g and (1-b2) g^2
+    # betas are binary32 inputs; 1 - beta is formed from them and rounded once
+    omb1 = np.float32(1.0 - float(np.float32(0.9)))
+    omb2 = np.float32(1.0 - float(np.float32(0.995)))
+    gf = g.astype(np.float32)
+    m1 = (omb1 * gf).astype(np.float32)
+    v1 = (omb2 * (gf * gf)).astype(np.float32)
+    ce, ae = exact_quantize_blockwise(qs, m1, B)
+    np.testing.assert_array_equal(c1, ce)
+    np.testing.assert_array_equal(a1, ae)
+    ce, ae = exact_quantize_blockwise(qu, v1, B)
+    np.testing.assert_array_equal(c2, ce)
+    np.testing.assert_array_equal(a2, ae)
+
+
+def test_step8_first_step_closed_form_adamw(maps):
+    qs, qu = maps
+    rng = np.random.default_rng(12)
+    n, B, wd = 3000, 512, 0.01
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    w = w0.copy()
+    c1, a1, c2, a2 = zero_state(n, B, oracle.ADAMW)
+    oracle.step8(oracle.ADAMW, B, w, g, c1, a1, qs, c2, a2, qu, **HP, wd=wd, step=1)
+    g64 = g.astype(np.float64)
+    ref = w0 * (1 - HP["lr"] * wd) - HP["lr"] * g64 / (np.abs(g64) + HP["eps"])
+    assert close(w, ref, HP["lr"])
+
+
+def test_step8_first_step_closed_form_momentum(maps):
+    """t = 1: m_0 = g_0 (Eq. 1), w1 = w0 - lr (g + wd w0)."""
+    qs, _ = maps
+    rng = np.random.default_rng(13)
+    n, B, lr, wd = 4097, 2048, 0.1, 1e-4
+    w0 = rng.standard_normal(n).astype(np.float32) * np.float32(0.05)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    w = w0.copy()
+    c1, a1, _, _ = zero_state(n, B, oracle.MOMENTUM)
+    oracle.step8(oracle.MOMENTUM, B, w, g, c1, a1, qs, None, None, None, lr, 0.9, 0.0, 0.0,
+                 wd, 1)
+    w64 = w0.astype(np.float64)
+    assert close(w, w64 - lr * (g + wd * w64), lr)
+    m1 = (g + np.float32(wd) * w0).astype(np.float32)
+    ce, ae = exact_quantize_blockwise(qs, m1, B)
+    assert np.count_nonzero(c1 != ce) <= 1
+    np.testing.assert_allclose(a1, ae, rtol=1e-6)
+
+
+@pytest.mark.parametrize("opt,wd,gdt,B", [
+    (oracle.ADAM, 0.0, np.float16, 256),
+    (oracle.ADAMW, 0.01, np.float16, 512),
+    (oracle.MOMENTUM, 1e-4, np.float32, 256),
+])
+def test_step8_equals_dequant_torch_requant(maps, opt, wd, gdt, B):
+    """8-bit step = dequantize -> torch.optim 32-bit update -> requantize.
+
+    torch updates exp_avg with a lerp rather than b1*m + (1-b1)*g, so a state
+    can differ by one rounding and sit on the other side of a code boundary:
+    codes must agree on >= 99.9% of elements and differ by at most 1.
+    """
+    qs, qu = maps
+    rng = np.random.default_rng(14)
+    n = 3 * B + 77
+    lr = 0.1 if opt == oracle.MOMENTUM else HP["lr"]
+    w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    c1, a1, c2, a2 = zero_state(n, B, opt)
+    for t in range(1, 5):
+        g = (rng.standard_normal(n) * 1e-3).astype(gdt)
+        # the reference update starts from the dequantized states
+        m_in = oracle.dequantize_blockwise(qs, c1, a1, B)
+        v_in = oracle.dequantize_blockwise(qu, c2, a2, B)
+        p = torch.nn.Parameter(torch.from_numpy(w.copy()))
+        o = torch_opt(opt, p, lr, HP["beta1"], HP["beta2"], HP["eps"], wd)
+        if opt == oracle.MOMENTUM:
+            o.state[p]["momentum_buffer"] = torch.from_numpy(m_in.copy()) if t > 1 else None
+        else:
+            o.state[p]["step"] = torch.tensor(float(t - 1))
+            o.state[p]["exp_avg"] = torch.from_numpy(m_in.copy())
+            o.state[p]["exp_avg_sq"] = torch.from_numpy(v_in.copy())
+        if opt == oracle.MOMENTUM and t == 1:
+            o.state[p].clear()
+        p.grad = torch.from_numpy(g.astype(np.float32))
+        o.step()
+        oracle.step8(opt, B, w, g, c1, a1, qs, c2, a2, qu, lr, HP["beta1"], HP["beta2"],
+                     HP["eps"], wd, t)
+        assert close(w, p.detach().numpy(), lr), t
+        key = "momentum_buffer" if opt == oracle.MOMENTUM else "exp_avg"
+        # absmax agrees to the few roundings by which torch's states differ
+        ce, ae = exact_quantize_blockwise(qs, o.state[p][key].numpy(), B)
+        np.testing.assert_allclose(a1, ae, rtol=4e-6)
+        d = np.abs(c1.astype(int) - ce.astype(int))
+        assert d.max() <= 1 and np.count_nonzero(d) <= max(1, n // 1000), t
+        if opt != oracle.MOMENTUM:
+            ce, ae = exact_quantize_blockwise(qu, o.state[p]["exp_avg_sq"].numpy(), B)
+            np.testing.assert_allclose(a2, ae, rtol=4e-6)
+            d = np.abs(c2.astype(int) - ce.astype(int))
+            assert d.max() <= 1 and np.count_nonzero(d) <= max(1, n // 1000), t
+
+
+def test_step8_thread_count_determinism(maps):
+    qs, qu = maps
+    spec = workloads.c1_specs()[0]
+    rng = workloads.host_rng(0, "c1")
+    w0 = workloads.init_param_host(spec, rng)[:300_000].copy()
+    outs = []
+    for nt in (1, 4):
+        w = w0.copy()
+        c1, a1, c2, a2 = zero_state(w.size, 2048, oracle.ADAM)
+        for t in range(1, 4):
+            g = workloads.grad_host("c1", spec, workloads.host_rng(0, "c1", 0, t))[:w.size].copy()
+            oracle.step8(oracle.ADAM, 2048, w, g, c1, a1, qs, c2, a2, qu, **HP, wd=0.0,
+                         step=t, nthreads=nt)
+        outs.append((w, c1, a1, c2, a2))
+    for x, y in zip(*outs):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_state_bytes_match_paper():
+    """Section 2.1: 32-bit Momentum / Adam states take 4 / 8 bytes per parameter
+    (4 GB / 8 GB per 1B parameters); 8-bit states take 1 / 2 GB.  Block-wise
+    absmax adds 4 bytes per block of 2048 per state."""
+    import json
+    import os
+    facts = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                        "paper_facts.json")))
+    n = 10 ** 9
+    B = facts["blocksize"]["value"]
+    for opt, nstates in (("momentum", 1), ("adam", 2)):
+        eight = nstates * (n + 4 * ((n + B - 1) // B))
+        want = facts["state_gb_per_1b_params_8bit"]["value"][opt]
+        assert abs(eight / 1e9 - want) / want < 0.005
+        assert nstates * 4 * n / 1e9 == facts["state_gb_per_1b_params_32bit"]["value"][opt]
