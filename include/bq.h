@@ -1,0 +1,155 @@
+/*
+ * bq.h - C ABI of libbq, 8-bit block-wise optimizers for AMD MI355X (gfx950).
+ *
+ * Implements the hot path of Dettmers, Lewis, Shleifer, Zettlemoyer,
+ * "8-bit Optimizers via Block-wise Quantization" (ICLR 2022):
+ *   - the dynamic (tree) quantization codebooks          (Sections 2.3, 3.2)
+ *   - block-wise quantization and dequantization         (Sections 2.2, 3.1, Eq. 3-4)
+ *   - the fused 8-bit Adam / AdamW / Momentum step       (Section 3, Eq. 1-2)
+ *
+ * Conventions shared by every call
+ *   - Pointers named "device" must point to GPU memory of the current HIP
+ *     device; host arrays are read or written only during the call.  The
+ *     caller owns all memory; the library keeps no pointer after returning and
+ *     allocates no device memory in these calls.
+ *   - A block covers flat elements [b*B, min((b+1)*B, n)) of one tensor, so a
+ *     tensor of n elements has ceil(n/B) blocks and its last block may be
+ *     partial.  Blocks never span tensors.
+ *   - blocksize B must be a power of two in [256, 4096] (the paper uses 2048).
+ *   - Element arrays (values, codes, params, grads, states) must be 16-byte
+ *     aligned; absmax arrays and codebooks 4-byte aligned.
+ *   - A codebook is 256 fp32 values in device memory, strictly increasing, so
+ *     that a code is the rank of its value, with every nonzero magnitude at
+ *     least 2^-60 (for such maps the division below is exact; see Eq. 4 note).
+ *   - Calls that take a stream are asynchronous and stream-ordered: they only
+ *     enqueue kernels on `stream` (0 = the null stream).  All argument checks
+ *     run before anything is enqueued, so on an error return nothing was
+ *     launched.  n == 0 (or ntensors == 0) is a no-op returning BQ_OK.
+ *   - Non-finite inputs are outside the contract.
+ */
+#ifndef BQ_H
+#define BQ_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum bq_status {
+    BQ_OK = 0,
+    BQ_ERR_NULL = 1,      /* a required pointer is NULL */
+    BQ_ERR_SIZE = 2,      /* negative n / numel / ntensors, or too large */
+    BQ_ERR_BLOCKSIZE = 3, /* blocksize not a power of two in [256, 4096] */
+    BQ_ERR_ENUM = 4,      /* unknown codebook kind or optimizer */
+    BQ_ERR_DTYPE = 5,     /* unknown gradient dtype */
+    BQ_ERR_ALIGN = 6,     /* a pointer violates the alignment rule above */
+    BQ_ERR_HIP = 7,       /* the HIP runtime reported an error at launch */
+    BQ_ERR_ARG = 8        /* a scalar argument is out of range (e.g. step < 1) */
+} bq_status;
+
+typedef enum bq_codebook_kind { BQ_SIGNED = 0, BQ_UNSIGNED = 1 } bq_codebook_kind;
+typedef enum bq_optimizer { BQ_ADAM = 0, BQ_ADAMW = 1, BQ_MOMENTUM = 2 } bq_optimizer;
+typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1 } bq_dtype;
+
+/*
+ * Build a 256-entry dynamic codebook on the host (synchronous, no GPU call).
+ * Section 2.3: after a sign bit, a run of E zero bits selects the decade
+ * 10^-E, a one bit ends the run and the remaining F bits are a linear fraction;
+ * Section 3.2: the unsigned map reuses the sign bit as a fraction bit.  Each
+ * decade holds the 2^F values 10^-E * (0.1 + 0.9 j / 2^F), j = 1..2^F, rounded
+ * once to fp32 (correctly rounded from the exact rational).
+ *   BQ_SIGNED:   E = 0..6, F = 6 - E, both signs (127 magnitudes each), plus 0
+ *                and +1e-7; -1 at code 0, 0 at code 127, +1 at code 255.
+ *   BQ_UNSIGNED: E = 0..7, F = 7 - E (255 magnitudes), plus 0 at code 0.
+ * out: host array of 256 floats, written in ascending order.
+ * Errors: BQ_ERR_NULL (out == NULL), BQ_ERR_ENUM (unknown kind).
+ */
+bq_status bq_make_dynamic_codebook(bq_codebook_kind kind, float out[256]);
+
+/*
+ * Block-wise quantization (Section 3.1, Eq. 4).  For each block b:
+ *   N_b = max_i |x_i|                              -> absmax[b]
+ *   code_i = argmin_j |qmap[j] - fl32(x_i / N_b)|  -> codes[i]
+ * where fl32(x/N) is the correctly rounded fp32 quotient, ties between two
+ * codes go to the lower index, and an all-zero block (N_b == 0) takes the code
+ * nearest to 0.
+ *   qmap   device, 256 fp32 (read)
+ *   x      device, n fp32 (read)
+ *   codes  device, n uint8 (written)
+ *   absmax device, ceil(n / blocksize) fp32 (written)
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE (n < 0), BQ_ERR_BLOCKSIZE, BQ_ERR_ALIGN,
+ * BQ_ERR_HIP.
+ */
+bq_status bq_quantize_blockwise(const float *qmap, const float *x, int64_t n,
+                                int32_t blocksize, uint8_t *codes, float *absmax,
+                                hipStream_t stream);
+
+/*
+ * Block-wise dequantization (Section 2.2): out_i = qmap[codes_i] * absmax[b],
+ * one fp32 multiply.
+ *   qmap   device, 256 fp32 (read)
+ *   codes  device, n uint8 (read)
+ *   absmax device, ceil(n / blocksize) fp32 (read)
+ *   out    device, n fp32 (written)
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_BLOCKSIZE, BQ_ERR_ALIGN, BQ_ERR_HIP.
+ */
+bq_status bq_dequantize_blockwise(const float *qmap, const uint8_t *codes,
+                                  const float *absmax, int64_t n, int32_t blocksize,
+                                  float *out, hipStream_t stream);
+
+/* One parameter tensor of the step; all pointers are device pointers. */
+typedef struct bq_tensor {
+    float *param;       /* numel fp32, updated in place */
+    const void *grad;   /* numel fp32 or fp16 (see grad_dtype), read only */
+    uint8_t *state1;    /* numel codes of the first state (m), in place */
+    uint8_t *state2;    /* numel codes of the second state (r); NULL for Momentum */
+    float *absmax1;     /* ceil(numel / B) block absmax of state 1, in place */
+    float *absmax2;     /* ceil(numel / B) block absmax of state 2; NULL for Momentum */
+    int64_t numel;
+} bq_tensor;
+
+/* Hyperparameters; step is t >= 1, incremented by the caller. */
+typedef struct bq_hparams {
+    float lr, beta1, beta2, eps, weight_decay;
+    int64_t step;
+} bq_hparams;
+
+/*
+ * The fused 8-bit optimizer step (Section 3, Fig. 1): for every block of every
+ * tensor, dequantize the states with the old absmax, apply the 32-bit update,
+ * take the new block absmax, and requantize each state to its nearest code
+ * (as bq_quantize_blockwise).  The param update uses the unquantized states.
+ *   Adam (Eq. 2, with bias correction):
+ *       g += wd * w   (only if weight_decay != 0)
+ *       m' = b1 m + (1 - b1) g;      r' = b2 r + (1 - b2) g^2
+ *       w' = w - (lr / (1 - b1^t)) * m' / (sqrt(r') / sqrt(1 - b2^t) + eps)
+ *   AdamW: w *= (1 - lr * wd) first, then Adam without the L2 term.
+ *   Momentum (Eq. 1): g += wd * w (if weight_decay != 0); m' = b1 m + g;
+ *       w' = w - lr m'  (beta2 and eps unused).
+ * State 1 uses qmap1 (the signed map), state 2 uses qmap2 (the unsigned map).
+ * A zero state is every code at the index of 0.0 with absmax 0.
+ *   tensors  host array of ntensors descriptors
+ *   hp       host pointer to the hyperparameters
+ *   qmap1    device, 256 fp32; qmap2 device, 256 fp32 (NULL for Momentum)
+ * Arithmetic of the states is fp32 in a fixed order without contraction, so
+ * codes and absmax are reproducible; the param update uses the hardware square
+ * root and reciprocal (relative error a few ulp of the update).
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_BLOCKSIZE, BQ_ERR_ENUM, BQ_ERR_DTYPE,
+ * BQ_ERR_ALIGN, BQ_ERR_ARG (hp->step < 1), BQ_ERR_HIP.
+ */
+bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                                const bq_tensor *tensors, int32_t ntensors,
+                                const bq_hparams *hp, const float *qmap1,
+                                const float *qmap2, hipStream_t stream);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char *bq_status_string(bq_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BQ_H */

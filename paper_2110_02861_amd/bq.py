@@ -1,0 +1,173 @@
+"""ctypes binding of libbq (include/bq.h), with the C names.
+
+Argument marshalling only: torch tensors are passed as device pointers and the
+current torch stream as the HIP stream; every step of the path runs in the HIP
+kernels of libbq.so.  There is no fallback: if the library is not built, or a
+call returns an error, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbq.so")
+
+BQ_OK, BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_BLOCKSIZE, BQ_ERR_ENUM = 0, 1, 2, 3, 4
+BQ_ERR_DTYPE, BQ_ERR_ALIGN, BQ_ERR_HIP, BQ_ERR_ARG = 5, 6, 7, 8
+BQ_SIGNED, BQ_UNSIGNED = 0, 1
+BQ_ADAM, BQ_ADAMW, BQ_MOMENTUM = 0, 1, 2
+BQ_F32, BQ_F16 = 0, 1
+OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM}
+
+EXPORTS = ("bq_make_dynamic_codebook", "bq_quantize_blockwise", "bq_dequantize_blockwise",
+           "bq_optimizer8bit_step", "bq_status_string")
+
+
+class BQError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+class bq_tensor(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("state1", ctypes.c_void_p), ("state2", ctypes.c_void_p),
+                ("absmax1", ctypes.c_void_p), ("absmax2", ctypes.c_void_p),
+                ("numel", ctypes.c_int64)]
+
+
+class bq_hparams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("step", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libbq.so (built by ``__graft_entry__.build()``); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m "
+                               "paper_2110_02861_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, I = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int
+        L.bq_make_dynamic_codebook.argtypes = [I, P]
+        L.bq_make_dynamic_codebook.restype = I
+        L.bq_quantize_blockwise.argtypes = [P, P, I64, I32, P, P, P]
+        L.bq_quantize_blockwise.restype = I
+        L.bq_dequantize_blockwise.argtypes = [P, P, P, I64, I32, P, P]
+        L.bq_dequantize_blockwise.restype = I
+        L.bq_optimizer8bit_step.argtypes = [I, I32, I, P, I32, P, P, P, P]
+        L.bq_optimizer8bit_step.restype = I
+        L.bq_status_string.argtypes = [I]
+        L.bq_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(s: int) -> str:
+    return lib().bq_status_string(int(s)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != BQ_OK:
+        raise BQError(status, where)
+
+
+def _dev_ptr(t, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU torch tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def bq_make_dynamic_codebook(kind: int) -> np.ndarray:
+    """Host call: the 256-entry signed (0) or unsigned (1) dynamic codebook."""
+    out = np.empty(256, np.float32)
+    _check(lib().bq_make_dynamic_codebook(int(kind), out.ctypes.data), "bq_make_dynamic_codebook")
+    return out
+
+
+def bq_quantize_blockwise(qmap, x, blocksize: int, codes=None, absmax=None, stream=None):
+    """codes (uint8, like x) and absmax (fp32, ceil(n/B)) of the GPU tensor x."""
+    import torch
+    n = x.numel()
+    if codes is None:
+        codes = torch.empty(n, dtype=torch.uint8, device=x.device)
+    if absmax is None:
+        absmax = torch.empty((n + blocksize - 1) // blocksize, dtype=torch.float32,
+                             device=x.device)
+    if x.dtype != torch.float32 or codes.dtype != torch.uint8 or absmax.dtype != torch.float32:
+        raise TypeError("x fp32, codes uint8, absmax fp32")
+    if codes.numel() < n or absmax.numel() < (n + blocksize - 1) // blocksize:
+        raise ValueError("output buffers too small")
+    _check(lib().bq_quantize_blockwise(_dev_ptr(qmap, "qmap"), _dev_ptr(x, "x"), n,
+                                       int(blocksize), _dev_ptr(codes, "codes"),
+                                       _dev_ptr(absmax, "absmax"), _stream(stream)),
+           "bq_quantize_blockwise")
+    return codes, absmax
+
+
+def bq_dequantize_blockwise(qmap, codes, absmax, blocksize: int, out=None, stream=None):
+    import torch
+    n = codes.numel()
+    if out is None:
+        out = torch.empty(n, dtype=torch.float32, device=codes.device)
+    if codes.dtype != torch.uint8 or absmax.dtype != torch.float32 or out.dtype != torch.float32:
+        raise TypeError("codes uint8, absmax fp32, out fp32")
+    if out.numel() < n or absmax.numel() < (n + blocksize - 1) // blocksize:
+        raise ValueError("buffers too small")
+    _check(lib().bq_dequantize_blockwise(_dev_ptr(qmap, "qmap"), _dev_ptr(codes, "codes"),
+                                         _dev_ptr(absmax, "absmax"), n, int(blocksize),
+                                         _dev_ptr(out, "out"), _stream(stream)),
+           "bq_dequantize_blockwise")
+    return out
+
+
+def make_tensor_array(tensors):
+    """Pack (param, grad, state1, state2, absmax1, absmax2) tuples of GPU
+    tensors (state2 / absmax2 may be None) into a ctypes bq_tensor array."""
+    arr = (bq_tensor * max(1, len(tensors)))()
+    for i, (p, g, s1, s2, a1, a2) in enumerate(tensors):
+        arr[i].param = _dev_ptr(p, "param")
+        arr[i].grad = _dev_ptr(g, "grad")
+        arr[i].state1 = _dev_ptr(s1, "state1")
+        arr[i].state2 = None if s2 is None else _dev_ptr(s2, "state2")
+        arr[i].absmax1 = _dev_ptr(a1, "absmax1")
+        arr[i].absmax2 = None if a2 is None else _dev_ptr(a2, "absmax2")
+        arr[i].numel = p.numel()
+    return arr
+
+
+def bq_optimizer8bit_step(opt, blocksize: int, grad_dtype: int, tensors, hp: dict, qmap1,
+                          qmap2=None, stream=None):
+    """One fused 8-bit step over a list of tensors (see make_tensor_array), or
+    over a prebuilt ``(bq_tensor array, count)`` pair."""
+    if isinstance(opt, str):
+        opt = OPTIMIZERS[opt]
+    if isinstance(tensors, tuple) and len(tensors) == 2 and isinstance(tensors[1], int):
+        arr, count = tensors
+    else:
+        arr, count = make_tensor_array(tensors), len(tensors)
+    h = bq_hparams(hp["lr"], hp["beta1"], hp.get("beta2", 0.0), hp.get("eps", 0.0),
+                   hp.get("wd", hp.get("weight_decay", 0.0)), int(hp["step"]))
+    _check(lib().bq_optimizer8bit_step(int(opt), int(blocksize), int(grad_dtype), arr, count,
+                                       ctypes.byref(h), _dev_ptr(qmap1, "qmap1"),
+                                       None if qmap2 is None else _dev_ptr(qmap2, "qmap2"),
+                                       _stream(stream)),
+           "bq_optimizer8bit_step")

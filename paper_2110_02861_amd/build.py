@@ -1,0 +1,60 @@
+"""Build libbq.so in-tree with hipcc for gfx950.
+
+    python -m paper_2110_02861_amd.build          # build
+    python -m paper_2110_02861_amd.build --asm    # also write gfx950 assembly
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+LIB = os.path.join(PKG, "libbq.so")
+SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_kernels.hip"]
+ARCH = "gfx950"
+
+# -ffp-contract=off: the state arithmetic must not be fused into fma, so that it
+# rounds exactly as its definition.  Packed fp32 instructions are disabled.
+# Correctly rounded fp32 division stays on (the HIP default).
+FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
+    "-ffp-contract=off",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+]
+
+
+def hipcc() -> str:
+    for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", "hipcc"):
+        if c and (os.path.sep not in c or os.path.exists(c)):
+            return c
+    raise RuntimeError("hipcc not found")
+
+
+def build(verbose: bool = False) -> str:
+    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    tmp = LIB + ".tmp"
+    cmd = [hipcc(), *FLAGS, "-shared", "-o", tmp, *srcs]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+def build_asm(out_dir: str) -> None:
+    """Write the device assembly of the kernels (for inspection only)."""
+    os.makedirs(out_dir, exist_ok=True)
+    src = os.path.join(CSRC, "bq_kernels.hip")
+    cmd = [hipcc(), *FLAGS, "--cuda-device-only", "-S", "-o",
+           os.path.join(out_dir, "bq_kernels.s"), src]
+    subprocess.run(cmd, check=True)
+
+
+if __name__ == "__main__":
+    build(verbose=True)
+    if "--asm" in sys.argv:
+        build_asm(os.path.join(ROOT, "_work", "asm"))

@@ -1,0 +1,198 @@
+// C-ABI entry points of libbq (declared in include/bq.h): argument checks,
+// per-step scalar precomputation, and packing of tensor descriptors into
+// kernel-argument chunks.  Every check runs before the first HIP call, so an
+// error return means nothing was enqueued.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "bq.h"
+#include "bq_internal.h"
+
+namespace {
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool valid_blocksize(int32_t b) { return b >= 256 && b <= 4096 && (b & (b - 1)) == 0; }
+
+// beta^t in double by right-to-left binary exponentiation.
+double beta_pow(double beta, int64_t t)
+{
+    double acc = 1.0;
+    for (double sq = beta; t > 0; t >>= 1, sq *= sq)
+        if (t & 1)
+            acc *= sq;
+    return acc;
+}
+
+// Bias-corrected Adam (the paper's Eq. 2 omits the correction constants),
+// decoupled AdamW decay, and the L2 weight-decay term; each scalar is formed in
+// double from the fp32 inputs and rounded once to fp32.
+bq::StepScalars make_scalars(const bq_hparams &hp)
+{
+    const double lr = hp.lr, b1 = hp.beta1, b2 = hp.beta2, wd = hp.weight_decay;
+    bq::StepScalars s;
+    s.b1 = hp.beta1;
+    s.omb1 = static_cast<float>(1.0 - b1);
+    s.b2 = hp.beta2;
+    s.omb2 = static_cast<float>(1.0 - b2);
+    s.eps = hp.eps;
+    s.lr = hp.lr;
+    s.wd = hp.weight_decay;
+    s.step_size = static_cast<float>(lr / (1.0 - beta_pow(b1, hp.step)));
+    s.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - beta_pow(b2, hp.step)));
+    s.decay = static_cast<float>(1.0 - lr * wd);
+    return s;
+}
+
+bq_status from_hip(hipError_t e) { return e == hipSuccess ? BQ_OK : BQ_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char *bq_status_string(bq_status s)
+{
+    switch (s) {
+    case BQ_OK: return "ok";
+    case BQ_ERR_NULL: return "required pointer is NULL";
+    case BQ_ERR_SIZE: return "size out of range";
+    case BQ_ERR_BLOCKSIZE: return "blocksize must be a power of two in [256, 4096]";
+    case BQ_ERR_ENUM: return "unknown codebook kind or optimizer";
+    case BQ_ERR_DTYPE: return "unknown gradient dtype";
+    case BQ_ERR_ALIGN: return "pointer misaligned (elements 16 B, absmax and codebook 4 B)";
+    case BQ_ERR_HIP: return "HIP runtime error";
+    case BQ_ERR_ARG: return "scalar argument out of range";
+    }
+    return "unknown status";
+}
+
+bq_status bq_make_dynamic_codebook(bq_codebook_kind kind, float out[256])
+{
+    if (out == nullptr)
+        return BQ_ERR_NULL;
+    if (kind != BQ_SIGNED && kind != BQ_UNSIGNED)
+        return BQ_ERR_ENUM;
+    return bq::build_dynamic_codebook(static_cast<int>(kind), out) == 0 ? BQ_OK : BQ_ERR_ENUM;
+}
+
+bq_status bq_quantize_blockwise(const float *qmap, const float *x, int64_t n, int32_t blocksize,
+                                uint8_t *codes, float *absmax, hipStream_t stream)
+{
+    if (n < 0)
+        return BQ_ERR_SIZE;
+    if (!valid_blocksize(blocksize))
+        return BQ_ERR_BLOCKSIZE;
+    if (n == 0)
+        return BQ_OK;
+    if (!qmap || !x || !codes || !absmax)
+        return BQ_ERR_NULL;
+    if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(absmax, 4) || !aligned(qmap, 4))
+        return BQ_ERR_ALIGN;
+    return from_hip(bq::launch_quantize(qmap, x, n, blocksize, codes, absmax, stream));
+}
+
+bq_status bq_dequantize_blockwise(const float *qmap, const uint8_t *codes, const float *absmax,
+                                  int64_t n, int32_t blocksize, float *out, hipStream_t stream)
+{
+    if (n < 0)
+        return BQ_ERR_SIZE;
+    if (!valid_blocksize(blocksize))
+        return BQ_ERR_BLOCKSIZE;
+    if (n == 0)
+        return BQ_OK;
+    if (!qmap || !codes || !absmax || !out)
+        return BQ_ERR_NULL;
+    if (!aligned(codes, 16) || !aligned(out, 16) || !aligned(absmax, 4) || !aligned(qmap, 4))
+        return BQ_ERR_ALIGN;
+    return from_hip(bq::launch_dequantize(qmap, codes, absmax, n, blocksize, out, stream));
+}
+
+bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                                const bq_tensor *tensors, int32_t ntensors,
+                                const bq_hparams *hp, const float *qmap1, const float *qmap2,
+                                hipStream_t stream)
+{
+    if (opt != BQ_ADAM && opt != BQ_ADAMW && opt != BQ_MOMENTUM)
+        return BQ_ERR_ENUM;
+    if (grad_dtype != BQ_F32 && grad_dtype != BQ_F16)
+        return BQ_ERR_DTYPE;
+    if (!valid_blocksize(blocksize))
+        return BQ_ERR_BLOCKSIZE;
+    if (ntensors < 0)
+        return BQ_ERR_SIZE;
+    if (ntensors == 0)
+        return BQ_OK;
+    if (!tensors || !hp || !qmap1)
+        return BQ_ERR_NULL;
+    const bool two = (opt != BQ_MOMENTUM);
+    if (two && !qmap2)
+        return BQ_ERR_NULL;
+    if (hp->step < 1)
+        return BQ_ERR_ARG;
+    if (!aligned(qmap1, 4) || (two && !aligned(qmap2, 4)))
+        return BQ_ERR_ALIGN;
+
+    const int64_t tile = bq::tile_elems(blocksize);
+    for (int32_t i = 0; i < ntensors; ++i) {
+        const bq_tensor &t = tensors[i];
+        if (t.numel < 0)
+            return BQ_ERR_SIZE;
+        // tiles of one launch are counted in int32
+        if (t.numel / tile >= (int64_t)INT32_MAX / 2)
+            return BQ_ERR_SIZE;
+        if (t.numel == 0)
+            continue;
+        if (!t.param || !t.grad || !t.state1 || !t.absmax1 ||
+            (two && (!t.state2 || !t.absmax2)))
+            return BQ_ERR_NULL;
+        if (!aligned(t.param, 16) || !aligned(t.grad, 16) || !aligned(t.state1, 16) ||
+            !aligned(t.absmax1, 4) ||
+            (two && (!aligned(t.state2, 16) || !aligned(t.absmax2, 4))))
+            return BQ_ERR_ALIGN;
+    }
+
+    bq::StepArgs args;
+    std::memset(&args, 0, sizeof(args));
+    args.q1 = qmap1;
+    args.q2 = two ? qmap2 : qmap1;
+    args.sc = make_scalars(*hp);
+    args.use_wd = (hp->weight_decay != 0.0f && opt != BQ_ADAMW) ? 1 : 0;
+
+    // Pack non-empty tensors into launches of at most kMaxDescPerLaunch
+    // descriptors, or fewer when a launch's tile count would overflow int32.
+    int32_t i = 0;
+    while (i < ntensors) {
+        int32_t k = 0;
+        int64_t tiles = 0;
+        for (; i < ntensors && k < bq::kMaxDescPerLaunch; ++i) {
+            const bq_tensor &t = tensors[i];
+            if (t.numel == 0)
+                continue;
+            const int64_t nt = (t.numel + tile - 1) / tile;
+            if (k > 0 && tiles + nt > (int64_t)INT32_MAX / 2)
+                break;
+            bq::TensorDesc &d = args.d[k++];
+            d.param = t.param;
+            d.grad = t.grad;
+            d.s1 = t.state1;
+            d.s2 = two ? t.state2 : nullptr;
+            d.a1 = t.absmax1;
+            d.a2 = two ? t.absmax2 : nullptr;
+            d.numel = t.numel;
+            d.tile_begin = tiles;
+            tiles += nt;
+        }
+        if (k == 0)
+            continue;
+        args.ntensors = k;
+        args.total_tiles = static_cast<int32_t>(tiles);
+        const hipError_t e = bq::launch_step(static_cast<int>(opt), static_cast<int>(grad_dtype),
+                                             blocksize, args, stream);
+        if (e != hipSuccess)
+            return BQ_ERR_HIP;
+    }
+    return BQ_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,66 @@
+// Internal declarations shared by the C-ABI layer (bq_api.cpp) and the HIP
+// kernels (bq_kernels.hip).  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace bq {
+
+// Per-step fp32 scalars, each formed in double on the host and rounded once.
+struct StepScalars {
+    float b1, omb1;        // beta1, 1 - beta1
+    float b2, omb2;        // beta2, 1 - beta2
+    float eps, lr, wd;
+    float step_size;       // lr / (1 - beta1^t)
+    float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
+    float decay;           // 1 - lr * wd  (AdamW)
+};
+
+// One tensor of a multi-tensor launch.  tile_begin is the index of the
+// tensor's first tile in the launch's flat tile list.
+struct TensorDesc {
+    float *param;
+    const void *grad;
+    uint8_t *s1;
+    uint8_t *s2;
+    float *a1;
+    float *a2;
+    int64_t numel;
+    int64_t tile_begin;
+};
+static_assert(sizeof(TensorDesc) == 64, "descriptor layout");
+
+// Descriptors travel by value in the kernel arguments; a launch carries at
+// most this many so that the argument block stays below 4 KiB.
+constexpr int kMaxDescPerLaunch = 56;
+
+struct StepArgs {
+    const float *q1;
+    const float *q2;
+    StepScalars sc;
+    int32_t ntensors;
+    int32_t total_tiles;
+    int32_t use_wd;        // L2 term for Adam / Momentum (weight_decay != 0)
+    int32_t pad;
+    TensorDesc d[kMaxDescPerLaunch];
+};
+static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must stay below 4 KiB");
+
+// Elements per tile (one workgroup iteration) for a given blocksize.
+constexpr int tile_elems(int blocksize) { return blocksize >= 2048 ? blocksize : 2048; }
+
+enum { kAdam = 0, kAdamW = 1, kMomentum = 2 };
+enum { kF32 = 0, kF16 = 1 };
+
+hipError_t launch_step(int opt, int grad_dtype, int blocksize, const StepArgs &args,
+                       hipStream_t stream);
+hipError_t launch_quantize(const float *qmap, const float *x, int64_t n, int blocksize,
+                           uint8_t *codes, float *absmax, hipStream_t stream);
+hipError_t launch_dequantize(const float *qmap, const uint8_t *codes, const float *absmax,
+                             int64_t n, int blocksize, float *out, hipStream_t stream);
+
+// Host-side codebook construction (bq_codebook.cpp).
+int build_dynamic_codebook(int kind, float out[256]);
+
+}  // namespace bq

@@ -1,0 +1,157 @@
+"""The C-ABI library without a GPU: symbols, the host codebook builder, and
+argument checks that must fail before any HIP call (nothing is enqueued).
+
+Every call below carries at least one invalid argument (or n == 0), so none of
+them reaches the HIP runtime; fake pointers are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2110_02861_amd import bq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+A16 = 0x10000          # a 16-byte aligned fake address, never dereferenced
+MIS = 0x10004          # 4-byte aligned, not 16-byte aligned
+
+
+@pytest.fixture(scope="module")
+def L():
+    return bq.lib()
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "bq.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(bq_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_exactly_the_exports():
+    assert header_functions() == sorted(bq.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in header_functions():
+        assert hasattr(L, name), name
+    # and no C++ mangled bq entry points leak as the public API
+    out = os.popen(f"nm -D --defined-only {bq.LIB_PATH}").read()
+    for name in header_functions():
+        assert re.search(rf"\bT {name}\b", out), name
+
+
+@pytest.mark.parametrize("kind", [bq.BQ_SIGNED, bq.BQ_UNSIGNED])
+def test_codebook_equals_oracle_bit_for_bit(kind):
+    got = bq.bq_make_dynamic_codebook(kind)
+    want = oracle.dynamic_codebook(kind)
+    np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_codebook_errors(L):
+    out = np.empty(256, np.float32)
+    assert L.bq_make_dynamic_codebook(2, out.ctypes.data) == bq.BQ_ERR_ENUM
+    assert L.bq_make_dynamic_codebook(0, None) == bq.BQ_ERR_NULL
+
+
+def test_status_strings(L):
+    for s in range(9):
+        assert len(bq.status_string(s)) > 0
+    assert bq.status_string(999) == "unknown status"
+
+
+def test_quantize_argument_checks(L):
+    q = L.bq_quantize_blockwise
+    assert q(A16, A16, -1, 2048, A16, A16, None) == bq.BQ_ERR_SIZE
+    for b in (0, 100, 128, 3000, 8192, -2048):
+        assert q(A16, A16, 10, b, A16, A16, None) == bq.BQ_ERR_BLOCKSIZE
+    assert q(None, A16, 10, 2048, A16, A16, None) == bq.BQ_ERR_NULL
+    assert q(A16, None, 10, 2048, A16, A16, None) == bq.BQ_ERR_NULL
+    assert q(A16, A16, 10, 2048, None, A16, None) == bq.BQ_ERR_NULL
+    assert q(A16, A16, 10, 2048, A16, None, None) == bq.BQ_ERR_NULL
+    assert q(A16, MIS, 10, 2048, A16, A16, None) == bq.BQ_ERR_ALIGN
+    assert q(A16, A16, 10, 2048, MIS, A16, None) == bq.BQ_ERR_ALIGN
+    assert q(A16, A16, 10, 2048, A16, A16 + 2, None) == bq.BQ_ERR_ALIGN
+    assert q(A16 + 1, A16, 10, 2048, A16, A16, None) == bq.BQ_ERR_ALIGN
+    # n == 0 is a no-op, even with NULL buffers
+    assert q(None, None, 0, 2048, None, None, None) == bq.BQ_OK
+
+
+def test_dequantize_argument_checks(L):
+    d = L.bq_dequantize_blockwise
+    assert d(A16, A16, A16, -5, 2048, A16, None) == bq.BQ_ERR_SIZE
+    assert d(A16, A16, A16, 5, 1000, A16, None) == bq.BQ_ERR_BLOCKSIZE
+    assert d(A16, None, A16, 5, 2048, A16, None) == bq.BQ_ERR_NULL
+    assert d(A16, A16, A16, 5, 2048, None, None) == bq.BQ_ERR_NULL
+    assert d(A16, MIS, A16, 5, 2048, A16, None) == bq.BQ_ERR_ALIGN
+    assert d(A16, A16, A16, 5, 2048, MIS, None) == bq.BQ_ERR_ALIGN
+    assert d(None, None, None, 0, 256, None, None) == bq.BQ_OK
+
+
+def _tensors(*rows):
+    arr = (bq.bq_tensor * len(rows))()
+    for i, r in enumerate(rows):
+        for k, v in r.items():
+            setattr(arr[i], k, v)
+    return arr
+
+
+def _good_row(n=100, two=True):
+    return dict(param=A16, grad=A16, state1=A16, state2=A16 if two else None, absmax1=A16,
+                absmax2=A16 if two else None, numel=n)
+
+
+def test_step_argument_checks(L):
+    s = L.bq_optimizer8bit_step
+    hp = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 1)
+    hp0 = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 0)
+    good = _tensors(_good_row())
+    H = ctypes.byref(hp)
+    assert s(3, 2048, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_ENUM
+    assert s(-1, 2048, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_ENUM
+    assert s(0, 2048, 2, good, 1, H, A16, A16, None) == bq.BQ_ERR_DTYPE
+    assert s(0, 1536, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_BLOCKSIZE
+    assert s(0, 2048, 0, good, -1, H, A16, A16, None) == bq.BQ_ERR_SIZE
+    assert s(0, 2048, 0, None, 1, H, A16, A16, None) == bq.BQ_ERR_NULL
+    assert s(0, 2048, 0, good, 1, None, A16, A16, None) == bq.BQ_ERR_NULL
+    assert s(0, 2048, 0, good, 1, H, None, A16, None) == bq.BQ_ERR_NULL
+    assert s(0, 2048, 0, good, 1, H, A16, None, None) == bq.BQ_ERR_NULL    # Adam needs qmap2
+    assert s(1, 2048, 0, good, 1, ctypes.byref(hp0), A16, A16, None) == bq.BQ_ERR_ARG
+    assert s(0, 2048, 0, good, 1, H, A16 + 2, A16, None) == bq.BQ_ERR_ALIGN
+    for field in ("param", "grad", "state1", "state2", "absmax1", "absmax2"):
+        row = _good_row()
+        row[field] = None
+        assert s(0, 2048, 1, _tensors(row), 1, H, A16, A16, None) == bq.BQ_ERR_NULL, field
+    for field, val in (("param", MIS), ("grad", MIS), ("state1", MIS), ("state2", MIS),
+                       ("absmax1", A16 + 2), ("absmax2", A16 + 1)):
+        row = _good_row()
+        row[field] = val
+        assert s(0, 2048, 1, _tensors(row), 1, H, A16, A16, None) == bq.BQ_ERR_ALIGN, field
+    row = _good_row()
+    row["numel"] = -3
+    assert s(0, 2048, 1, _tensors(row), 1, H, A16, A16, None) == bq.BQ_ERR_SIZE
+    # a bad tensor later in the list is still caught before anything is enqueued
+    assert s(2, 2048, 0, _tensors(_good_row(two=False), dict(_good_row(two=False), grad=None)),
+             2, H, A16, None, None) == bq.BQ_ERR_NULL
+    # empty work is a no-op: no tensors, or only empty tensors (NULL pointers allowed)
+    assert s(0, 2048, 0, None, 0, None, None, None, None) == bq.BQ_OK
+    empty = _tensors(dict(numel=0))
+    assert s(0, 2048, 0, empty, 1, H, A16, A16, None) == bq.BQ_OK
+
+
+def test_momentum_does_not_need_second_state(L):
+    s = L.bq_optimizer8bit_step
+    hp = bq.bq_hparams(0.1, 0.9, 0.0, 0.0, 1e-4, 1)
+    # second state and map absent is fine for Momentum; misaligned grad proves
+    # the call stops at validation and never launches
+    row = dict(_good_row(two=False), grad=MIS)
+    assert s(2, 2048, 0, _tensors(row), 1, ctypes.byref(hp), A16, None, None) == bq.BQ_ERR_ALIGN
+
+
+def test_product_path_has_no_fallback(monkeypatch, tmp_path):
+    """Without the built library the binding raises instead of computing."""
+    monkeypatch.setattr(bq, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(bq, "_lib", None)
+    with pytest.raises(RuntimeError):
+        bq.lib()

@@ -1,0 +1,112 @@
+"""GPU parity at full size: the GPT-2-medium-shaped list (AdamW, 354.8M params)
+and the 1.5B-parameter LM-shaped list (Adam), stepped in one call over every
+tensor (the configuration bench.py times).
+
+The oracle cannot step 1.5B parameters in seconds, but blocks are independent
+(Section 3.1: each block is normalized by its own absmax), so it steps a sample
+of blocks: the first and last (often partial) block of every tensor plus
+random blocks.  Their inputs are copied to the host before each GPU step; the
+oracle steps each sampled block on its own, and the GPU's bytes for those
+blocks must match: codes and absmax bit-exact, params within 1e-6 |w_ref| plus
+1e-6 of each step's update and one rounding of w, summed over the steps.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2110_02861_amd import bq, workloads
+from tests.gpu_helpers import OPT_ID, codebooks_on_device, host, needs_gpu, param_close, say
+
+import oracle
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+B = 2048
+
+
+def build_list(config, grad_dtype):
+    specs = workloads.SPECS[config]()
+    dev = torch.device("cuda")
+    tensors = []
+    for i, s in enumerate(specs):
+        n = s.numel
+        nb = (n + B - 1) // B
+        w = torch.empty(n, dtype=torch.float32, device=dev)
+        workloads.init_param_device(s, w, 0, config, i)
+        tensors.append(dict(
+            w=w, g=torch.empty(n, dtype=grad_dtype, device=dev),
+            c1=torch.full((n,), 127, dtype=torch.uint8, device=dev),
+            c2=torch.zeros(n, dtype=torch.uint8, device=dev),
+            a1=torch.zeros(nb, dtype=torch.float32, device=dev),
+            a2=torch.zeros(nb, dtype=torch.float32, device=dev)))
+    return specs, tensors
+
+
+def sample_blocks(specs, nrandom, seed):
+    rng = np.random.default_rng(seed)
+    picks = set()
+    for i, s in enumerate(specs):
+        nb = (s.numel + B - 1) // B
+        picks.add((i, 0))
+        picks.add((i, nb - 1))
+    sizes = np.array([(s.numel + B - 1) // B for s in specs])
+    cum = np.cumsum(sizes)
+    for r in rng.integers(0, cum[-1], nrandom):
+        i = int(np.searchsorted(cum, r, side="right"))
+        picks.add((i, int(r - (cum[i] - sizes[i]))))
+    return sorted(picks)
+
+
+def run_sampled(config, opt, steps, nrandom):
+    hp = {k: getattr(workloads, config.upper())[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
+    gdtype = workloads.GRADS[config][0]
+    tdt = torch.float16 if gdtype == "float16" else torch.float32
+    gflag = bq.BQ_F16 if gdtype == "float16" else bq.BQ_F32
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    say(f"{config}: allocating")
+    specs, T = build_list(config, tdt)
+    torch.cuda.synchronize()
+    arr = bq.make_tensor_array([(t["w"], t["g"], t["c1"], t["c2"], t["a1"], t["a2"]) for t in T])
+    picks = sample_blocks(specs, nrandom, seed=17)
+    hostb = {}
+    for (i, b) in picks:
+        s = slice(b * B, min((b + 1) * B, specs[i].numel))
+        hostb[(i, b)] = dict(w=host(T[i]["w"][s]).copy(),
+                             c1=np.full(s.stop - s.start, 127, np.uint8),
+                             c2=np.zeros(s.stop - s.start, np.uint8),
+                             a1=np.zeros(1, np.float32), a2=np.zeros(1, np.float32),
+                             tol=np.zeros(s.stop - s.start, np.float64))
+    for t in range(1, steps + 1):
+        say(f"{config}: generating grads t={t}")
+        for i, s in enumerate(specs):
+            workloads.grad_device(config, s, T[i]["g"], 0, i, t)
+        grads = {}
+        for (i, b) in picks:
+            s = slice(b * B, min((b + 1) * B, specs[i].numel))
+            grads[(i, b)] = host(T[i]["g"][s]).copy()
+        say(f"{config}: step t={t} over {len(specs)} tensors")
+        bq.bq_optimizer8bit_step(opt, B, gflag, (arr, len(specs)), dict(hp, step=t), qs_d, qu_d)
+        torch.cuda.synchronize()
+        for (i, b), hb in hostb.items():
+            prev = hb["w"].astype(np.float64)
+            oracle.step8(OPT_ID[opt], B, hb["w"], grads[(i, b)], hb["c1"], hb["a1"], qs,
+                         hb["c2"], hb["a2"], qu, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
+                         hp["wd"], t)
+            w64 = hb["w"].astype(np.float64)
+            hb["tol"] += 1e-6 * np.abs(prev - w64) + 2.0 ** -23 * np.abs(w64)
+            s = slice(b * B, min((b + 1) * B, specs[i].numel))
+            ok, worst = param_close(host(T[i]["w"][s]), hb["w"], hb["tol"])
+            assert ok, (config, t, specs[i].name, b, worst)
+            np.testing.assert_array_equal(host(T[i]["c1"][s]), hb["c1"])
+            np.testing.assert_array_equal(host(T[i]["c2"][s]), hb["c2"])
+            assert host(T[i]["a1"][b:b + 1])[0] == hb["a1"][0], (config, t, specs[i].name, b)
+            assert host(T[i]["a2"][b:b + 1])[0] == hb["a2"][0], (config, t, specs[i].name, b)
+    say(f"{config}: {len(picks)} sampled blocks matched over {steps} steps")
+
+
+def test_gpt2_medium_adamw_sampled():
+    run_sampled("c4", "adamw", steps=3, nrandom=256)
+
+
+def test_lm_1p5b_adam_sampled():
+    run_sampled("c5", "adam", steps=3, nrandom=512)

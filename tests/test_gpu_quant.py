@@ -1,0 +1,136 @@
+"""GPU parity: standalone block-wise quantize / dequantize vs the oracle.
+
+Codes and absmax must be bit-exact, and so must dequantized values (one fp32
+multiply of the looked-up code by the block absmax, Section 2.2).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2110_02861_amd import bq, workloads
+from tests.gpu_helpers import codebooks_on_device, dev, host, needs_gpu, say
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+BLOCKSIZES = [256, 512, 1024, 2048, 4096]
+
+
+def run_pair(qmap_h, qmap_d, x, B):
+    say(f"quantize n={x.size} B={B}")
+    c_d, a_d = bq.bq_quantize_blockwise(qmap_d, dev(x), B)
+    torch.cuda.synchronize()
+    c_ref, a_ref = oracle.quantize_blockwise(qmap_h, x, B)
+    np.testing.assert_array_equal(host(a_d).view(np.uint32), a_ref.view(np.uint32))
+    np.testing.assert_array_equal(host(c_d), c_ref)
+    say(f"dequantize n={x.size} B={B}")
+    out = bq.bq_dequantize_blockwise(qmap_d, c_d, a_d, B)
+    torch.cuda.synchronize()
+    ref = oracle.dequantize_blockwise(qmap_h, c_ref, a_ref, B)
+    np.testing.assert_array_equal(host(out).view(np.uint32), ref.view(np.uint32))
+
+
+@pytest.mark.parametrize("B", BLOCKSIZES)
+def test_ragged_multi_tile(B):
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    tile = max(B, 2048)
+    n = 7 * tile + 1234          # several tiles and a ragged tail
+    x = workloads.student_t_host(n, seed=B)
+    run_pair(qs, qs_d, x, B)
+    run_pair(qu, qu_d, np.abs(x), B)
+
+
+@pytest.mark.parametrize("n", [1, 7, 255, 256, 257, 2047, 2048, 2049, 4095, 4097, 10000])
+def test_edge_lengths(n):
+    qs, _, qs_d, _ = codebooks_on_device()
+    x = workloads.student_t_host(n, seed=n)
+    for B in (256, 2048, 4096):
+        run_pair(qs, qs_d, x, B)
+
+
+def test_ties_and_neighbours_exact():
+    """Values whose quotient by the absmax lands exactly on a midpoint of two
+    codes, and one ulp either side: ties go to the lower code (Eq. 3)."""
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    for q, q_d in ((qs, qs_d), (qu, qu_d)):
+        ys = []
+        for j in range(255):
+            m = np.float32((float(q[j]) + float(q[j + 1])) / 2.0)
+            ys += [np.nextafter(m, np.float32(-np.inf), dtype=np.float32), m,
+                   np.nextafter(m, np.float32(np.inf), dtype=np.float32)]
+        ys = np.array(ys, np.float32)
+        B = 2048
+        # block absmax 1 (and a scaled copy): one element fixes the absmax
+        for N in (np.float32(1.0), np.float32(0.375), np.float32(3.0e-3)):
+            blocks = []
+            for s in range(0, ys.size, B - 1):
+                chunk = (ys[s:s + B - 1] * N).astype(np.float32)
+                blk = np.zeros(B, np.float32)
+                blk[:chunk.size] = chunk
+                blk[-1] = N
+                blocks.append(blk)
+            run_pair(q, q_d, np.concatenate(blocks), B)
+
+
+def test_zero_blocks_and_signed_zero():
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    x = np.zeros(3 * 2048 + 5, np.float32)
+    x[2048:4096] = workloads.student_t_host(2048, seed=3)
+    x[100] = -0.0
+    for q, q_d in ((qs, qs_d), (qu, qu_d)):
+        run_pair(q, q_d, x, 2048)
+
+
+@pytest.mark.parametrize("scale", [2.0 ** -120, 2.0 ** -70, 2.0 ** -30, 1.0, 2.0 ** 40, 2.0 ** 90])
+def test_extreme_block_scales(scale):
+    """Blocks whose absmax needs the power-of-two rescaling of the divisor."""
+    qs, _, qs_d, _ = codebooks_on_device()
+    x = (workloads.student_t_host(3 * 2048, seed=5).astype(np.float64) * scale).astype(np.float32)
+    run_pair(qs, qs_d, x, 2048)
+
+
+def test_round_trip_every_code():
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    B = 256
+    codes = np.tile(np.arange(256, dtype=np.uint8), 8)
+    absmax = np.array([1.0, 0.37, 3e-5, 12345.678, 2.0 ** -70, 2.0 ** 70, 7.0, 1e-3], np.float32)
+    for q_d in (qs_d, qu_d):
+        say("round trip")
+        x = bq.bq_dequantize_blockwise(q_d, dev(codes), dev(absmax), B)
+        c2, a2 = bq.bq_quantize_blockwise(q_d, x, B)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(c2), codes)
+        np.testing.assert_array_equal(host(a2), absmax)
+
+
+@pytest.mark.parametrize("B", [2048, 4096])
+def test_full_size_student_t(B):
+    """67,108,864 Student-t(3) values scaled 1e-2, every code and absmax compared."""
+    qs, _, qs_d, _ = codebooks_on_device()
+    n = 67_108_864
+    x = workloads.student_t_host(n, seed=0)
+    say(f"full-size quantize n={n} B={B}")
+    x_d = dev(x)
+    c_d, a_d = bq.bq_quantize_blockwise(qs_d, x_d, B)
+    out_d = bq.bq_dequantize_blockwise(qs_d, c_d, a_d, B)
+    torch.cuda.synchronize()
+    c_ref, a_ref = oracle.quantize_blockwise(qs, x, B)
+    np.testing.assert_array_equal(host(a_d).view(np.uint32), a_ref.view(np.uint32))
+    np.testing.assert_array_equal(host(c_d), c_ref)
+    ref = oracle.dequantize_blockwise(qs, c_ref, a_ref, B)
+    np.testing.assert_array_equal(host(out_d).view(np.uint32), ref.view(np.uint32))
+
+
+def test_non_default_stream_ordering():
+    qs, _, qs_d, _ = codebooks_on_device()
+    x = workloads.student_t_host(5 * 2048 + 3, seed=9)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        x_d = dev(x)
+        say("quantize on a side stream")
+        c_d, a_d = bq.bq_quantize_blockwise(qs_d, x_d, 2048, stream=s)
+        out = bq.bq_dequantize_blockwise(qs_d, c_d, a_d, 2048, stream=s)
+    s.synchronize()
+    c_ref, a_ref = oracle.quantize_blockwise(qs, x, 2048)
+    np.testing.assert_array_equal(host(c_d), c_ref)
+    np.testing.assert_array_equal(host(out), oracle.dequantize_blockwise(qs, c_ref, a_ref, 2048))

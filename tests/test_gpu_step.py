@@ -1,0 +1,179 @@
+"""GPU parity: the fused 8-bit optimizer step vs the oracle.
+
+Both sides start from the same zero state and the same seeded gradients and
+run free: state codes and absmax must stay bit-exact (the state arithmetic is
+fp32 in the same order on both sides and the requantization is exact).  The
+HIP path takes the hardware square root and reciprocal in the param update
+only, a few ulp of the update: one step from one state must agree within
+1e-6 (|w_ref| + |update|); free-running params within 1e-6 |w_ref| plus those
+per-step update terms (and one rounding of w) summed over the steps.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2110_02861_amd import bq, workloads
+from tests.gpu_helpers import (DevState, HostState, codebooks_on_device, codes_agree, host,
+                               needs_gpu, param_close, say)
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+HPS = {
+    "adam": dict(lr=1e-3, beta1=0.9, beta2=0.995, eps=1e-8, wd=0.0),
+    "adamw": dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.01),
+    "momentum": dict(lr=0.1, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4),
+}
+
+
+def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=True):
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    two = opt != "momentum"
+    hp = dict(HPS[opt] if hp is None else hp)
+    tdt = torch.float16 if grad_dtype == bq.BQ_F16 else torch.float32
+    ndt = np.float16 if grad_dtype == bq.BQ_F16 else np.float32
+    hs, ds = [], []
+    for i, n in enumerate(sizes):
+        rng = np.random.default_rng([seed, i])
+        w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+        hs.append(HostState(w, B, two))
+        ds.append(DevState(w, B, two, tdt))
+    arr = bq.make_tensor_array([d.row() for d in ds])
+    for t in range(1, steps + 1):
+        grads = []
+        for i, n in enumerate(sizes):
+            rng = np.random.default_rng([seed, i, t])
+            g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+            g[rng.random(n) < 1e-3] *= 100.0
+            g = g.astype(ndt)
+            grads.append(g)
+            ds[i].g.copy_(torch.from_numpy(g))
+        say(f"step opt={opt} B={B} grad={ndt.__name__} tensors={len(sizes)} t={t}")
+        bq.bq_optimizer8bit_step(opt, B, grad_dtype, (arr, len(ds)), dict(hp, step=t),
+                                 qs_d, qu_d if two else None)
+        torch.cuda.synchronize()
+        for i in range(len(sizes)):
+            hs[i].step(opt, B, grads[i], qs, qu if two else None, hp, t)
+            ok, worst = param_close(host(ds[i].w), hs[i].w, hs[i].tol)
+            assert ok, (opt, B, t, i, worst)
+            pairs = [(ds[i].c1, ds[i].a1, hs[i].c1, hs[i].a1)]
+            if two:
+                pairs.append((ds[i].c2, ds[i].a2, hs[i].c2, hs[i].a2))
+            for cd, ad, ch, ah in pairs:
+                if exact_codes:
+                    np.testing.assert_array_equal(host(ad).view(np.uint32), ah.view(np.uint32))
+                    np.testing.assert_array_equal(host(cd), ch)
+                else:
+                    np.testing.assert_allclose(host(ad), ah, rtol=1e-6, atol=0)
+                    ok, frac, mx = codes_agree(host(cd), ch)
+                    assert ok, (opt, B, t, i, frac, mx)
+
+
+RAGGED = [1, 255, 256, 257, 2047, 2048, 2049, 4095, 4096, 4097, 3 * 4096 + 77, 20000]
+
+
+@pytest.mark.parametrize("opt", ["adam", "adamw", "momentum"])
+@pytest.mark.parametrize("grad_dtype", [bq.BQ_F16, bq.BQ_F32])
+@pytest.mark.parametrize("B", [256, 512, 1024, 2048, 4096])
+def test_ragged_list(opt, grad_dtype, B):
+    run_lists(opt, B, grad_dtype, RAGGED, steps=3)
+
+
+def test_adam_l2_weight_decay():
+    """Adam's L2 term feeds the param into the gradient, so a param that differs
+    by an ulp (hardware sqrt / reciprocal) can move a state across a code
+    boundary: codes agree on >= 99.99% and differ by at most one."""
+    hp = dict(HPS["adam"], wd=1e-2)
+    run_lists("adam", 2048, bq.BQ_F16, RAGGED, steps=3, hp=hp, exact_codes=False)
+
+
+def test_c1_adam_ten_steps():
+    """One fp32 tensor of 1,048,576 params, fp16 grads, Adam, 10 steps from zero.
+
+    Free-running: both sides chain their own steps; codes and absmax stay
+    bit-exact, params within the per-step bounds summed over the steps.
+    Per step: before each GPU step a second GPU copy is loaded with the
+    oracle's state, so that step alone is held to the one-step bound."""
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    spec = workloads.c1_specs()[0]
+    hp = {k: workloads.C1[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
+    w = workloads.init_param_host(spec, workloads.host_rng(0, "c1"))
+    h = HostState(w, 2048, True)
+    d = DevState(w, 2048, True, torch.float16)
+    f = DevState(w, 2048, True, torch.float16)
+    arr_d = bq.make_tensor_array([d.row()])
+    arr_f = bq.make_tensor_array([f.row()])
+    for t in range(1, 11):
+        g = workloads.grad_host("c1", spec, workloads.host_rng(0, "c1", 0, t))
+        d.g.copy_(torch.from_numpy(g))
+        f.g.copy_(torch.from_numpy(g))
+        f.load(h)
+        say(f"C1 step t={t}")
+        bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F16, (arr_d, 1), dict(hp, step=t), qs_d, qu_d)
+        bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F16, (arr_f, 1), dict(hp, step=t), qs_d, qu_d)
+        torch.cuda.synchronize()
+        h.step("adam", 2048, g, qs, qu, hp, t)
+        for dev_state, tol, kind in ((d, h.tol, "free"), (f, h.step_tol, "one step")):
+            ok, worst = param_close(host(dev_state.w), h.w, tol)
+            assert ok, (t, kind, worst)
+            np.testing.assert_array_equal(host(dev_state.c1), h.c1)
+            np.testing.assert_array_equal(host(dev_state.c2), h.c2)
+            np.testing.assert_array_equal(host(dev_state.a1), h.a1)
+            np.testing.assert_array_equal(host(dev_state.a2), h.a2)
+
+
+def test_many_tensors_chunked_launches():
+    """More tensors than one launch's descriptor capacity (56)."""
+    sizes = [64 * (i % 7 + 1) + (i * 37) % 2048 for i in range(150)]
+    run_lists("adam", 2048, bq.BQ_F16, sizes, steps=2, seed=3)
+
+
+def test_resnet50_momentum_list():
+    """161 ResNet-50 tensors (99 smaller than one block), fp32 grads, Momentum."""
+    sizes = [s.numel for s in workloads.resnet50_specs()]
+    run_lists("momentum", 2048, bq.BQ_F32, sizes, steps=3, seed=4)
+
+
+def test_zero_gradient_keeps_zero_state():
+    """A zero gradient on a zero state leaves codes at the zero code and absmax 0."""
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    w = np.linspace(-1, 1, 5000).astype(np.float32)
+    d = DevState(w, 2048, True, torch.float32)
+    d.g.zero_()
+    say("zero gradient step")
+    bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F32, [d.row()], dict(HPS["adam"], step=1),
+                             qs_d, qu_d)
+    torch.cuda.synchronize()
+    assert np.all(host(d.c1) == 127) and np.all(host(d.c2) == 0)
+    assert np.all(host(d.a1) == 0) and np.all(host(d.a2) == 0)
+    np.testing.assert_array_equal(host(d.w), w)
+
+
+def test_determinism_and_resume():
+    """Two runs give identical bytes, and 2 + 2 steps with the state copied out
+    and back in equal 4 straight steps (checkpoint / resume)."""
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    rng = np.random.default_rng(7)
+    n = 3 * 2048 + 11
+    w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    gs = [(rng.standard_normal(n) * 1e-3).astype(np.float16) for _ in range(4)]
+
+    def run(states, t0, t1):
+        arr = bq.make_tensor_array([states.row()])
+        for t in range(t0, t1):
+            states.g.copy_(torch.from_numpy(gs[t - 1]))
+            say(f"resume run t={t}")
+            bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F16, (arr, 1),
+                                     dict(HPS["adam"], step=t), qs_d, qu_d)
+        torch.cuda.synchronize()
+
+    a = DevState(w, 2048, True, torch.float16)
+    run(a, 1, 5)
+    b = DevState(w, 2048, True, torch.float16)
+    run(b, 1, 3)
+    saved = [x.clone().cpu() for x in (b.w, b.c1, b.c2, b.a1, b.a2)]
+    c = DevState(w * 0, 2048, True, torch.float16)
+    for dst, src in zip((c.w, c.c1, c.c2, c.a1, c.a2), saved):
+        dst.copy_(src)
+    run(c, 3, 5)
+    for x, y in zip((a.w, a.c1, a.c2, a.a1, a.a2), (c.w, c.c1, c.c2, c.a1, c.a2)):
+        assert torch.equal(x, y)
