@@ -1,8 +1,11 @@
 """Benchmark: fused 8-bit Adam step on the 1.5B-parameter LM-shaped list.
 
-One step = one call of the fused 8-bit optimizer step over every tensor of the
-list (dequantize states, fp32 Adam update, block absmax, requantize), with the
-params, fp16 grads and 8-bit states already resident in HBM.
+One step = one run of the fused 8-bit optimizer step over every tensor of the
+list (prepare both codebooks' decision tables, then dequantize states, fp32
+Adam update, block absmax, requantize), with the params, fp16 grads and 8-bit
+states already resident in HBM.  By default the step goes through a step plan
+(bq_step_plan_run: one launch over all 580 tensors); --path call uses
+bq_optimizer8bit_step.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 
@@ -60,12 +63,9 @@ def setup_c5(torch, bq, workloads, seed=0):
                        torch.zeros(nb, dtype=torch.float32, device=dev),
                        torch.zeros(nb, dtype=torch.float32, device=dev)))
     torch.cuda.synchronize()
-    arrays = []
-    for r in range(2):
-        rows = [(params[i], grads[r][i], states[i][0], states[i][1], states[i][2], states[i][3])
-                for i in range(len(specs))]
-        arrays.append((bq.make_tensor_array(rows), len(rows)))
-    return specs, params, grads, states, arrays
+    rows = [[(params[i], grads[r][i], states[i][0], states[i][1], states[i][2], states[i][3])
+             for i in range(len(specs))] for r in range(2)]
+    return specs, params, grads, states, rows
 
 
 def cpu_baseline(specs, params, grads, layers):
@@ -116,6 +116,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=8)
+    ap.add_argument("--path", choices=["plan", "call"], default="plan",
+                    help="plan: bq_step_plan_run (one launch over all 580 tensors); "
+                         "call: bq_optimizer8bit_step (descriptor chunks of 56 tensors)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the 8-bit step has no cross-GPU exchange, and "
@@ -129,7 +132,7 @@ def main():
     qs_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)).cuda()
     qu_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)).cuda()
     log("allocating the 1.5B-parameter list")
-    specs, params, grads, states, arrays = setup_c5(torch, bq, workloads)
+    specs, params, grads, states, rows = setup_c5(torch, bq, workloads)
     numels = [s.numel for s in specs]
     nparams = sum(numels)
     bytes_step = step_bytes(numels, BLOCKSIZE, 2, 2)
@@ -143,9 +146,18 @@ def main():
 
     stream = torch.cuda.current_stream()
 
-    def step(t):
-        bq.bq_optimizer8bit_step(bq.BQ_ADAM, BLOCKSIZE, bq.BQ_F16, arrays[t % 2],
-                                 dict(hp, step=t), qs_d, qu_d, stream=stream)
+    # a ring of two gradient buffers, one plan (or descriptor array) for each
+    if args.path == "plan":
+        plans = [bq.StepPlan(bq.BQ_ADAM, BLOCKSIZE, bq.BQ_F16, r) for r in rows]
+
+        def step(t):
+            plans[t % 2].run(dict(hp, step=t), qs_d, qu_d, stream=stream)
+    else:
+        arrays = [(bq.make_tensor_array(r), len(r)) for r in rows]
+
+        def step(t):
+            bq.bq_optimizer8bit_step(bq.BQ_ADAM, BLOCKSIZE, bq.BQ_F16, arrays[t % 2],
+                                     dict(hp, step=t), qs_d, qu_d, stream=stream)
 
     log(f"warmup {args.warmup} steps")
     t = 1
@@ -183,7 +195,7 @@ def main():
                         "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4) "
                         "with 0.01% outliers x1000, blocksize 2048",
             "tensors": len(specs), "params": nparams, "blocksize": BLOCKSIZE,
-            "grad_dtype": "fp16", "state_dtype": "u8",
+            "grad_dtype": "fp16", "state_dtype": "u8", "path": args.path,
         },
         "gbs": gbs,
         "hbm_frac": gbs / HBM_PEAK_GBS,

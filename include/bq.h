@@ -11,7 +11,8 @@
  *   - Pointers named "device" must point to GPU memory of the current HIP
  *     device; host arrays are read or written only during the call.  The
  *     caller owns all memory; the library keeps no pointer after returning and
- *     allocates no device memory in these calls.
+ *     allocates no device memory, except bq_step_plan_create (a plan owns the
+ *     device copy of its descriptors until bq_step_plan_destroy).
  *   - A block covers flat elements [b*B, min((b+1)*B, n)) of one tensor, so a
  *     tensor of n elements has ceil(n/B) blocks and its last block may be
  *     partial.  Blocks never span tensors.
@@ -129,7 +130,8 @@ typedef struct bq_hparams {
  *   AdamW: w *= (1 - lr * wd) first, then Adam without the L2 term.
  *   Momentum (Eq. 1): g += wd * w (if weight_decay != 0); m' = b1 m + g;
  *       w' = w - lr m'  (beta2 and eps unused).
- * State 1 uses qmap1 (the signed map), state 2 uses qmap2 (the unsigned map).
+ * State 1 uses qmap1 (the signed map), state 2 uses qmap2 (the unsigned map;
+ * any map for state 2 must have no negative entries, so that r' >= 0).
  * A zero state is every code at the index of 0.0 with absmax 0.
  *   tensors  host array of ntensors descriptors
  *   hp       host pointer to the hyperparameters
@@ -144,6 +146,73 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
                                 const bq_tensor *tensors, int32_t ntensors,
                                 const bq_hparams *hp, const float *qmap1,
                                 const float *qmap2, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Prepared codebooks and step plans: the fast path.
+ *
+ * The calls above build a codebook's decision tables inside every persistent
+ * workgroup, because they receive nothing but the raw map.  The calls below
+ * keep those tables in caller-visible device memory, so that every block can
+ * run as its own short-lived workgroup (512 threads, one tile of 2048
+ * elements or one 4096 block), which streams HBM markedly faster on MI355X.
+ * Results are identical to the calls above, bit for bit.
+ * ------------------------------------------------------------------------ */
+
+/* Bytes of device memory one prepared codebook occupies (16-byte aligned). */
+#define BQ_PREPARED_CODEBOOK_BYTES 8720
+
+/*
+ * Build the decision tables of codebook qmap (256 fp32, device) into
+ * `prepared` (device, BQ_PREPARED_CODEBOOK_BYTES, 16-byte aligned, owned by the
+ * caller): the map itself, the thresholds halfway between adjacent codes
+ * (Eq. 3's argmin boundaries) and a bucket index over fp32 bit patterns.
+ * Stream-ordered; re-run it whenever qmap's contents change.
+ * Errors: BQ_ERR_NULL, BQ_ERR_ALIGN, BQ_ERR_HIP.
+ */
+bq_status bq_prepare_codebook(const float *qmap, void *prepared, hipStream_t stream);
+
+/*
+ * bq_quantize_blockwise with a prepared codebook (Section 3.1, Eq. 4); same
+ * arguments and results, one workgroup per tile.
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE (n < 0, or more than 8,388,607 tiles),
+ * BQ_ERR_BLOCKSIZE, BQ_ERR_ALIGN, BQ_ERR_HIP.
+ */
+bq_status bq_quantize_blockwise_prepared(const void *prepared, const float *x, int64_t n,
+                                         int32_t blocksize, uint8_t *codes, float *absmax,
+                                         hipStream_t stream);
+
+/* Opaque multi-tensor step plan. */
+typedef struct bq_step_plan_s *bq_step_plan;
+
+/*
+ * Create a plan for the fused 8-bit step (Section 3, Fig. 1) over a fixed
+ * tensor list.  This is the only allocating call: it copies the descriptors
+ * and a tile-to-tensor map (4 bytes per tile of 2048 elements) to device
+ * memory of the current device and reserves space for two prepared codebooks.
+ * Synchronous.  The tensors' buffers must stay valid while the plan is used.
+ *   tensors  host array of ntensors descriptors (as bq_optimizer8bit_step)
+ *   plan     receives the handle (NULL on error)
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE (more than 8,388,607 tiles in total),
+ * BQ_ERR_BLOCKSIZE, BQ_ERR_ENUM, BQ_ERR_DTYPE, BQ_ERR_ALIGN, BQ_ERR_HIP.
+ */
+bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                              const bq_tensor *tensors, int32_t ntensors, bq_step_plan *plan);
+
+/*
+ * One step of the plan's optimizer over all its tensors, as
+ * bq_optimizer8bit_step with the same hyperparameters and codebooks: one
+ * launch that prepares both codebooks, then one launch over every tile of
+ * every tensor.  Allocates nothing.  Must be called with the plan's device
+ * current (else BQ_ERR_ARG).  A plan holds one codebook workspace: runs of one
+ * plan on different streams must not overlap.
+ * Errors: BQ_ERR_NULL, BQ_ERR_ALIGN, BQ_ERR_ARG (step < 1, wrong device),
+ * BQ_ERR_HIP.
+ */
+bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float *qmap1,
+                           const float *qmap2, hipStream_t stream);
+
+/* Free a plan's device memory (synchronizes with the device).  NULL is a no-op. */
+bq_status bq_step_plan_destroy(bq_step_plan plan);
 
 /* Static, human-readable name of a status code (never NULL). */
 const char *bq_status_string(bq_status s);

@@ -23,7 +23,10 @@ BQ_F32, BQ_F16 = 0, 1
 OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM}
 
 EXPORTS = ("bq_make_dynamic_codebook", "bq_quantize_blockwise", "bq_dequantize_blockwise",
-           "bq_optimizer8bit_step", "bq_status_string")
+           "bq_optimizer8bit_step", "bq_prepare_codebook", "bq_quantize_blockwise_prepared",
+           "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_destroy",
+           "bq_status_string")
+BQ_PREPARED_CODEBOOK_BYTES = 8720
 
 
 class BQError(RuntimeError):
@@ -65,6 +68,16 @@ def lib() -> ctypes.CDLL:
         L.bq_dequantize_blockwise.restype = I
         L.bq_optimizer8bit_step.argtypes = [I, I32, I, P, I32, P, P, P, P]
         L.bq_optimizer8bit_step.restype = I
+        L.bq_prepare_codebook.argtypes = [P, P, P]
+        L.bq_prepare_codebook.restype = I
+        L.bq_quantize_blockwise_prepared.argtypes = [P, P, I64, I32, P, P, P]
+        L.bq_quantize_blockwise_prepared.restype = I
+        L.bq_step_plan_create.argtypes = [I, I32, I, P, I32, ctypes.POINTER(ctypes.c_void_p)]
+        L.bq_step_plan_create.restype = I
+        L.bq_step_plan_run.argtypes = [P, P, P, P, P]
+        L.bq_step_plan_run.restype = I
+        L.bq_step_plan_destroy.argtypes = [P]
+        L.bq_step_plan_destroy.restype = I
         L.bq_status_string.argtypes = [I]
         L.bq_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -164,10 +177,94 @@ def bq_optimizer8bit_step(opt, blocksize: int, grad_dtype: int, tensors, hp: dic
         arr, count = tensors
     else:
         arr, count = make_tensor_array(tensors), len(tensors)
-    h = bq_hparams(hp["lr"], hp["beta1"], hp.get("beta2", 0.0), hp.get("eps", 0.0),
-                   hp.get("wd", hp.get("weight_decay", 0.0)), int(hp["step"]))
+    h = _hparams(hp)
     _check(lib().bq_optimizer8bit_step(int(opt), int(blocksize), int(grad_dtype), arr, count,
                                        ctypes.byref(h), _dev_ptr(qmap1, "qmap1"),
                                        None if qmap2 is None else _dev_ptr(qmap2, "qmap2"),
                                        _stream(stream)),
            "bq_optimizer8bit_step")
+
+
+def _hparams(hp: dict) -> bq_hparams:
+    return bq_hparams(hp["lr"], hp["beta1"], hp.get("beta2", 0.0), hp.get("eps", 0.0),
+                      hp.get("wd", hp.get("weight_decay", 0.0)), int(hp["step"]))
+
+
+def bq_prepare_codebook(qmap, prepared=None, stream=None):
+    """Decision tables of a device codebook into a device uint8 buffer of
+    BQ_PREPARED_CODEBOOK_BYTES (allocated here by torch if not given)."""
+    import torch
+    if prepared is None:
+        prepared = torch.empty(BQ_PREPARED_CODEBOOK_BYTES, dtype=torch.uint8, device=qmap.device)
+    if prepared.numel() < BQ_PREPARED_CODEBOOK_BYTES:
+        raise ValueError("prepared buffer too small")
+    _check(lib().bq_prepare_codebook(_dev_ptr(qmap, "qmap"), _dev_ptr(prepared, "prepared"),
+                                     _stream(stream)), "bq_prepare_codebook")
+    return prepared
+
+
+def bq_quantize_blockwise_prepared(prepared, x, blocksize: int, codes=None, absmax=None,
+                                   stream=None):
+    import torch
+    n = x.numel()
+    if codes is None:
+        codes = torch.empty(n, dtype=torch.uint8, device=x.device)
+    if absmax is None:
+        absmax = torch.empty((n + blocksize - 1) // blocksize, dtype=torch.float32,
+                             device=x.device)
+    if x.dtype != torch.float32 or codes.dtype != torch.uint8 or absmax.dtype != torch.float32:
+        raise TypeError("x fp32, codes uint8, absmax fp32")
+    if codes.numel() < n or absmax.numel() < (n + blocksize - 1) // blocksize:
+        raise ValueError("output buffers too small")
+    _check(lib().bq_quantize_blockwise_prepared(_dev_ptr(prepared, "prepared"), _dev_ptr(x, "x"),
+                                                n, int(blocksize), _dev_ptr(codes, "codes"),
+                                                _dev_ptr(absmax, "absmax"), _stream(stream)),
+           "bq_quantize_blockwise_prepared")
+    return codes, absmax
+
+
+class StepPlan:
+    """bq_step_plan_create / bq_step_plan_run / bq_step_plan_destroy.
+
+    The plan holds device pointers to the given tensors; keep them alive (this
+    object keeps references) while the plan is used."""
+
+    def __init__(self, opt, blocksize: int, grad_dtype: int, tensors):
+        if isinstance(opt, str):
+            opt = OPTIMIZERS[opt]
+        self._keep = [t for row in tensors for t in row if t is not None]
+        arr = make_tensor_array(tensors)
+        h = ctypes.c_void_p()
+        _check(lib().bq_step_plan_create(int(opt), int(blocksize), int(grad_dtype), arr,
+                                         len(tensors), ctypes.byref(h)), "bq_step_plan_create")
+        self._h = h
+
+    def run(self, hp: dict, qmap1, qmap2=None, stream=None):
+        h = _hparams(hp)
+        _check(lib().bq_step_plan_run(self._h, ctypes.byref(h), _dev_ptr(qmap1, "qmap1"),
+                                      None if qmap2 is None else _dev_ptr(qmap2, "qmap2"),
+                                      _stream(stream)), "bq_step_plan_run")
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value is not None:
+            lib().bq_step_plan_destroy(self._h)
+        self._h = None
+        self._keep = []
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def bq_step_plan_create(opt, blocksize, grad_dtype, tensors):
+    return StepPlan(opt, blocksize, grad_dtype, tensors)
+
+
+def bq_step_plan_run(plan: StepPlan, hp: dict, qmap1, qmap2=None, stream=None):
+    plan.run(hp, qmap1, qmap2, stream)
+
+
+def bq_step_plan_destroy(plan: StepPlan):
+    plan.close()

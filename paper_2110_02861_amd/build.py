@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libbq.so")
-SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_kernels.hip"]
+SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_kernels.hip", "bq_oneshot.hip"]
 ARCH = "gfx950"
 
 # -ffp-contract=off: the state arithmetic must not be fused into fma, so that it
@@ -48,10 +48,10 @@ def build(verbose: bool = False) -> str:
 def build_asm(out_dir: str) -> None:
     """Write the device assembly of the kernels (for inspection only)."""
     os.makedirs(out_dir, exist_ok=True)
-    src = os.path.join(CSRC, "bq_kernels.hip")
-    cmd = [hipcc(), *FLAGS, "--cuda-device-only", "-S", "-o",
-           os.path.join(out_dir, "bq_kernels.s"), src]
-    subprocess.run(cmd, check=True)
+    for name in ("bq_kernels.hip", "bq_oneshot.hip"):
+        cmd = [hipcc(), *FLAGS, "--cuda-device-only", "-S", "-o",
+               os.path.join(out_dir, name.replace(".hip", ".s")), os.path.join(CSRC, name)]
+        subprocess.run(cmd, check=True)
 
 
 if __name__ == "__main__":

@@ -1,10 +1,12 @@
 // C-ABI entry points of libbq (declared in include/bq.h): argument checks,
-// per-step scalar precomputation, and packing of tensor descriptors into
-// kernel-argument chunks.  Every check runs before the first HIP call, so an
-// error return means nothing was enqueued.
+// per-step scalar precomputation, packing of tensor descriptors (kernel-argument
+// chunks, or a device-resident plan), and launches.  Every check runs before
+// the first HIP call, so an error return means nothing was enqueued.
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <new>
+#include <vector>
 
 #include "bq.h"
 #include "bq_internal.h"
@@ -14,6 +16,8 @@ namespace {
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
 bool valid_blocksize(int32_t b) { return b >= 256 && b <= 4096 && (b & (b - 1)) == 0; }
+bool valid_opt(bq_optimizer o) { return o == BQ_ADAM || o == BQ_ADAMW || o == BQ_MOMENTUM; }
+bool valid_dtype(bq_dtype d) { return d == BQ_F32 || d == BQ_F16; }
 
 // beta^t in double by right-to-left binary exponentiation.
 double beta_pow(double beta, int64_t t)
@@ -47,7 +51,61 @@ bq::StepScalars make_scalars(const bq_hparams &hp)
 
 bq_status from_hip(hipError_t e) { return e == hipSuccess ? BQ_OK : BQ_ERR_HIP; }
 
+// Checks every descriptor of a tensor list (no HIP call).
+bq_status check_tensors(const bq_tensor *tensors, int32_t ntensors, int32_t blocksize, bool two)
+{
+    const int64_t tile = bq::tile_elems(blocksize);
+    for (int32_t i = 0; i < ntensors; ++i) {
+        const bq_tensor &t = tensors[i];
+        if (t.numel < 0)
+            return BQ_ERR_SIZE;
+        // tiles of one launch are counted in int32
+        if (t.numel / tile >= (int64_t)INT32_MAX / 2)
+            return BQ_ERR_SIZE;
+        if (t.numel == 0)
+            continue;
+        if (!t.param || !t.grad || !t.state1 || !t.absmax1 ||
+            (two && (!t.state2 || !t.absmax2)))
+            return BQ_ERR_NULL;
+        if (!aligned(t.param, 16) || !aligned(t.grad, 16) || !aligned(t.state1, 16) ||
+            !aligned(t.absmax1, 4) ||
+            (two && (!aligned(t.state2, 16) || !aligned(t.absmax2, 4))))
+            return BQ_ERR_ALIGN;
+    }
+    return BQ_OK;
+}
+
+bq::TensorDesc make_desc(const bq_tensor &t, bool two, int64_t tile_begin)
+{
+    bq::TensorDesc d;
+    d.param = t.param;
+    d.grad = t.grad;
+    d.s1 = t.state1;
+    d.s2 = two ? t.state2 : nullptr;
+    d.a1 = t.absmax1;
+    d.a2 = two ? t.absmax2 : nullptr;
+    d.numel = t.numel;
+    d.tile_begin = tile_begin;
+    return d;
+}
+
+// One-shot launches place one 512-thread workgroup per tile; the grid in
+// work-items must stay below 2^32.
+constexpr int64_t kMaxOneShotTiles = (int64_t{1} << 32) / 512 - 1;
+
 }  // namespace
+
+struct bq_step_plan_s {
+    int device;
+    bq_optimizer opt;
+    int32_t blocksize;
+    bq_dtype grad_dtype;
+    int32_t ntensors;      // non-empty tensors
+    int64_t total_tiles;
+    bq::TensorDesc *desc;  // device
+    int32_t *tile_tensor;  // device, tensor index of every tile
+    uint8_t *tables;       // device, two prepared maps
+};
 
 extern "C" {
 
@@ -105,6 +163,8 @@ bq_status bq_dequantize_blockwise(const float *qmap, const uint8_t *codes, const
         return BQ_ERR_NULL;
     if (!aligned(codes, 16) || !aligned(out, 16) || !aligned(absmax, 4) || !aligned(qmap, 4))
         return BQ_ERR_ALIGN;
+    if ((n + 2047) / 2048 > kMaxOneShotTiles)
+        return BQ_ERR_SIZE;
     return from_hip(bq::launch_dequantize(qmap, codes, absmax, n, blocksize, out, stream));
 }
 
@@ -113,9 +173,9 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
                                 const bq_hparams *hp, const float *qmap1, const float *qmap2,
                                 hipStream_t stream)
 {
-    if (opt != BQ_ADAM && opt != BQ_ADAMW && opt != BQ_MOMENTUM)
+    if (!valid_opt(opt))
         return BQ_ERR_ENUM;
-    if (grad_dtype != BQ_F32 && grad_dtype != BQ_F16)
+    if (!valid_dtype(grad_dtype))
         return BQ_ERR_DTYPE;
     if (!valid_blocksize(blocksize))
         return BQ_ERR_BLOCKSIZE;
@@ -132,25 +192,9 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
         return BQ_ERR_ARG;
     if (!aligned(qmap1, 4) || (two && !aligned(qmap2, 4)))
         return BQ_ERR_ALIGN;
-
-    const int64_t tile = bq::tile_elems(blocksize);
-    for (int32_t i = 0; i < ntensors; ++i) {
-        const bq_tensor &t = tensors[i];
-        if (t.numel < 0)
-            return BQ_ERR_SIZE;
-        // tiles of one launch are counted in int32
-        if (t.numel / tile >= (int64_t)INT32_MAX / 2)
-            return BQ_ERR_SIZE;
-        if (t.numel == 0)
-            continue;
-        if (!t.param || !t.grad || !t.state1 || !t.absmax1 ||
-            (two && (!t.state2 || !t.absmax2)))
-            return BQ_ERR_NULL;
-        if (!aligned(t.param, 16) || !aligned(t.grad, 16) || !aligned(t.state1, 16) ||
-            !aligned(t.absmax1, 4) ||
-            (two && (!aligned(t.state2, 16) || !aligned(t.absmax2, 4))))
-            return BQ_ERR_ALIGN;
-    }
+    const bq_status st = check_tensors(tensors, ntensors, blocksize, two);
+    if (st != BQ_OK)
+        return st;
 
     bq::StepArgs args;
     std::memset(&args, 0, sizeof(args));
@@ -161,6 +205,7 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
 
     // Pack non-empty tensors into launches of at most kMaxDescPerLaunch
     // descriptors, or fewer when a launch's tile count would overflow int32.
+    const int64_t tile = bq::tile_elems(blocksize);
     int32_t i = 0;
     while (i < ntensors) {
         int32_t k = 0;
@@ -172,15 +217,7 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
             const int64_t nt = (t.numel + tile - 1) / tile;
             if (k > 0 && tiles + nt > (int64_t)INT32_MAX / 2)
                 break;
-            bq::TensorDesc &d = args.d[k++];
-            d.param = t.param;
-            d.grad = t.grad;
-            d.s1 = t.state1;
-            d.s2 = two ? t.state2 : nullptr;
-            d.a1 = t.absmax1;
-            d.a2 = two ? t.absmax2 : nullptr;
-            d.numel = t.numel;
-            d.tile_begin = tiles;
+            args.d[k++] = make_desc(t, two, tiles);
             tiles += nt;
         }
         if (k == 0)
@@ -193,6 +230,153 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
             return BQ_ERR_HIP;
     }
     return BQ_OK;
+}
+
+bq_status bq_prepare_codebook(const float *qmap, void *prepared, hipStream_t stream)
+{
+    if (!qmap || !prepared)
+        return BQ_ERR_NULL;
+    if (!aligned(qmap, 4) || !aligned(prepared, 16))
+        return BQ_ERR_ALIGN;
+    return from_hip(bq::launch_prepare(qmap, nullptr, static_cast<uint8_t *>(prepared), stream));
+}
+
+bq_status bq_quantize_blockwise_prepared(const void *prepared, const float *x, int64_t n,
+                                         int32_t blocksize, uint8_t *codes, float *absmax,
+                                         hipStream_t stream)
+{
+    if (n < 0)
+        return BQ_ERR_SIZE;
+    if (!valid_blocksize(blocksize))
+        return BQ_ERR_BLOCKSIZE;
+    if (n == 0)
+        return BQ_OK;
+    if (!prepared || !x || !codes || !absmax)
+        return BQ_ERR_NULL;
+    if (!aligned(prepared, 16) || !aligned(x, 16) || !aligned(codes, 16) || !aligned(absmax, 4))
+        return BQ_ERR_ALIGN;
+    const int64_t tile = bq::tile_elems(blocksize);
+    if ((n + tile - 1) / tile > kMaxOneShotTiles)
+        return BQ_ERR_SIZE;
+    return from_hip(bq::launch_quantize_prepared(static_cast<const uint8_t *>(prepared), x, n,
+                                                 blocksize, codes, absmax, stream));
+}
+
+bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                              const bq_tensor *tensors, int32_t ntensors, bq_step_plan *plan)
+{
+    if (!plan)
+        return BQ_ERR_NULL;
+    *plan = nullptr;
+    if (!valid_opt(opt))
+        return BQ_ERR_ENUM;
+    if (!valid_dtype(grad_dtype))
+        return BQ_ERR_DTYPE;
+    if (!valid_blocksize(blocksize))
+        return BQ_ERR_BLOCKSIZE;
+    if (ntensors < 0)
+        return BQ_ERR_SIZE;
+    if (ntensors > 0 && !tensors)
+        return BQ_ERR_NULL;
+    const bool two = (opt != BQ_MOMENTUM);
+    const bq_status st = check_tensors(tensors, ntensors, blocksize, two);
+    if (st != BQ_OK)
+        return st;
+
+    const int64_t tile = bq::tile_elems(blocksize);
+    std::vector<bq::TensorDesc> desc;
+    std::vector<int32_t> tile_tensor;
+    int64_t tiles = 0;
+    for (int32_t i = 0; i < ntensors; ++i) {
+        const bq_tensor &t = tensors[i];
+        if (t.numel == 0)
+            continue;
+        const int64_t nt = (t.numel + tile - 1) / tile;
+        if (tiles + nt > kMaxOneShotTiles)
+            return BQ_ERR_SIZE;
+        desc.push_back(make_desc(t, two, tiles));
+        tile_tensor.insert(tile_tensor.end(), (size_t)nt, (int32_t)(desc.size() - 1));
+        tiles += nt;
+    }
+
+    bq_step_plan_s *p = new (std::nothrow) bq_step_plan_s();
+    if (!p)
+        return BQ_ERR_HIP;
+    p->opt = opt;
+    p->blocksize = blocksize;
+    p->grad_dtype = grad_dtype;
+    p->ntensors = (int32_t)desc.size();
+    p->total_tiles = tiles;
+    hipError_t e = hipGetDevice(&p->device);
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&p->tables), 2 * bq::kPreparedBytes);
+    if (e == hipSuccess && !desc.empty()) {
+        e = hipMalloc(reinterpret_cast<void **>(&p->desc), desc.size() * sizeof(bq::TensorDesc));
+        if (e == hipSuccess)
+            e = hipMalloc(reinterpret_cast<void **>(&p->tile_tensor),
+                          tile_tensor.size() * sizeof(int32_t));
+        if (e == hipSuccess)
+            e = hipMemcpy(p->desc, desc.data(), desc.size() * sizeof(bq::TensorDesc),
+                          hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = hipMemcpy(p->tile_tensor, tile_tensor.data(), tile_tensor.size() * sizeof(int32_t),
+                          hipMemcpyHostToDevice);
+    }
+    if (e != hipSuccess) {
+        bq_step_plan_destroy(p);
+        return BQ_ERR_HIP;
+    }
+    *plan = p;
+    return BQ_OK;
+}
+
+bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float *qmap1,
+                           const float *qmap2, hipStream_t stream)
+{
+    if (!plan || !hp || !qmap1)
+        return BQ_ERR_NULL;
+    const bool two = (plan->opt != BQ_MOMENTUM);
+    if (two && !qmap2)
+        return BQ_ERR_NULL;
+    if (hp->step < 1)
+        return BQ_ERR_ARG;
+    if (!aligned(qmap1, 4) || (two && !aligned(qmap2, 4)))
+        return BQ_ERR_ALIGN;
+    if (plan->total_tiles == 0)
+        return BQ_OK;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return BQ_ERR_HIP;
+    if (dev != plan->device)
+        return BQ_ERR_ARG;
+
+    bq::PlanArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.tables = plan->tables;
+    a.desc = plan->desc;
+    a.tile_tensor = plan->tile_tensor;
+    a.sc = make_scalars(*hp);
+    a.use_wd = (hp->weight_decay != 0.0f && plan->opt != BQ_ADAMW) ? 1 : 0;
+    a.total_tiles = (int32_t)plan->total_tiles;
+    hipError_t e = bq::launch_prepare(qmap1, two ? qmap2 : nullptr, plan->tables, stream);
+    if (e == hipSuccess)
+        e = bq::launch_step_oneshot((int)plan->opt, (int)plan->grad_dtype, plan->blocksize, a,
+                                    stream);
+    return from_hip(e);
+}
+
+bq_status bq_step_plan_destroy(bq_step_plan plan)
+{
+    if (!plan)
+        return BQ_OK;
+    hipError_t e = hipSuccess;
+    for (void *ptr : {static_cast<void *>(plan->desc), static_cast<void *>(plan->tile_tensor),
+                      static_cast<void *>(plan->tables)}) {
+        if (ptr && hipFree(ptr) != hipSuccess)
+            e = hipErrorUnknown;
+    }
+    delete plan;
+    return from_hip(e);
 }
 
 }  // extern "C"

@@ -1,0 +1,324 @@
+// Device helpers shared by the HIP kernels (gfx950): codebook decision tables,
+// exact nearest-code search, exact division by the block absmax, wave / group
+// max reductions, vector loads and stores.
+//
+// Exact nearest code (Eq. 3 / Eq. 4 of the paper, ties to the lower index)
+//   With T_j the smallest fp32 above the midpoint of codes j and j+1 and
+//   T_255 = +inf, the nearest code of y is #{j : y >= T_j}.  The sign, exponent
+//   and top 7 mantissa bits of y select a bucket (a run of fp32 bit patterns);
+//   a table holds, per bucket, the number of thresholds at or below the
+//   bucket's smallest value.  At most K thresholds lie inside any bucket (K is
+//   computed with the table; K = 1 for the dynamic maps), so K compares
+//   against T finish the count.  This is exact for every strictly increasing
+//   map.
+//
+// Exact division
+//   y = x / N is the correctly rounded quotient: per block r = RN(1/N'), per
+//   element q = x' r, e = fma(-q, N', x'), y = fma(e, r, q) (Markstein's
+//   correction), with x' = x s, N' = N s and s a power of two keeping N' within
+//   [2^-64, 2^64].  Exact whenever |y| >= 2^-100, far below any threshold of a
+//   map whose nonzero magnitudes are >= 2^-60.  An all-zero block uses r = 0,
+//   which sends every element to y = 0.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bq_internal.h"
+
+namespace bq {
+namespace dev {
+
+// Bucket index: bits [30:16] of |y| (8 exponent + 7 mantissa bits), clamped to
+// the binades [2^-25, 2^1).  Magnitudes below 2^-25 share the first bucket,
+// magnitudes of 1 and above the last.
+constexpr uint32_t kBucketShift = 16;
+constexpr uint32_t kBucketLo = (127u - 25u) << 7;
+constexpr uint32_t kBucketHi = (127u << 7) + 127u;
+constexpr uint32_t kBuckets = kBucketHi - kBucketLo + 1;  // per sign
+static_assert(kBuckets == kPreparedBuckets, "prepared table layout");
+
+// Read-only view of one map's decision tables (in LDS).
+struct Tables {
+    const float *q;       // 256 codebook values
+    const float *t;       // 256 thresholds, t[255] = +inf
+    const uint8_t *base;  // [sign * kBuckets + bucket]; only the + half for NONNEG use
+    int kmax;             // max thresholds strictly inside one bucket
+};
+
+__device__ inline float next_up(float f)
+{
+    if (f == 0.0f)
+        return __uint_as_float(1u);  // smallest positive subnormal
+    const uint32_t u = __float_as_uint(f);
+    return __uint_as_float(f > 0.0f ? u + 1u : u - 1u);
+}
+
+// #{j : t_j <= v} for finite v (at most 255 since t_255 = +inf).
+__device__ inline uint32_t count_le(const float *t, float v)
+{
+    uint32_t c = 0;
+#pragma unroll
+    for (uint32_t s = 128; s >= 1; s >>= 1)
+        c += (t[c + s - 1] <= v) ? s : 0u;
+    return c;
+}
+
+__device__ inline uint32_t bucket_lo_bits(uint32_t b)
+{
+    return b == 0 ? 0u : (kBucketLo + b) << kBucketShift;
+}
+__device__ inline uint32_t bucket_hi_bits(uint32_t b)
+{
+    return b == kBuckets - 1 ? 0x7f7fffffu : ((kBucketLo + b + 1) << kBucketShift) - 1u;
+}
+
+// Build q, t, base and kmax for one map.  All NT threads of the workgroup take
+// part (NT >= 256); the function contains barriers.  q, t and base may live in
+// LDS or global memory; t must be readable by every thread after the first
+// barrier.  kmax_out is an LDS int, set to the maximum over the workgroup.
+template <int NT>
+__device__ void build_tables(const float *__restrict__ qmap, float *q, float *t, uint8_t *base,
+                             int *kmax_out)
+{
+    static_assert(NT >= 256, "one thread per code");
+    const uint32_t j = threadIdx.x;
+    if (j < 256) {
+        const float qj = qmap[j];
+        q[j] = qj;
+        float thr = __builtin_inff();
+        if (j < 255) {
+            // adjacent codes of a valid map are within 2^29 of each other, so
+            // the double sum is exact
+            const double mid = ((double)qj + (double)qmap[j + 1]) * 0.5;
+            float f = (float)mid;
+            if ((double)f <= mid)
+                f = next_up(f);
+            thr = f;
+        }
+        t[j] = thr;
+    }
+    if (j == 0)
+        *kmax_out = 0;
+    __syncthreads();
+
+    // Each thread walks a contiguous run of buckets on each side in ascending
+    // value order: one binary search, then a forward scan gives every count.
+    constexpr uint32_t kPer = (kBuckets + NT - 1) / NT;
+    const uint32_t b0 = j * kPer;
+    const uint32_t b1 = b0 + kPer < kBuckets ? b0 + kPer : kBuckets;
+    int kmax = 0;
+    if (b0 < b1) {
+        // positive side: values [lo, hi] rise with b
+        uint32_t c = count_le(t, __uint_as_float(bucket_lo_bits(b0)));
+        for (uint32_t b = b0; b < b1; ++b) {
+            const float lo = __uint_as_float(bucket_lo_bits(b));
+            const float hi = __uint_as_float(bucket_hi_bits(b));
+            while (t[c] <= lo)
+                ++c;
+            base[b] = (uint8_t)c;
+            uint32_t e = c;
+            while (t[e] <= hi)
+                ++e;
+            kmax = max(kmax, (int)(e - c));
+            c = e;
+        }
+        // negative side: values [-hi, -lo] rise as b falls
+        c = count_le(t, -__uint_as_float(bucket_hi_bits(b1 - 1)));
+        for (uint32_t b = b1; b-- > b0;) {
+            const float lo = -__uint_as_float(bucket_hi_bits(b));
+            const float hi = -__uint_as_float(bucket_lo_bits(b));
+            while (t[c] <= lo)
+                ++c;
+            base[kBuckets + b] = (uint8_t)c;
+            uint32_t e = c;
+            while (t[e] <= hi)
+                ++e;
+            kmax = max(kmax, (int)(e - c));
+            c = e;
+        }
+    }
+    atomicMax(kmax_out, kmax);
+    __syncthreads();
+}
+
+// Bucket of y.  NONNEG: y is +0 or positive.
+template <bool NONNEG>
+__device__ inline uint32_t bucket_of(float y)
+{
+    const uint32_t u = __float_as_uint(y);
+    if constexpr (NONNEG) {
+        return min(max(u >> kBucketShift, kBucketLo), kBucketHi) - kBucketLo;
+    } else {
+        const uint32_t a = (u & 0x7fffffffu) >> kBucketShift;
+        return min(max(a, kBucketLo), kBucketHi) - kBucketLo + (u >> 31) * kBuckets;
+    }
+}
+
+// Nearest codes of N values: one bucket lookup each, then kmax rounds of one
+// threshold compare each over all values, so independent LDS reads overlap.
+template <int N, bool NONNEG>
+__device__ inline void nearest_codes(const Tables &M, const float (&y)[N], uint32_t (&c)[N])
+{
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+        c[i] = M.base[bucket_of<NONNEG>(y[i])];
+    for (int k = 0; k < M.kmax; ++k) {
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            c[i] += (y[i] >= M.t[c[i]]) ? 1u : 0u;
+    }
+}
+
+struct Normalizer {
+    float n;  // scaled divisor N' (1 for an all-zero block)
+    float r;  // RN(1 / N'), or 0 for an all-zero block
+    float s;  // power-of-two scale applied to x
+};
+
+__device__ inline Normalizer make_normalizer(float N)
+{
+    Normalizer z;
+    z.s = 1.0f;
+    if (N < 0x1p-64f)
+        z.s = 0x1p64f;
+    else if (N > 0x1p64f)
+        z.s = 0x1p-64f;
+    const bool zero = !(N > 0.0f);
+    z.n = zero ? 1.0f : N * z.s;
+    z.r = zero ? 0.0f : 1.0f / z.n;  // correctly rounded division
+    return z;
+}
+
+template <bool SCALED>
+__device__ inline float normalize(const Normalizer &z, float x)
+{
+    const float xs = SCALED ? x * z.s : x;
+    const float q = xs * z.r;
+    const float e = __builtin_fmaf(-q, z.n, xs);
+    return __builtin_fmaf(e, z.r, q);
+}
+
+// Requantize N values of one thread against map M with block absmax A.
+// GROUP >= 64 means a wave lies inside one block (A is wave-uniform).
+template <int N, int GROUP, bool NONNEG>
+__device__ inline void requantize(const Tables &M, float A, const float (&x)[N], uint32_t (&c)[N])
+{
+    const Normalizer z = make_normalizer(A);
+    bool scaled = (z.s != 1.0f);
+    if constexpr (GROUP >= 64)
+        scaled = __builtin_amdgcn_readfirstlane((int)scaled) != 0;
+    float y[N];
+    if (!scaled) {
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            y[i] = normalize<false>(z, x[i]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            y[i] = normalize<true>(z, x[i]);
+    }
+    nearest_codes<N, NONNEG>(M, y, c);
+}
+
+// ---------------------------------------------------------------------------
+// Reductions
+// ---------------------------------------------------------------------------
+
+template <int CTRL, int ROW_MASK>
+__device__ inline float dpp_max(float v)
+{
+    const int iv = __builtin_bit_cast(int, v);
+    const int o = __builtin_amdgcn_update_dpp(iv, iv, CTRL, ROW_MASK, 0xf, false);
+    return fmaxf(v, __builtin_bit_cast(float, o));
+}
+
+// Max over each row of 16 lanes, left in every lane of the row.
+__device__ inline float row_max(float v)
+{
+    v = dpp_max<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
+    v = dpp_max<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
+    v = dpp_max<0x141, 0xf>(v);  // row_half_mirror
+    v = dpp_max<0x140, 0xf>(v);  // row_mirror
+    return v;
+}
+
+__device__ inline float lane_f(float v, int lane)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+
+// Max of (x, y) over each group of GROUP consecutive threads (power of two,
+// 32..1024).  slots: LDS scratch of (threads / 64) float2 not in use by another
+// reduction of the same workgroup.  Contains a barrier when GROUP > 64.
+template <int GROUP>
+__device__ inline float2 group_max(float2 v, float2 *slots)
+{
+    v.x = row_max(v.x);
+    v.y = row_max(v.y);
+    v.x = dpp_max<0x142, 0xa>(v.x);  // row_bcast:15 -> lanes 31, 63 hold half maxima
+    v.y = dpp_max<0x142, 0xa>(v.y);
+    if constexpr (GROUP == 32) {
+        const bool hi = (threadIdx.x & 32) != 0;
+        return make_float2(hi ? lane_f(v.x, 63) : lane_f(v.x, 31),
+                           hi ? lane_f(v.y, 63) : lane_f(v.y, 31));
+    } else {
+        v.x = dpp_max<0x143, 0xc>(v.x);  // row_bcast:31 -> lane 63 holds the wave max
+        v.y = dpp_max<0x143, 0xc>(v.y);
+        const float2 w = make_float2(lane_f(v.x, 63), lane_f(v.y, 63));
+        if constexpr (GROUP == 64) {
+            return w;
+        } else {
+            constexpr int WPG = GROUP / 64;
+            const int wave = threadIdx.x >> 6;
+            if ((threadIdx.x & 63) == 0)
+                slots[wave] = w;
+            __syncthreads();
+            const int first = (wave / WPG) * WPG;
+            float2 r = slots[first];
+#pragma unroll
+            for (int k = 1; k < WPG; ++k) {
+                const float2 o = slots[first + k];
+                r.x = fmaxf(r.x, o.x);
+                r.y = fmaxf(r.y, o.y);
+            }
+            return r;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Memory access
+// ---------------------------------------------------------------------------
+
+typedef float vf4 __attribute__((ext_vector_type(4)));
+typedef uint32_t vu2 __attribute__((ext_vector_type(2)));
+typedef uint32_t vu4 __attribute__((ext_vector_type(4)));
+
+// Global-memory (address space 1) views of generic pointers: loads and stores
+// through them compile to global_* instructions (vector memory counter only)
+// instead of flat_*, which keeps the compiler's wait counts precise.
+template <typename T>
+using gptr = __attribute__((address_space(1))) T *;
+template <typename T>
+__device__ inline gptr<T> G(T *p) { return (gptr<T>)p; }
+template <typename T>
+__device__ inline gptr<const T> G(const T *p) { return (gptr<const T>)p; }
+
+// Streaming (non-temporal) accesses: every byte of the step is touched once.
+template <typename T>
+__device__ inline T ld_nt(const T *p) { return __builtin_nontemporal_load(G(p)); }
+template <typename T>
+__device__ inline void st_nt(T *p, T v) { __builtin_nontemporal_store(v, G(p)); }
+
+__device__ inline float half_lo(uint32_t w)
+{
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xffffu));
+}
+__device__ inline float half_hi(uint32_t w)
+{
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+}
+
+}  // namespace dev
+}  // namespace bq

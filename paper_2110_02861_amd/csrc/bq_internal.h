@@ -50,6 +50,41 @@ static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must stay below 4
 // Elements per tile (one workgroup iteration) for a given blocksize.
 constexpr int tile_elems(int blocksize) { return blocksize >= 2048 ? blocksize : 2048; }
 
+// Prepared codebook: decision tables of one map in device memory, built once
+// by the prepare kernel and copied into LDS by every workgroup.
+//   [0, 1024)      float q[256]          codebook values
+//   [1024, 2048)   float t[256]          thresholds, t[255] = +inf
+//   [2048, 5376)   uint8 base[+, 3328]   per bucket of positive values
+//   [5376, 8704)   uint8 base[-, 3328]   per bucket of negative values
+//   [8704, 8708)   int32 kmax            thresholds inside one bucket, at most
+constexpr int kPreparedBuckets = 3328;
+constexpr int kPreparedOffQ = 0;
+constexpr int kPreparedOffT = 1024;
+constexpr int kPreparedOffBase = 2048;
+constexpr int kPreparedOffKmax = kPreparedOffBase + 2 * kPreparedBuckets;
+constexpr int kPreparedBytes = kPreparedOffKmax + 16;
+constexpr int kPreparedSignedBytes = kPreparedOffKmax;            // q, t, both halves
+constexpr int kPreparedNonnegBytes = kPreparedOffBase + kPreparedBuckets;  // q, t, + half
+static_assert(kPreparedBytes % 16 == 0 && kPreparedNonnegBytes % 16 == 0, "16 B granules");
+
+// Arguments of the one-shot step kernel (one workgroup per tile).
+struct PlanArgs {
+    const uint8_t *tables;        // prepared map of state 1, then of state 2
+    const TensorDesc *desc;       // device array of descriptors
+    const int32_t *tile_tensor;   // device array: tensor index of every tile
+    StepScalars sc;
+    int32_t use_wd;
+    int32_t total_tiles;
+};
+
+hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *tables,
+                          hipStream_t stream);
+hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const PlanArgs &args,
+                               hipStream_t stream);
+hipError_t launch_quantize_prepared(const uint8_t *tables, const float *x, int64_t n,
+                                    int blocksize, uint8_t *codes, float *absmax,
+                                    hipStream_t stream);
+
 enum { kAdam = 0, kAdamW = 1, kMomentum = 2 };
 enum { kF32 = 0, kF16 = 1 };
 

@@ -1,43 +1,15 @@
-// HIP kernels for gfx950: block-wise quantize / dequantize and the fused
-// 8-bit optimizer step (Dettmers et al., "8-bit Optimizers via Block-wise
-// Quantization", Sections 2.2, 3, 3.1; Eq. 1-4).
+// Persistent HIP kernels for gfx950 behind the allocation-free calls
+// bq_quantize_blockwise and bq_optimizer8bit_step (Dettmers et al., "8-bit
+// Optimizers via Block-wise Quantization", Sections 3, 3.1; Eq. 1-4).
 //
-// Execution model
-//   * Persistent workgroups of 256 threads (4 wave64).  A workgroup first
-//     stages each codebook, its decision thresholds and a bucket index in LDS,
-//     then walks a strided list of tiles.  A tile is 2048 elements (or one 4096
-//     block); each thread owns EPT contiguous elements, moved with 128-bit (or
-//     64-bit, for 8 codes) accesses.
-//   * A quantization block of B elements is owned by B / EPT consecutive
-//     threads: its absmax is a DPP reduction inside a wave plus, when the block
-//     spans waves, one LDS exchange behind one barrier.
-//   * Tiles never span tensors, so neither do blocks.
-//
-// Exact nearest code (Eq. 3, ties to the lower index)
-//   With T_j the smallest fp32 above the midpoint of codes j and j+1 and
-//   T_255 = +inf, the nearest code of y is #{j : y >= T_j}.  Instead of a
-//   binary search over T, the sign, exponent and top 7 mantissa bits of y
-//   select a bucket (a run of fp32 bit patterns); LDS holds, per bucket, the
-//   number of thresholds at or below the bucket's smallest value.  At most K
-//   thresholds lie inside any bucket (K is computed in the prologue; K = 1 for
-//   the dynamic maps), so K compares against T finish the count.  This is
-//   exact for every strictly increasing map.
-//
-// Exact division
-//   y = x / N is the correctly rounded quotient: per block r = RN(1/N'), per
-//   element q = x' r, e = fma(-q, N', x'), y = fma(e, r, q) (Markstein's
-//   correction), with x' = x s, N' = N s and s a power of two keeping N' within
-//   [2^-64, 2^64].  Exact whenever |y| >= 2^-100, far below any threshold of a
-//   map whose nonzero magnitudes are >= 2^-60.  An all-zero block uses r = 0,
-//   which sends every element to y = 0.
-//
-// State arithmetic is fp32 without contraction (-ffp-contract=off), in the
-// operation order of the update's definition, so codes and absmax are
-// reproducible bit for bit.
-#include <hip/hip_runtime.h>
-#include <stdint.h>
-
-#include "bq_internal.h"
+// These calls receive raw codebooks and no workspace, so each workgroup builds
+// the codebook's decision tables in its own LDS once and then walks a strided
+// list of tiles.  A tile is 2048 elements (or one 4096 block) of one tensor;
+// each thread owns EPT contiguous elements, moved with 128-bit (or 64-bit, for
+// 8 codes) accesses.  A quantization block of B elements belongs to B / EPT
+// consecutive threads.  Descriptors of up to 56 tensors travel in the kernel
+// arguments.  The prepared-codebook path (bq_oneshot.hip) is the faster one.
+#include "bq_device.h"
 
 namespace bq {
 namespace {
@@ -45,236 +17,23 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 
-// Bucket index: bits [30:16] of |y| (8 exponent + 7 mantissa bits), clamped to
-// the binades [2^-25, 2^1).  Magnitudes below 2^-25 share the first bucket,
-// magnitudes of 1 and above the last.
-constexpr uint32_t kBucketShift = 16;
-constexpr uint32_t kBucketLo = (127u - 25u) << 7;
-constexpr uint32_t kBucketHi = (127u << 7) + 127u;
-constexpr uint32_t kBuckets = kBucketHi - kBucketLo + 1;  // per sign
-
-// ---------------------------------------------------------------------------
-// Codebook tables in LDS
-// ---------------------------------------------------------------------------
+using namespace dev;
 
 struct MapTables {
-    float q[256];                  // codebook values (dequantization)
-    float t[256];                  // decision thresholds, t[255] = +inf
-    uint8_t base[2 * kBuckets];    // [sign * kBuckets + bucket] -> #{j : t_j <= bucket min}
-    int kmax;                      // max thresholds strictly inside one bucket
+    float q[256];
+    float t[256];
+    uint8_t base[2 * kBuckets];
+    int kmax;
 };
 
-__device__ inline float next_up(float f)
+__device__ inline Tables view(const MapTables &M, int kmax)
 {
-    if (f == 0.0f)
-        return __uint_as_float(1u);  // smallest positive subnormal
-    const uint32_t u = __float_as_uint(f);
-    return __uint_as_float(f > 0.0f ? u + 1u : u - 1u);
-}
-
-// #{j : t_j <= v} for finite v (at most 255 since t_255 = +inf).
-__device__ inline uint32_t count_le(const float *t, float v)
-{
-    uint32_t c = 0;
-#pragma unroll
-    for (uint32_t s = 128; s >= 1; s >>= 1)
-        c += (t[c + s - 1] <= v) ? s : 0u;
-    return c;
-}
-
-// Smallest and largest magnitude bit pattern of bucket b.
-__device__ inline uint32_t bucket_lo_bits(uint32_t b) { return b == 0 ? 0u : (kBucketLo + b) << kBucketShift; }
-__device__ inline uint32_t bucket_hi_bits(uint32_t b)
-{
-    return b == kBuckets - 1 ? 0x7f7fffffu : ((kBucketLo + b + 1) << kBucketShift) - 1u;
-}
-
-// Build the tables of one map; all 256 threads take part.  Contains barriers.
-__device__ void stage_map(MapTables &M, const float *__restrict__ qmap)
-{
-    const uint32_t j = threadIdx.x;
-    const float qj = qmap[j];
-    M.q[j] = qj;
-    float thr = __builtin_inff();
-    if (j < 255) {
-        // adjacent codes of a valid map are within 2^29 of each other, so the
-        // double sum is exact
-        const double mid = ((double)qj + (double)qmap[j + 1]) * 0.5;
-        float f = (float)mid;
-        if ((double)f <= mid)
-            f = next_up(f);
-        thr = f;
-    }
-    M.t[j] = thr;
-    if (j == 0)
-        M.kmax = 0;
-    __syncthreads();
-
-    // Each thread walks a contiguous run of buckets on each side in ascending
-    // value order, so one binary search plus a forward scan gives every count.
-    constexpr uint32_t kPer = (kBuckets + kThreads - 1) / kThreads;
-    const uint32_t b0 = j * kPer;
-    const uint32_t b1 = b0 + kPer < kBuckets ? b0 + kPer : kBuckets;
-    int kmax = 0;
-    if (b0 < b1) {
-        // positive side: values [lo, hi] rise with b
-        uint32_t c = count_le(M.t, __uint_as_float(bucket_lo_bits(b0)));
-        for (uint32_t b = b0; b < b1; ++b) {
-            const float lo = __uint_as_float(bucket_lo_bits(b));
-            const float hi = __uint_as_float(bucket_hi_bits(b));
-            while (M.t[c] <= lo)
-                ++c;
-            M.base[b] = (uint8_t)c;
-            uint32_t e = c;
-            while (M.t[e] <= hi)
-                ++e;
-            kmax = max(kmax, (int)(e - c));
-            c = e;
-        }
-        // negative side: values [-hi, -lo] rise as b falls
-        c = count_le(M.t, -__uint_as_float(bucket_hi_bits(b1 - 1)));
-        for (uint32_t b = b1; b-- > b0;) {
-            const float lo = -__uint_as_float(bucket_hi_bits(b));
-            const float hi = -__uint_as_float(bucket_lo_bits(b));
-            while (M.t[c] <= lo)
-                ++c;
-            M.base[kBuckets + b] = (uint8_t)c;
-            uint32_t e = c;
-            while (M.t[e] <= hi)
-                ++e;
-            kmax = max(kmax, (int)(e - c));
-            c = e;
-        }
-    }
-    atomicMax(&M.kmax, kmax);
-}
-
-// Bucket of y (index into MapTables::base).  NONNEG: y is +0 or positive.
-template <bool NONNEG>
-__device__ inline uint32_t bucket_of(float y)
-{
-    const uint32_t u = __float_as_uint(y);
-    if constexpr (NONNEG) {
-        return min(max(u >> kBucketShift, kBucketLo), kBucketHi) - kBucketLo;
-    } else {
-        const uint32_t a = (u & 0x7fffffffu) >> kBucketShift;
-        return min(max(a, kBucketLo), kBucketHi) - kBucketLo + (u >> 31) * kBuckets;
-    }
-}
-
-// Nearest codes of EPT values: one bucket lookup each, then kmax rounds of
-// one threshold compare each (the rounds run over all EPT values at once so
-// the LDS reads of different values overlap).
-template <int EPT, bool NONNEG>
-__device__ inline void nearest_codes(const MapTables &M, int kmax, const float (&y)[EPT],
-                                     uint32_t (&c)[EPT])
-{
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-        c[i] = M.base[bucket_of<NONNEG>(y[i])];
-    for (int k = 0; k < kmax; ++k) {
-#pragma unroll
-        for (int i = 0; i < EPT; ++i)
-            c[i] += (y[i] >= M.t[c[i]]) ? 1u : 0u;
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Exact division by the block absmax
-// ---------------------------------------------------------------------------
-
-struct Normalizer {
-    float n;  // scaled divisor N' (1 for an all-zero block)
-    float r;  // RN(1 / N'), or 0 for an all-zero block
-    float s;  // power-of-two scale applied to x
-};
-
-__device__ inline Normalizer make_normalizer(float N)
-{
-    Normalizer z;
-    z.s = 1.0f;
-    if (N < 0x1p-64f)
-        z.s = 0x1p64f;
-    else if (N > 0x1p64f)
-        z.s = 0x1p-64f;
-    const bool zero = !(N > 0.0f);
-    z.n = zero ? 1.0f : N * z.s;
-    z.r = zero ? 0.0f : 1.0f / z.n;  // correctly rounded division
-    return z;
-}
-
-template <bool SCALED>
-__device__ inline float normalize(const Normalizer &z, float x)
-{
-    const float xs = SCALED ? x * z.s : x;
-    const float q = xs * z.r;
-    const float e = __builtin_fmaf(-q, z.n, xs);
-    return __builtin_fmaf(e, z.r, q);
-}
-
-// ---------------------------------------------------------------------------
-// Block absmax reduction
-// ---------------------------------------------------------------------------
-
-template <int CTRL, int ROW_MASK>
-__device__ inline float dpp_max(float v)
-{
-    const int iv = __builtin_bit_cast(int, v);
-    const int o = __builtin_amdgcn_update_dpp(iv, iv, CTRL, ROW_MASK, 0xf, false);
-    return fmaxf(v, __builtin_bit_cast(float, o));
-}
-
-// Max over each row of 16 lanes, left in every lane of the row.
-__device__ inline float row_max(float v)
-{
-    v = dpp_max<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
-    v = dpp_max<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
-    v = dpp_max<0x141, 0xf>(v);  // row_half_mirror
-    v = dpp_max<0x140, 0xf>(v);  // row_mirror
-    return v;
-}
-
-__device__ inline float lane_f(float v, int lane)
-{
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
-}
-
-// Max of (x, y) over each group of GROUP consecutive threads (power of two,
-// 32..256).  slots: LDS scratch of kWaves float2, double-buffered by caller.
-template <int GROUP>
-__device__ inline float2 group_max(float2 v, float2 *slots)
-{
-    v.x = row_max(v.x);
-    v.y = row_max(v.y);
-    v.x = dpp_max<0x142, 0xa>(v.x);  // row_bcast:15 -> lanes 31, 63 hold half maxima
-    v.y = dpp_max<0x142, 0xa>(v.y);
-    if constexpr (GROUP == 32) {
-        const bool hi = (threadIdx.x & 32) != 0;
-        return make_float2(hi ? lane_f(v.x, 63) : lane_f(v.x, 31),
-                           hi ? lane_f(v.y, 63) : lane_f(v.y, 31));
-    } else {
-        v.x = dpp_max<0x143, 0xc>(v.x);  // row_bcast:31 -> lane 63 holds the wave max
-        v.y = dpp_max<0x143, 0xc>(v.y);
-        const float2 w = make_float2(lane_f(v.x, 63), lane_f(v.y, 63));
-        if constexpr (GROUP == 64) {
-            return w;
-        } else {
-            constexpr int WPG = GROUP / 64;
-            const int wave = threadIdx.x >> 6;
-            if ((threadIdx.x & 63) == 0)
-                slots[wave] = w;
-            __syncthreads();
-            const int first = (wave / WPG) * WPG;
-            float2 r = slots[first];
-#pragma unroll
-            for (int k = 1; k < WPG; ++k) {
-                const float2 o = slots[first + k];
-                r.x = fmaxf(r.x, o.x);
-                r.y = fmaxf(r.y, o.y);
-            }
-            return r;
-        }
-    }
+    Tables T;
+    T.q = M.q;
+    T.t = M.t;
+    T.base = M.base;
+    T.kmax = kmax;
+    return T;
 }
 
 // ---------------------------------------------------------------------------
@@ -359,28 +118,6 @@ struct Shape {
     static_assert(TILE == tile_elems(B), "tile size");
 };
 
-// Requantize EPT values of one thread against map M, block absmax N.
-template <int EPT, int GROUP, bool NONNEG>
-__device__ inline void requantize(const MapTables &M, int kmax, float N, const float (&x)[EPT],
-                                  uint32_t (&c)[EPT])
-{
-    const Normalizer z = make_normalizer(N);
-    bool scaled = (z.s != 1.0f);
-    if constexpr (GROUP >= 64)
-        scaled = __builtin_amdgcn_readfirstlane((int)scaled) != 0;  // wave-uniform
-    float y[EPT];
-    if (!scaled) {
-#pragma unroll
-        for (int i = 0; i < EPT; ++i)
-            y[i] = normalize<false>(z, x[i]);
-    } else {
-#pragma unroll
-        for (int i = 0; i < EPT; ++i)
-            y[i] = normalize<true>(z, x[i]);
-    }
-    nearest_codes<EPT, NONNEG>(M, kmax, y, c);
-}
-
 // ---------------------------------------------------------------------------
 // Fused 8-bit optimizer step
 // ---------------------------------------------------------------------------
@@ -394,8 +131,8 @@ struct StepTile {
     // One tile of one tensor: e0 is this thread's first element, valid the
     // number of its elements inside the tensor (EPT on full tiles).
     template <bool FULL>
-    __device__ static void run(const StepArgs &a, const TensorDesc &D, const MapTables &T1,
-                               const MapTables &T2, int k1, int k2, int64_t e0, int valid,
+    __device__ static void run(const StepArgs &a, const TensorDesc &D, const Tables &T1,
+                               const Tables &T2, int64_t e0, int valid,
                                float2 *slots)
     {
         const StepScalars &sc = a.sc;
@@ -460,7 +197,7 @@ struct StepTile {
                 if (!FULL && i >= valid)
                     vi = 0.0f;
                 v[i] = vi;
-                mx2 = fmaxf(mx2, vi);  // v' >= 0
+                mx2 = fmaxf(mx2, fabsf(vi));
             }
             if (!FULL && i >= valid)
                 mi = 0.0f;
@@ -471,9 +208,9 @@ struct StepTile {
 
         const float2 mx = group_max<S::GROUP>(make_float2(mx1, mx2), slots);
 
-        requantize<EPT, S::GROUP, false>(T1, k1, mx.x, m, c1);
+        requantize<EPT, S::GROUP, false>(T1, mx.x, m, c1);
         if constexpr (kTwo)
-            requantize<EPT, S::GROUP, true>(T2, k2, mx.y, v, c2);
+            requantize<EPT, S::GROUP, true>(T2, mx.y, v, c2);
 
         if (FULL) {
             store_f32<EPT>(D.param + e0, w);
@@ -510,12 +247,11 @@ __global__ __launch_bounds__(kThreads) void step_kernel(const StepArgs a)
     __shared__ MapTables T2;
     __shared__ float2 slots[2][kWaves];
 
-    stage_map(T1, a.q1);
+    build_tables<kThreads>(a.q1, T1.q, T1.t, T1.base, &T1.kmax);
     if constexpr (Tile::kTwo)
-        stage_map(T2, a.q2);
-    __syncthreads();
-    const int k1 = __builtin_amdgcn_readfirstlane(T1.kmax);
-    const int k2 = Tile::kTwo ? __builtin_amdgcn_readfirstlane(T2.kmax) : 0;
+        build_tables<kThreads>(a.q2, T2.q, T2.t, T2.base, &T2.kmax);
+    const Tables V1 = view(T1, __builtin_amdgcn_readfirstlane(T1.kmax));
+    const Tables V2 = view(T2, Tile::kTwo ? __builtin_amdgcn_readfirstlane(T2.kmax) : 0);
 
     int t = 0;
     int parity = 0;
@@ -526,11 +262,11 @@ __global__ __launch_bounds__(kThreads) void step_kernel(const StepArgs a)
         const int64_t t0 = (int64_t)(tile - D.tile_begin) * S::TILE;
         const int64_t e0 = t0 + (int64_t)threadIdx.x * EPT;
         if (t0 + S::TILE <= D.numel) {
-            Tile::template run<true>(a, D, T1, T2, k1, k2, e0, EPT, slots[parity]);
+            Tile::template run<true>(a, D, V1, V2, e0, EPT, slots[parity]);
         } else {
             const int64_t rem = D.numel - e0;
             const int valid = rem <= 0 ? 0 : (rem >= EPT ? EPT : (int)rem);
-            Tile::template run<false>(a, D, T1, T2, k1, k2, e0, valid, slots[parity]);
+            Tile::template run<false>(a, D, V1, V2, e0, valid, slots[parity]);
         }
     }
 }
@@ -545,7 +281,7 @@ struct QuantTile {
     static constexpr int EPT = S::EPT;
 
     template <bool FULL>
-    __device__ static void run(const MapTables &T, int kmax, const float *__restrict__ x,
+    __device__ static void run(const Tables &T, const float *__restrict__ x,
                                uint8_t *__restrict__ codes, float *__restrict__ absmax,
                                int64_t e0, int valid, float2 *slots)
     {
@@ -563,7 +299,7 @@ struct QuantTile {
             mx = fmaxf(mx, fabsf(v[i]));
         const float N = group_max<S::GROUP>(make_float2(mx, 0.0f), slots).x;
         uint32_t c[EPT];
-        requantize<EPT, S::GROUP, false>(T, kmax, N, v, c);
+        requantize<EPT, S::GROUP, false>(T, N, v, c);
         if (FULL) {
             store_codes<EPT>(codes + e0, c);
         } else {
@@ -588,55 +324,20 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const float *__restr
     constexpr int EPT = S::EPT;
     __shared__ MapTables T;
     __shared__ float2 slots[2][kWaves];
-    stage_map(T, qmap);
-    __syncthreads();
-    const int kmax = __builtin_amdgcn_readfirstlane(T.kmax);
+    build_tables<kThreads>(qmap, T.q, T.t, T.base, &T.kmax);
+    const Tables V = view(T, __builtin_amdgcn_readfirstlane(T.kmax));
 
     int parity = 0;
     for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x, parity ^= 1) {
         const int64_t t0 = tile * S::TILE;
         const int64_t e0 = t0 + (int64_t)threadIdx.x * EPT;
         if (t0 + S::TILE <= n) {
-            QuantTile<B>::template run<true>(T, kmax, x, codes, absmax, e0, EPT, slots[parity]);
+            QuantTile<B>::template run<true>(V, x, codes, absmax, e0, EPT, slots[parity]);
         } else {
             const int64_t rem = n - e0;
             const int valid = rem <= 0 ? 0 : (rem >= EPT ? EPT : (int)rem);
-            QuantTile<B>::template run<false>(T, kmax, x, codes, absmax, e0, valid,
+            QuantTile<B>::template run<false>(V, x, codes, absmax, e0, valid,
                                               slots[parity]);
-        }
-    }
-}
-
-// Dequantize: 8 elements per thread; blocksize >= 256 keeps each thread's 8
-// elements inside one block.
-__global__ __launch_bounds__(kThreads) void dequantize_kernel(const float *__restrict__ qmap,
-                                                              const uint8_t *__restrict__ codes,
-                                                              const float *__restrict__ absmax,
-                                                              int64_t n, int64_t ntiles,
-                                                              int log2_blocksize,
-                                                              float *__restrict__ out)
-{
-    constexpr int EPT = 8;
-    __shared__ float q[256];
-    q[threadIdx.x] = qmap[threadIdx.x];
-    __syncthreads();
-    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        const int64_t e0 = tile * (kThreads * EPT) + (int64_t)threadIdx.x * EPT;
-        const int64_t rem = n - e0;
-        if (rem <= 0)
-            continue;
-        const float N = absmax[e0 >> log2_blocksize];
-        if (rem >= EPT) {
-            uint32_t c[EPT];
-            float v[EPT];
-            load_codes<EPT>(codes + e0, c);
-#pragma unroll
-            for (int i = 0; i < EPT; ++i)
-                v[i] = q[c[i]] * N;
-            store_f32<EPT>(out + e0, v);
-        } else {
-            for (int i = 0; i < (int)rem; ++i)
-                out[e0 + i] = q[codes[e0 + i]] * N;
         }
     }
 }
@@ -733,19 +434,6 @@ hipError_t launch_quantize(const float *qmap, const float *x, int64_t n, int blo
     case 4096: return launch_quantize_t<4096>(qmap, x, n, codes, absmax, stream);
     default: return hipErrorInvalidValue;
     }
-}
-
-hipError_t launch_dequantize(const float *qmap, const uint8_t *codes, const float *absmax,
-                             int64_t n, int blocksize, float *out, hipStream_t stream)
-{
-    const int64_t tiles = (n + kThreads * 8 - 1) / (kThreads * 8);
-    const int64_t grid = persistent_grid(dequantize_kernel, tiles);
-    int lg = 0;
-    while ((1 << lg) < blocksize)
-        ++lg;
-    hipLaunchKernelGGL(dequantize_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream, qmap,
-                       codes, absmax, n, tiles, lg, out);
-    return hipGetLastError();
 }
 
 }  // namespace bq

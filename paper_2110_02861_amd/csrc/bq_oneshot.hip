@@ -1,0 +1,608 @@
+// One-shot kernels for gfx950: one workgroup of 512 threads per tile of 2048
+// elements (or per 4096 block), 4 contiguous elements per thread and chunk,
+// wave-contiguous non-temporal loads and stores.  The decision tables of each
+// codebook are built once per call by prepare_kernel into a prepared-codebook
+// buffer and copied from there (L2) into LDS by every workgroup.
+//
+// On MI355X this shape streams the step's byte mix (read 4 + 2 + 1 + 1 B,
+// write 4 + 1 + 1 B per element) markedly faster than persistent workgroups
+// walking a strided tile list, which is why the hot path is organised this way.
+#include "bq_device.h"
+
+namespace bq {
+namespace {
+
+using namespace dev;
+
+constexpr int kOS = 512;  // threads per workgroup
+constexpr int kOSWaves = kOS / 64;
+
+template <int B>
+struct OSShape {
+    static constexpr int CHUNKS = B == 4096 ? 2 : 1;        // chunks of 4 per thread
+    static constexpr int EPT = 4 * CHUNKS;                   // elements per thread
+    static constexpr int TILE = kOS * EPT;                   // elements per workgroup
+    static constexpr int GROUP = B >= 2048 ? kOS : B / 4;    // threads per block
+    static_assert(TILE == tile_elems(B), "tile size");
+};
+
+// ---------------------------------------------------------------------------
+// Prepare: decision tables of 1 or 2 maps (one workgroup each)
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void prepare_kernel(const float *__restrict__ q1,
+                                                      const float *__restrict__ q2,
+                                                      uint8_t *__restrict__ out)
+{
+    __shared__ float q[256];
+    __shared__ float t[256];
+    __shared__ __attribute__((aligned(16))) uint8_t base[2 * kBuckets];
+    __shared__ int kmax;
+    const float *qm = blockIdx.x == 0 ? q1 : q2;
+    build_tables<256>(qm, q, t, base, &kmax);
+    uint8_t *dst = out + (size_t)blockIdx.x * kPreparedBytes;
+    const int j = threadIdx.x;
+    reinterpret_cast<float *>(dst + kPreparedOffQ)[j] = q[j];
+    reinterpret_cast<float *>(dst + kPreparedOffT)[j] = t[j];
+    const uint32_t *bs = reinterpret_cast<const uint32_t *>(base);
+    uint32_t *bd = reinterpret_cast<uint32_t *>(dst + kPreparedOffBase);
+    for (int i = j; i < (int)(2 * kBuckets / 4); i += 256)
+        bd[i] = bs[i];
+    if (j == 0)
+        *reinterpret_cast<int *>(dst + kPreparedOffKmax) = kmax;
+}
+
+// Copy `bytes` (a multiple of 16) of a prepared map into LDS.
+__device__ inline void copy_granules(uint8_t *lds, const uint8_t *__restrict__ src, int bytes)
+{
+    for (int i = threadIdx.x; i < bytes / 16; i += blockDim.x)
+        reinterpret_cast<vu4 *>(lds)[i] = reinterpret_cast<const vu4 *>(src)[i];
+}
+
+__device__ inline Tables tables_at(const uint8_t *lds, int kmax)
+{
+    Tables M;
+    M.q = reinterpret_cast<const float *>(lds + kPreparedOffQ);
+    M.t = reinterpret_cast<const float *>(lds + kPreparedOffT);
+    M.base = lds + kPreparedOffBase;
+    M.kmax = kmax;
+    return M;
+}
+
+__device__ inline int prepared_kmax(const uint8_t *tables)
+{
+    return __builtin_amdgcn_readfirstlane(
+        *G(reinterpret_cast<const int *>(tables + kPreparedOffKmax)));
+}
+
+// ---------------------------------------------------------------------------
+// Per-block normalizers, computed once per block by wave 0
+// ---------------------------------------------------------------------------
+
+// Everything requantization needs from a block's new absmax A, for one state.
+struct BlockNorm {
+    float a;  // the absmax itself (stored to memory)
+    float n;  // scaled divisor N' (1 for an all-zero block)
+    float r;  // RN(1 / N') (0 for an all-zero block)
+    float s;  // power-of-two scale of x (1 unless A is tiny or huge)
+};
+
+__device__ inline BlockNorm block_norm(float A)
+{
+    const Normalizer z = make_normalizer(A);
+    BlockNorm b;
+    b.a = A;
+    b.n = z.n;
+    b.r = z.r;
+    b.s = z.s;
+    return b;
+}
+
+template <int N, bool NONNEG>
+__device__ inline void requantize_norm(const Tables &M, const BlockNorm &b, const float (&x)[N],
+                                       uint32_t (&c)[N])
+{
+    Normalizer z;
+    z.n = b.n;
+    z.r = b.r;
+    z.s = b.s;
+    float y[N];
+    if (__builtin_amdgcn_readfirstlane(__float_as_int(b.s)) == __float_as_int(1.0f)) {
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            y[i] = normalize<false>(z, x[i]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            y[i] = normalize<true>(z, x[i]);
+    }
+    nearest_codes<N, NONNEG>(M, y, c);
+}
+
+// LDS layout of the one-shot step workgroup.  The bucket tables sit above
+// kBucketLo bytes so that "bucket - kBucketLo" folds into the LDS instruction's
+// immediate offset.
+constexpr int kLdsQ1 = 0;                                   // float q1[256]
+constexpr int kLdsT1 = 1024;                                // float t1[256]
+constexpr int kLdsQ2 = 2048;                                // float q2[256]
+constexpr int kLdsT2 = 3072;                                // float t2[256]
+constexpr int kLdsSlots = 4096;                             // float2 slots[8]
+constexpr int kLdsNorms = 4160;                             // BlockNorm norms[8][2]
+constexpr int kLdsBase2 = (int)kBucketLo;                   // uint8 base2[+, kBuckets]
+constexpr int kLdsBase1 = kLdsBase2 + (int)kBuckets;        // uint8 base1[+/-, 2 kBuckets]
+constexpr int kLdsBytes = kLdsBase1 + 2 * (int)kBuckets;
+static_assert(kLdsNorms + 8 * 2 * (int)sizeof(BlockNorm) <= kLdsBase2, "LDS layout");
+static_assert(kLdsBase1 % 16 == 0 && kLdsBase2 % 16 == 0, "16 B granules");
+
+// Granule g (16 B) of the staged tables: source offset in the prepared pair,
+// destination offset in LDS.  Map 1: q, t, base(+/-); map 2: q, t, base(+).
+__device__ inline void granule_route(int g, bool two, int &src, int &dst)
+{
+    constexpr int kQT = 2048 / 16;                       // q and t of one map
+    constexpr int kB1 = 2 * (int)kBuckets / 16;          // both halves of map 1
+    constexpr int kB2 = (int)kBuckets / 16;              // + half of map 2
+    if (g < kQT) {                                       // map 1 q, t
+        src = 16 * g;
+        dst = kLdsQ1 + 16 * g;
+    } else if (g < kQT + kB1) {                          // map 1 base
+        src = kPreparedOffBase + 16 * (g - kQT);
+        dst = kLdsBase1 + 16 * (g - kQT);
+    } else if (two && g < 2 * kQT + kB1) {               // map 2 q, t
+        src = kPreparedBytes + 16 * (g - kQT - kB1);
+        dst = kLdsQ2 + 16 * (g - kQT - kB1);
+    } else {                                             // map 2 base (+)
+        src = kPreparedBytes + kPreparedOffBase + 16 * (g - 2 * kQT - kB1);
+        dst = kLdsBase2 + 16 * (g - 2 * kQT - kB1);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fused 8-bit optimizer step, one tile per workgroup
+// ---------------------------------------------------------------------------
+
+template <int OPT, int GRAD, int B>
+struct StepOS {
+    using S = OSShape<B>;
+    static constexpr int C = S::CHUNKS;
+    static constexpr int N = S::EPT;
+    static constexpr bool kTwo = (OPT != kMomentum);
+    static constexpr int kBPT = S::TILE / B > 0 ? S::TILE / B : 1;   // blocks per tile
+    static constexpr int kWPB = kOSWaves / kBPT;                       // waves per block
+    static constexpr int kGran = (2048 + 2 * (int)kBuckets) / 16 +
+                                 (kTwo ? (2048 + (int)kBuckets) / 16 : 0);
+    static constexpr int kGPT = (kGran + kOS - 1) / kOS;              // granules per thread
+
+    // One tile.  gran / gdst: this thread's decision-table granules, loaded by
+    // the caller before anything else so their L2 latency overlaps the HBM loads.
+    template <bool FULL>
+    __device__ static void tile(const PlanArgs &a, const TensorDesc &D, int64_t t0, uint8_t *lds,
+                                const vu4 (&gran)[kGPT], const int (&gdst)[kGPT])
+    {
+        float2 *slots = reinterpret_cast<float2 *>(lds + kLdsSlots);
+        BlockNorm *norms = reinterpret_cast<BlockNorm *>(lds + kLdsNorms);
+        const int tid = threadIdx.x;
+        const int wave = tid >> 6;
+
+        // the tile's streaming loads, kept raw until the tables are in LDS
+        vf4 wr[C], gr32[C];
+        vu2 gr16[C];
+        uint32_t k1r[C], k2r[C];
+        int valid[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            if (FULL) {
+                valid[c] = 4;
+                wr[c] = ld_nt(reinterpret_cast<const vf4 *>(D.param + e));
+                if constexpr (GRAD == kF16)
+                    gr16[c] = ld_nt(reinterpret_cast<const vu2 *>(
+                        static_cast<const _Float16 *>(D.grad) + e));
+                else
+                    gr32[c] = ld_nt(reinterpret_cast<const vf4 *>(
+                        static_cast<const float *>(D.grad) + e));
+                k1r[c] = ld_nt(reinterpret_cast<const uint32_t *>(D.s1 + e));
+                k2r[c] = kTwo ? ld_nt(reinterpret_cast<const uint32_t *>(D.s2 + e)) : 0u;
+            } else {
+                const int64_t rem = D.numel - e;
+                valid[c] = rem <= 0 ? 0 : (rem >= 4 ? 4 : (int)rem);
+                float wv[4], gv[4];
+                uint32_t a1 = 0, a2 = 0;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const bool ok = r < valid[c];
+                    const int64_t i = e + r;
+                    wv[r] = ok ? G(D.param)[i] : 0.0f;
+                    if constexpr (GRAD == kF16)
+                        gv[r] = ok ? (float)G(static_cast<const _Float16 *>(D.grad))[i] : 0.0f;
+                    else
+                        gv[r] = ok ? G(static_cast<const float *>(D.grad))[i] : 0.0f;
+                    a1 |= (ok ? (uint32_t)G(D.s1)[i] : 0u) << (8 * r);
+                    if constexpr (kTwo)
+                        a2 |= (ok ? (uint32_t)G(D.s2)[i] : 0u) << (8 * r);
+                }
+                wr[c] = vf4{wv[0], wv[1], wv[2], wv[3]};
+                gr32[c] = vf4{gv[0], gv[1], gv[2], gv[3]};
+                k1r[c] = a1;
+                k2r[c] = a2;
+            }
+        }
+        // every wave lies inside one block, so the block index and the old
+        // absmax are wave-uniform
+        const int blk = __builtin_amdgcn_readfirstlane((int)((t0 + tid * 4) / B));
+        const bool live =
+            FULL || __builtin_amdgcn_readfirstlane((int)(t0 + (tid & ~63) * 4 < D.numel));
+        const float n1 = live ? G(D.a1)[blk] : 0.0f;
+        const float n2 = (kTwo && live) ? G(D.a2)[blk] : 0.0f;
+        const int km1 = prepared_kmax(a.tables);
+        const int km2 = kTwo ? prepared_kmax(a.tables + kPreparedBytes) : 0;
+
+        // tables into LDS (threads past the last granule rewrite it, same bytes)
+#pragma unroll
+        for (int k = 0; k < kGPT; ++k)
+            *reinterpret_cast<vu4 *>(lds + gdst[k]) = gran[k];
+        __syncthreads();
+        Tables T1, T2;
+        T1.q = reinterpret_cast<const float *>(lds + kLdsQ1);
+        T1.t = reinterpret_cast<const float *>(lds + kLdsT1);
+        T1.base = lds + kLdsBase1;
+        T1.kmax = km1;
+        T2.q = reinterpret_cast<const float *>(lds + kLdsQ2);
+        T2.t = reinterpret_cast<const float *>(lds + kLdsT2);
+        T2.base = lds + kLdsBase2;
+        T2.kmax = km2;
+
+        // unpack, dequantize, 32-bit update, new absmax
+        float w[N], g[N], m[N], v[N];
+        uint32_t c1[N], c2[N];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            w[4 * c] = wr[c].x;
+            w[4 * c + 1] = wr[c].y;
+            w[4 * c + 2] = wr[c].z;
+            w[4 * c + 3] = wr[c].w;
+            if (GRAD == kF16 && FULL) {
+                g[4 * c] = half_lo(gr16[c].x);
+                g[4 * c + 1] = half_hi(gr16[c].x);
+                g[4 * c + 2] = half_lo(gr16[c].y);
+                g[4 * c + 3] = half_hi(gr16[c].y);
+            } else {
+                g[4 * c] = gr32[c].x;
+                g[4 * c + 1] = gr32[c].y;
+                g[4 * c + 2] = gr32[c].z;
+                g[4 * c + 3] = gr32[c].w;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                c1[4 * c + r] = (k1r[c] >> (8 * r)) & 0xffu;
+                c2[4 * c + r] = (k2r[c] >> (8 * r)) & 0xffu;
+            }
+        }
+        const StepScalars &sc = a.sc;
+        if (a.use_wd) {
+#pragma unroll
+            for (int i = 0; i < N; ++i)
+                g[i] = g[i] + sc.wd * w[i];
+        }
+        float mx1 = 0.0f, mx2 = 0.0f;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const bool ok = FULL || (i & 3) < valid[i / 4];
+            float wi = w[i];
+            const float gi = g[i];
+            float mi = T1.q[c1[i]] * n1;
+            if constexpr (OPT == kMomentum) {
+                mi = sc.b1 * mi + gi;
+                wi = wi - sc.lr * mi;
+            } else {
+                float vi = T2.q[c2[i]] * n2;
+                if constexpr (OPT == kAdamW)
+                    wi = wi * sc.decay;
+                mi = sc.b1 * mi + sc.omb1 * gi;
+                vi = sc.b2 * vi + sc.omb2 * (gi * gi);
+                const float denom = __builtin_amdgcn_sqrtf(vi) * sc.inv_sqrt_bc2 + sc.eps;
+                // the param update is not rounded like the oracle's anyway
+                // (hardware sqrt and reciprocal), so it may fuse
+                wi = __builtin_fmaf(-sc.step_size, mi * __builtin_amdgcn_rcpf(denom), wi);
+                v[i] = ok ? vi : 0.0f;
+                mx2 = fmaxf(mx2, fabsf(v[i]));
+            }
+            m[i] = ok ? mi : 0.0f;
+            w[i] = wi;
+            mx1 = fmaxf(mx1, fabsf(m[i]));
+        }
+
+        // block absmax: wave max -> slot; wave 0 finishes each block and
+        // computes its normalizers once
+        mx1 = row_max(mx1);
+        mx2 = row_max(mx2);
+        mx1 = dpp_max<0x142, 0xa>(mx1);
+        mx2 = dpp_max<0x142, 0xa>(mx2);
+        mx1 = dpp_max<0x143, 0xc>(mx1);
+        mx2 = dpp_max<0x143, 0xc>(mx2);
+        if ((tid & 63) == 63)
+            slots[wave] = make_float2(mx1, mx2);
+        __syncthreads();
+        if (wave == 0 && tid < kBPT) {
+            float2 r = slots[tid * kWPB];
+#pragma unroll
+            for (int k = 1; k < kWPB; ++k) {
+                const float2 o = slots[tid * kWPB + k];
+                r.x = fmaxf(r.x, o.x);
+                r.y = fmaxf(r.y, o.y);
+            }
+            norms[2 * tid] = block_norm(r.x);
+            if constexpr (kTwo)
+                norms[2 * tid + 1] = block_norm(r.y);
+        }
+        __syncthreads();
+        const int bit = wave / kWPB;  // block of this wave inside the tile
+        const BlockNorm b1 = norms[2 * bit];
+
+        // requantize
+        requantize_norm<N, false>(T1, b1, m, c1);
+        BlockNorm b2;
+        if constexpr (kTwo) {
+            b2 = norms[2 * bit + 1];
+            requantize_norm<N, true>(T2, b2, v, c2);
+        }
+
+        // store
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            if (FULL) {
+                st_nt(reinterpret_cast<vf4 *>(D.param + e),
+                      vf4{w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]});
+                st_nt(reinterpret_cast<uint32_t *>(D.s1 + e),
+                      c1[4 * c] | (c1[4 * c + 1] << 8) | (c1[4 * c + 2] << 16) |
+                          (c1[4 * c + 3] << 24));
+                if constexpr (kTwo)
+                    st_nt(reinterpret_cast<uint32_t *>(D.s2 + e),
+                          c2[4 * c] | (c2[4 * c + 1] << 8) | (c2[4 * c + 2] << 16) |
+                              (c2[4 * c + 3] << 24));
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if (r < valid[c]) {
+                        G(D.param)[e + r] = w[4 * c + r];
+                        G(D.s1)[e + r] = (uint8_t)c1[4 * c + r];
+                        if constexpr (kTwo)
+                            G(D.s2)[e + r] = (uint8_t)c2[4 * c + r];
+                    }
+                }
+            }
+        }
+        if (live && (tid & (S::GROUP - 1)) == 0) {
+            G(D.a1)[blk] = b1.a;
+            if constexpr (kTwo)
+                G(D.a2)[blk] = b2.a;
+        }
+    }
+};
+
+template <int OPT, int GRAD, int B>
+__global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
+{
+    using K = StepOS<OPT, GRAD, B>;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
+    const int tid = threadIdx.x;
+
+    // decision-table granules (L2 resident), issued first
+    vu4 gran[K::kGPT];
+    int gdst[K::kGPT];
+#pragma unroll
+    for (int k = 0; k < K::kGPT; ++k) {
+        const int gi = min(tid + k * kOS, K::kGran - 1);
+        int src;
+        granule_route(gi, K::kTwo, src, gdst[k]);
+        gran[k] = *G(reinterpret_cast<const vu4 *>(a.tables + src));
+    }
+
+    const int tile = blockIdx.x;
+    const int ti = __builtin_amdgcn_readfirstlane(G(a.tile_tensor)[tile]);
+    const gptr<const TensorDesc> dp = G(a.desc) + ti;
+    TensorDesc D;
+    D.param = dp->param;
+    D.grad = dp->grad;
+    D.s1 = dp->s1;
+    D.s2 = dp->s2;
+    D.a1 = dp->a1;
+    D.a2 = dp->a2;
+    D.numel = dp->numel;
+    D.tile_begin = dp->tile_begin;
+    const int64_t t0 = (int64_t)(tile - D.tile_begin) * K::S::TILE;
+    if (t0 + K::S::TILE <= D.numel)
+        K::template tile<true>(a, D, t0, lds, gran, gdst);
+    else
+        K::template tile<false>(a, D, t0, lds, gran, gdst);
+}
+
+// ---------------------------------------------------------------------------
+// Block-wise quantize with a prepared map, one tile per workgroup
+// ---------------------------------------------------------------------------
+
+template <int B>
+__global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__restrict__ tables,
+                                                               const float *__restrict__ x,
+                                                               int64_t n,
+                                                               uint8_t *__restrict__ codes,
+                                                               float *__restrict__ absmax)
+{
+    using S = OSShape<B>;
+    constexpr int C = S::CHUNKS;
+    constexpr int N = S::EPT;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kPreparedSignedBytes];
+    __shared__ float2 slots[kOSWaves];
+
+    const int64_t t0 = (int64_t)blockIdx.x * S::TILE;
+    const bool full = t0 + S::TILE <= n;
+    const int tid = threadIdx.x;
+    float v[N];
+    int valid[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+        const int64_t rem = n - e;
+        valid[c] = rem <= 0 ? 0 : (rem >= 4 ? 4 : (int)rem);
+        if (full) {
+            const vf4 y = ld_nt(reinterpret_cast<const vf4 *>(x + e));
+            v[4 * c] = y.x;
+            v[4 * c + 1] = y.y;
+            v[4 * c + 2] = y.z;
+            v[4 * c + 3] = y.w;
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                v[4 * c + r] = r < valid[c] ? x[e + r] : 0.0f;
+        }
+    }
+    copy_granules(lds, tables, kPreparedSignedBytes);
+    const Tables T = tables_at(lds, prepared_kmax(tables));
+    __syncthreads();
+
+    float mx = 0.0f;
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+        mx = fmaxf(mx, fabsf(v[i]));
+    const float A = group_max<S::GROUP>(make_float2(mx, 0.0f), slots).x;
+    uint32_t c[N];
+    requantize<N, S::GROUP, false>(T, A, v, c);
+#pragma unroll
+    for (int k = 0; k < C; ++k) {
+        const int64_t e = t0 + k * (kOS * 4) + tid * 4;
+        if (full) {
+            st_nt(reinterpret_cast<uint32_t *>(codes + e),
+                  c[4 * k] | (c[4 * k + 1] << 8) | (c[4 * k + 2] << 16) | (c[4 * k + 3] << 24));
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                if (r < valid[k])
+                    codes[e + r] = (uint8_t)c[4 * k + r];
+        }
+    }
+    const int64_t first = t0 + tid * 4;
+    if (first < n && (tid % S::GROUP) == 0)
+        absmax[first / B] = A;
+}
+
+// ---------------------------------------------------------------------------
+// Block-wise dequantize: out = q[code] * absmax, one tile per workgroup
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kOS) void dequantize_kernel(const float *__restrict__ qmap,
+                                                         const uint8_t *__restrict__ codes,
+                                                         const float *__restrict__ absmax,
+                                                         int64_t n, int log2_blocksize,
+                                                         float *__restrict__ out)
+{
+    __shared__ float q[256];
+    const int tid = threadIdx.x;
+    const int64_t e = (int64_t)blockIdx.x * (kOS * 4) + tid * 4;
+    uint32_t k = 0;
+    float A = 0.0f;
+    const bool full = e + 4 <= n;
+    if (full) {
+        k = ld_nt(reinterpret_cast<const uint32_t *>(codes + e));
+        A = absmax[e >> log2_blocksize];   // blocksize >= 256: 4 elements, one block
+    }
+    if (tid < 256)
+        q[tid] = qmap[tid];
+    __syncthreads();
+    if (full) {
+        const vf4 y = {q[k & 0xffu] * A, q[(k >> 8) & 0xffu] * A, q[(k >> 16) & 0xffu] * A,
+                       q[k >> 24] * A};
+        st_nt(reinterpret_cast<vf4 *>(out + e), y);
+    } else if (e < n) {
+        const float Ap = absmax[e >> log2_blocksize];
+        for (int64_t i = e; i < n; ++i)
+            out[i] = q[codes[i]] * Ap;
+    }
+}
+
+template <int OPT, int GRAD, int B>
+hipError_t launch_os_t(const PlanArgs &a, hipStream_t s)
+{
+    hipLaunchKernelGGL((step_oneshot_kernel<OPT, GRAD, B>), dim3((unsigned)a.total_tiles),
+                       dim3(kOS), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int OPT, int GRAD>
+hipError_t launch_os_b(int blocksize, const PlanArgs &a, hipStream_t s)
+{
+    switch (blocksize) {
+    case 256: return launch_os_t<OPT, GRAD, 256>(a, s);
+    case 512: return launch_os_t<OPT, GRAD, 512>(a, s);
+    case 1024: return launch_os_t<OPT, GRAD, 1024>(a, s);
+    case 2048: return launch_os_t<OPT, GRAD, 2048>(a, s);
+    case 4096: return launch_os_t<OPT, GRAD, 4096>(a, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int OPT>
+hipError_t launch_os_g(int grad_dtype, int blocksize, const PlanArgs &a, hipStream_t s)
+{
+    return grad_dtype == kF16 ? launch_os_b<OPT, kF16>(blocksize, a, s)
+                              : launch_os_b<OPT, kF32>(blocksize, a, s);
+}
+
+template <int B>
+hipError_t launch_qp_t(const uint8_t *tables, const float *x, int64_t n, uint8_t *codes,
+                       float *absmax, hipStream_t s)
+{
+    const int64_t tiles = (n + OSShape<B>::TILE - 1) / OSShape<B>::TILE;
+    hipLaunchKernelGGL((quantize_oneshot_kernel<B>), dim3((unsigned)tiles), dim3(kOS), 0, s,
+                       tables, x, n, codes, absmax);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *tables,
+                          hipStream_t stream)
+{
+    const unsigned maps = qmap2 ? 2u : 1u;
+    hipLaunchKernelGGL(prepare_kernel, dim3(maps), dim3(256), 0, stream, qmap1,
+                       qmap2 ? qmap2 : qmap1, tables);
+    return hipGetLastError();
+}
+
+hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const PlanArgs &a,
+                               hipStream_t stream)
+{
+    switch (opt) {
+    case kAdam: return launch_os_g<kAdam>(grad_dtype, blocksize, a, stream);
+    case kAdamW: return launch_os_g<kAdamW>(grad_dtype, blocksize, a, stream);
+    case kMomentum: return launch_os_g<kMomentum>(grad_dtype, blocksize, a, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_dequantize(const float *qmap, const uint8_t *codes, const float *absmax,
+                             int64_t n, int blocksize, float *out, hipStream_t stream)
+{
+    const int64_t tiles = (n + kOS * 4 - 1) / (kOS * 4);
+    int lg = 0;
+    while ((1 << lg) < blocksize)
+        ++lg;
+    hipLaunchKernelGGL(dequantize_kernel, dim3((unsigned)tiles), dim3(kOS), 0, stream, qmap,
+                       codes, absmax, n, lg, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_prepared(const uint8_t *tables, const float *x, int64_t n,
+                                    int blocksize, uint8_t *codes, float *absmax,
+                                    hipStream_t stream)
+{
+    switch (blocksize) {
+    case 256: return launch_qp_t<256>(tables, x, n, codes, absmax, stream);
+    case 512: return launch_qp_t<512>(tables, x, n, codes, absmax, stream);
+    case 1024: return launch_qp_t<1024>(tables, x, n, codes, absmax, stream);
+    case 2048: return launch_qp_t<2048>(tables, x, n, codes, absmax, stream);
+    case 4096: return launch_qp_t<4096>(tables, x, n, codes, absmax, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace bq

@@ -149,6 +149,47 @@ def test_momentum_does_not_need_second_state(L):
     assert s(2, 2048, 0, _tensors(row), 1, ctypes.byref(hp), A16, None, None) == bq.BQ_ERR_ALIGN
 
 
+def test_prepared_codebook_argument_checks(L):
+    assert L.bq_prepare_codebook(None, A16, None) == bq.BQ_ERR_NULL
+    assert L.bq_prepare_codebook(A16, None, None) == bq.BQ_ERR_NULL
+    assert L.bq_prepare_codebook(A16 + 2, A16, None) == bq.BQ_ERR_ALIGN
+    assert L.bq_prepare_codebook(A16, A16 + 4, None) == bq.BQ_ERR_ALIGN
+    q = L.bq_quantize_blockwise_prepared
+    assert q(A16, A16, -1, 2048, A16, A16, None) == bq.BQ_ERR_SIZE
+    assert q(A16, A16, 10, 3000, A16, A16, None) == bq.BQ_ERR_BLOCKSIZE
+    assert q(None, A16, 10, 2048, A16, A16, None) == bq.BQ_ERR_NULL
+    assert q(A16 + 8, A16, 10, 2048, A16, A16, None) == bq.BQ_ERR_ALIGN
+    assert q(A16, MIS, 10, 2048, A16, A16, None) == bq.BQ_ERR_ALIGN
+    assert q(A16, A16, 10, 2048, A16, A16 + 1, None) == bq.BQ_ERR_ALIGN
+    # more tiles than one grid of 512-thread workgroups can hold
+    assert q(A16, A16, (1 << 32) * 2048, 2048, A16, A16, None) == bq.BQ_ERR_SIZE
+    assert q(None, None, 0, 2048, None, None, None) == bq.BQ_OK
+
+
+def test_step_plan_argument_checks(L):
+    c = L.bq_step_plan_create
+    h = ctypes.c_void_p(123)
+    good = _tensors(_good_row())
+    assert c(0, 2048, 1, good, 1, None) == bq.BQ_ERR_NULL
+    assert c(5, 2048, 1, good, 1, ctypes.byref(h)) == bq.BQ_ERR_ENUM
+    assert h.value is None  # the handle is cleared on every error
+    assert c(0, 2048, 9, good, 1, ctypes.byref(h)) == bq.BQ_ERR_DTYPE
+    assert c(0, 100, 1, good, 1, ctypes.byref(h)) == bq.BQ_ERR_BLOCKSIZE
+    assert c(0, 2048, 1, good, -1, ctypes.byref(h)) == bq.BQ_ERR_SIZE
+    assert c(0, 2048, 1, None, 1, ctypes.byref(h)) == bq.BQ_ERR_NULL
+    assert c(0, 2048, 1, _tensors(dict(_good_row(), state2=None)), 1,
+             ctypes.byref(h)) == bq.BQ_ERR_NULL
+    assert c(0, 2048, 1, _tensors(dict(_good_row(), param=MIS)), 1,
+             ctypes.byref(h)) == bq.BQ_ERR_ALIGN
+    # tile count beyond one grid
+    big = _tensors(*[dict(_good_row(), numel=(1 << 31)) for _ in range(9)])
+    assert c(0, 2048, 1, big, 9, ctypes.byref(h)) == bq.BQ_ERR_SIZE
+    hp = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 1)
+    r = L.bq_step_plan_run
+    assert r(None, ctypes.byref(hp), A16, A16, None) == bq.BQ_ERR_NULL
+    assert L.bq_step_plan_destroy(None) == bq.BQ_OK
+
+
 def test_product_path_has_no_fallback(monkeypatch, tmp_path):
     """Without the built library the binding raises instead of computing."""
     monkeypatch.setattr(bq, "LIB_PATH", str(tmp_path / "missing.so"))

@@ -1,6 +1,7 @@
 """GPU parity at full size: the GPT-2-medium-shaped list (AdamW, 354.8M params)
 and the 1.5B-parameter LM-shaped list (Adam), stepped in one call over every
-tensor (the configuration bench.py times).
+tensor, through bq_optimizer8bit_step and through a step plan (the launch
+configuration bench.py times).
 
 The oracle cannot step 1.5B parameters in seconds, but blocks are independent
 (Section 3.1: each block is normalized by its own absmax), so it steps a sample
@@ -57,7 +58,7 @@ def sample_blocks(specs, nrandom, seed):
     return sorted(picks)
 
 
-def run_sampled(config, opt, steps, nrandom):
+def run_sampled(config, opt, steps, nrandom, path):
     hp = {k: getattr(workloads, config.upper())[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
     gdtype = workloads.GRADS[config][0]
     tdt = torch.float16 if gdtype == "float16" else torch.float32
@@ -66,7 +67,9 @@ def run_sampled(config, opt, steps, nrandom):
     say(f"{config}: allocating")
     specs, T = build_list(config, tdt)
     torch.cuda.synchronize()
-    arr = bq.make_tensor_array([(t["w"], t["g"], t["c1"], t["c2"], t["a1"], t["a2"]) for t in T])
+    rows = [(t["w"], t["g"], t["c1"], t["c2"], t["a1"], t["a2"]) for t in T]
+    arr = bq.make_tensor_array(rows)
+    plan = bq.StepPlan(opt, B, gflag, rows) if path == "plan" else None
     picks = sample_blocks(specs, nrandom, seed=17)
     hostb = {}
     for (i, b) in picks:
@@ -84,8 +87,12 @@ def run_sampled(config, opt, steps, nrandom):
         for (i, b) in picks:
             s = slice(b * B, min((b + 1) * B, specs[i].numel))
             grads[(i, b)] = host(T[i]["g"][s]).copy()
-        say(f"{config}: step t={t} over {len(specs)} tensors")
-        bq.bq_optimizer8bit_step(opt, B, gflag, (arr, len(specs)), dict(hp, step=t), qs_d, qu_d)
+        say(f"{config}: {path} step t={t} over {len(specs)} tensors")
+        if plan is not None:
+            plan.run(dict(hp, step=t), qs_d, qu_d)
+        else:
+            bq.bq_optimizer8bit_step(opt, B, gflag, (arr, len(specs)), dict(hp, step=t),
+                                     qs_d, qu_d)
         torch.cuda.synchronize()
         for (i, b), hb in hostb.items():
             prev = hb["w"].astype(np.float64)
@@ -104,9 +111,12 @@ def run_sampled(config, opt, steps, nrandom):
     say(f"{config}: {len(picks)} sampled blocks matched over {steps} steps")
 
 
-def test_gpt2_medium_adamw_sampled():
-    run_sampled("c4", "adamw", steps=3, nrandom=256)
+@pytest.mark.parametrize("path", ["call", "plan"])
+def test_gpt2_medium_adamw_sampled(path):
+    run_sampled("c4", "adamw", steps=3, nrandom=256, path=path)
 
 
-def test_lm_1p5b_adam_sampled():
-    run_sampled("c5", "adam", steps=3, nrandom=512)
+@pytest.mark.parametrize("path", ["call", "plan"])
+def test_lm_1p5b_adam_sampled(path):
+    """The bench workload; "plan" is the launch configuration bench.py times."""
+    run_sampled("c5", "adam", steps=3, nrandom=512, path=path)

@@ -18,11 +18,15 @@ BLOCKSIZES = [256, 512, 1024, 2048, 4096]
 
 def run_pair(qmap_h, qmap_d, x, B):
     say(f"quantize n={x.size} B={B}")
-    c_d, a_d = bq.bq_quantize_blockwise(qmap_d, dev(x), B)
+    x_d = dev(x)
+    c_d, a_d = bq.bq_quantize_blockwise(qmap_d, x_d, B)
+    prep = bq.bq_prepare_codebook(qmap_d)
+    c_p, a_p = bq.bq_quantize_blockwise_prepared(prep, x_d, B)
     torch.cuda.synchronize()
     c_ref, a_ref = oracle.quantize_blockwise(qmap_h, x, B)
-    np.testing.assert_array_equal(host(a_d).view(np.uint32), a_ref.view(np.uint32))
-    np.testing.assert_array_equal(host(c_d), c_ref)
+    for c, a in ((c_d, a_d), (c_p, a_p)):
+        np.testing.assert_array_equal(host(a).view(np.uint32), a_ref.view(np.uint32))
+        np.testing.assert_array_equal(host(c), c_ref)
     say(f"dequantize n={x.size} B={B}")
     out = bq.bq_dequantize_blockwise(qmap_d, c_d, a_d, B)
     torch.cuda.synchronize()
@@ -113,10 +117,12 @@ def test_full_size_student_t(B):
     x_d = dev(x)
     c_d, a_d = bq.bq_quantize_blockwise(qs_d, x_d, B)
     out_d = bq.bq_dequantize_blockwise(qs_d, c_d, a_d, B)
+    c_p, a_p = bq.bq_quantize_blockwise_prepared(bq.bq_prepare_codebook(qs_d), x_d, B)
     torch.cuda.synchronize()
     c_ref, a_ref = oracle.quantize_blockwise(qs, x, B)
-    np.testing.assert_array_equal(host(a_d).view(np.uint32), a_ref.view(np.uint32))
-    np.testing.assert_array_equal(host(c_d), c_ref)
+    for c, a in ((c_d, a_d), (c_p, a_p)):
+        np.testing.assert_array_equal(host(a).view(np.uint32), a_ref.view(np.uint32))
+        np.testing.assert_array_equal(host(c), c_ref)
     ref = oracle.dequantize_blockwise(qs, c_ref, a_ref, B)
     np.testing.assert_array_equal(host(out_d).view(np.uint32), ref.view(np.uint32))
 

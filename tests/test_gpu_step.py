@@ -25,7 +25,7 @@ HPS = {
 }
 
 
-def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=True):
+def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=True, path="plan"):
     qs, qu, qs_d, qu_d = codebooks_on_device()
     two = opt != "momentum"
     hp = dict(HPS[opt] if hp is None else hp)
@@ -38,6 +38,7 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
         hs.append(HostState(w, B, two))
         ds.append(DevState(w, B, two, tdt))
     arr = bq.make_tensor_array([d.row() for d in ds])
+    plan = bq.StepPlan(opt, B, grad_dtype, [d.row() for d in ds]) if path == "plan" else None
     for t in range(1, steps + 1):
         grads = []
         for i, n in enumerate(sizes):
@@ -47,9 +48,12 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
             g = g.astype(ndt)
             grads.append(g)
             ds[i].g.copy_(torch.from_numpy(g))
-        say(f"step opt={opt} B={B} grad={ndt.__name__} tensors={len(sizes)} t={t}")
-        bq.bq_optimizer8bit_step(opt, B, grad_dtype, (arr, len(ds)), dict(hp, step=t),
-                                 qs_d, qu_d if two else None)
+        say(f"step {path} opt={opt} B={B} grad={ndt.__name__} tensors={len(sizes)} t={t}")
+        if plan is not None:
+            plan.run(dict(hp, step=t), qs_d, qu_d if two else None)
+        else:
+            bq.bq_optimizer8bit_step(opt, B, grad_dtype, (arr, len(ds)), dict(hp, step=t),
+                                     qs_d, qu_d if two else None)
         torch.cuda.synchronize()
         for i in range(len(sizes)):
             hs[i].step(opt, B, grads[i], qs, qu if two else None, hp, t)
@@ -71,22 +75,28 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
 RAGGED = [1, 255, 256, 257, 2047, 2048, 2049, 4095, 4096, 4097, 3 * 4096 + 77, 20000]
 
 
+PATHS = ["call", "plan"]
+
+
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("opt", ["adam", "adamw", "momentum"])
 @pytest.mark.parametrize("grad_dtype", [bq.BQ_F16, bq.BQ_F32])
 @pytest.mark.parametrize("B", [256, 512, 1024, 2048, 4096])
-def test_ragged_list(opt, grad_dtype, B):
-    run_lists(opt, B, grad_dtype, RAGGED, steps=3)
+def test_ragged_list(opt, grad_dtype, B, path):
+    run_lists(opt, B, grad_dtype, RAGGED, steps=3, path=path)
 
 
-def test_adam_l2_weight_decay():
+@pytest.mark.parametrize("path", PATHS)
+def test_adam_l2_weight_decay(path):
     """Adam's L2 term feeds the param into the gradient, so a param that differs
     by an ulp (hardware sqrt / reciprocal) can move a state across a code
     boundary: codes agree on >= 99.99% and differ by at most one."""
     hp = dict(HPS["adam"], wd=1e-2)
-    run_lists("adam", 2048, bq.BQ_F16, RAGGED, steps=3, hp=hp, exact_codes=False)
+    run_lists("adam", 2048, bq.BQ_F16, RAGGED, steps=3, hp=hp, exact_codes=False, path=path)
 
 
-def test_c1_adam_ten_steps():
+@pytest.mark.parametrize("path", PATHS)
+def test_c1_adam_ten_steps(path):
     """One fp32 tensor of 1,048,576 params, fp16 grads, Adam, 10 steps from zero.
 
     Free-running: both sides chain their own steps; codes and absmax stay
@@ -102,14 +112,22 @@ def test_c1_adam_ten_steps():
     f = DevState(w, 2048, True, torch.float16)
     arr_d = bq.make_tensor_array([d.row()])
     arr_f = bq.make_tensor_array([f.row()])
+    plans = (bq.StepPlan("adam", 2048, bq.BQ_F16, [d.row()]),
+             bq.StepPlan("adam", 2048, bq.BQ_F16, [f.row()])) if path == "plan" else None
     for t in range(1, 11):
         g = workloads.grad_host("c1", spec, workloads.host_rng(0, "c1", 0, t))
         d.g.copy_(torch.from_numpy(g))
         f.g.copy_(torch.from_numpy(g))
         f.load(h)
-        say(f"C1 step t={t}")
-        bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F16, (arr_d, 1), dict(hp, step=t), qs_d, qu_d)
-        bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F16, (arr_f, 1), dict(hp, step=t), qs_d, qu_d)
+        say(f"C1 {path} step t={t}")
+        if plans is not None:
+            plans[0].run(dict(hp, step=t), qs_d, qu_d)
+            plans[1].run(dict(hp, step=t), qs_d, qu_d)
+        else:
+            bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F16, (arr_d, 1), dict(hp, step=t),
+                                     qs_d, qu_d)
+            bq.bq_optimizer8bit_step("adam", 2048, bq.BQ_F16, (arr_f, 1), dict(hp, step=t),
+                                     qs_d, qu_d)
         torch.cuda.synchronize()
         h.step("adam", 2048, g, qs, qu, hp, t)
         for dev_state, tol, kind in ((d, h.tol, "free"), (f, h.step_tol, "one step")):
@@ -121,16 +139,19 @@ def test_c1_adam_ten_steps():
             np.testing.assert_array_equal(host(dev_state.a2), h.a2)
 
 
-def test_many_tensors_chunked_launches():
-    """More tensors than one launch's descriptor capacity (56)."""
+@pytest.mark.parametrize("path", PATHS)
+def test_many_tensors_chunked_launches(path):
+    """More tensors than one launch's descriptor capacity (56), with empty ones."""
     sizes = [64 * (i % 7 + 1) + (i * 37) % 2048 for i in range(150)]
-    run_lists("adam", 2048, bq.BQ_F16, sizes, steps=2, seed=3)
+    sizes[5] = sizes[77] = 0
+    run_lists("adam", 2048, bq.BQ_F16, sizes, steps=2, seed=3, path=path)
 
 
-def test_resnet50_momentum_list():
+@pytest.mark.parametrize("path", PATHS)
+def test_resnet50_momentum_list(path):
     """161 ResNet-50 tensors (99 smaller than one block), fp32 grads, Momentum."""
     sizes = [s.numel for s in workloads.resnet50_specs()]
-    run_lists("momentum", 2048, bq.BQ_F32, sizes, steps=3, seed=4)
+    run_lists("momentum", 2048, bq.BQ_F32, sizes, steps=3, seed=4, path=path)
 
 
 def test_zero_gradient_keeps_zero_state():
