@@ -54,7 +54,8 @@ bq_status from_hip(hipError_t e) { return e == hipSuccess ? BQ_OK : BQ_ERR_HIP; 
 // Checks every descriptor of a tensor list (no HIP call).
 bq_status check_tensors(const bq_tensor *tensors, int32_t ntensors, int32_t blocksize, bool two)
 {
-    const int64_t tile = bq::tile_elems(blocksize);
+    const int64_t tile = bq::tile_elems(blocksize) < bq::kStepTile ? bq::tile_elems(blocksize)
+                                                                    : bq::kStepTile;
     for (int32_t i = 0; i < ntensors; ++i) {
         const bq_tensor &t = tensors[i];
         if (t.numel < 0)
@@ -283,7 +284,7 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
     if (st != BQ_OK)
         return st;
 
-    const int64_t tile = bq::tile_elems(blocksize);
+    const int64_t tile = bq::kStepTile;
     std::vector<bq::TensorDesc> desc;
     std::vector<int32_t> tile_tensor;
     int64_t tiles = 0;

@@ -151,7 +151,7 @@ __device__ inline uint32_t bucket_of(float y)
         return min(max(u >> kBucketShift, kBucketLo), kBucketHi) - kBucketLo;
     } else {
         const uint32_t a = (u & 0x7fffffffu) >> kBucketShift;
-        return min(max(a, kBucketLo), kBucketHi) - kBucketLo + (u >> 31) * kBuckets;
+        return (u >> 31) * kBuckets + (min(max(a, kBucketLo), kBucketHi) - kBucketLo);
     }
 }
 
@@ -225,47 +225,58 @@ __device__ inline void requantize(const Tables &M, float A, const float (&x)[N],
 // Reductions
 // ---------------------------------------------------------------------------
 
+// Unsigned max with a DPP-shifted copy of v, foldable into one v_max_u32 with
+// a DPP operand.  Lanes of rows that ROW_MASK disables receive an unspecified
+// value; the reduction below only relies on the lanes each step enables.
+// Non-negative floats order like their bit patterns, so block absmax
+// reductions run on the bits: exact, and free of NaN canonicalization.
 template <int CTRL, int ROW_MASK>
-__device__ inline float dpp_max(float v)
+__device__ inline uint32_t dpp_umax(uint32_t v)
 {
-    const int iv = __builtin_bit_cast(int, v);
-    const int o = __builtin_amdgcn_update_dpp(iv, iv, CTRL, ROW_MASK, 0xf, false);
-    return fmaxf(v, __builtin_bit_cast(float, o));
+    const uint32_t o = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, ROW_MASK, 0xf, true);
+    return max(v, o);
 }
 
-// Max over each row of 16 lanes, left in every lane of the row.
-__device__ inline float row_max(float v)
+// Max of non-negative bit patterns over the wave, valid in lane 63 only.
+__device__ inline uint32_t wave_umax_lane63(uint32_t v)
 {
-    v = dpp_max<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
-    v = dpp_max<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
-    v = dpp_max<0x141, 0xf>(v);  // row_half_mirror
-    v = dpp_max<0x140, 0xf>(v);  // row_mirror
+    v = dpp_umax<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
+    v = dpp_umax<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
+    v = dpp_umax<0x141, 0xf>(v);  // row_half_mirror
+    v = dpp_umax<0x140, 0xf>(v);  // row_mirror: every lane holds its row max
+    v = dpp_umax<0x142, 0xa>(v);  // row_bcast:15 -> rows 1, 3 hold pair maxima
+    v = dpp_umax<0x143, 0xc>(v);  // row_bcast:31 -> lane 63 holds the wave max
     return v;
 }
 
-__device__ inline float lane_f(float v, int lane)
-{
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
-}
-
-// Max of (x, y) over each group of GROUP consecutive threads (power of two,
-// 32..1024).  slots: LDS scratch of (threads / 64) float2 not in use by another
-// reduction of the same workgroup.  Contains a barrier when GROUP > 64.
+// Max of non-negative (x, y) over each group of GROUP consecutive threads
+// (power of two, 32..1024), returned to every thread of the group.  slots: LDS
+// scratch of (threads / 64) float2 not in use by another reduction of the same
+// workgroup.  Contains a barrier when GROUP > 64.
 template <int GROUP>
 __device__ inline float2 group_max(float2 v, float2 *slots)
 {
-    v.x = row_max(v.x);
-    v.y = row_max(v.y);
-    v.x = dpp_max<0x142, 0xa>(v.x);  // row_bcast:15 -> lanes 31, 63 hold half maxima
-    v.y = dpp_max<0x142, 0xa>(v.y);
+    uint32_t x = __float_as_uint(v.x), y = __float_as_uint(v.y);
+    x = dpp_umax<0xb1, 0xf>(x);
+    y = dpp_umax<0xb1, 0xf>(y);
+    x = dpp_umax<0x4e, 0xf>(x);
+    y = dpp_umax<0x4e, 0xf>(y);
+    x = dpp_umax<0x141, 0xf>(x);
+    y = dpp_umax<0x141, 0xf>(y);
+    x = dpp_umax<0x140, 0xf>(x);
+    y = dpp_umax<0x140, 0xf>(y);
+    x = dpp_umax<0x142, 0xa>(x);  // row_bcast:15 -> lanes 31, 63 hold half maxima
+    y = dpp_umax<0x142, 0xa>(y);
     if constexpr (GROUP == 32) {
         const bool hi = (threadIdx.x & 32) != 0;
-        return make_float2(hi ? lane_f(v.x, 63) : lane_f(v.x, 31),
-                           hi ? lane_f(v.y, 63) : lane_f(v.y, 31));
+        const uint32_t x31 = __builtin_amdgcn_readlane(x, 31), x63 = __builtin_amdgcn_readlane(x, 63);
+        const uint32_t y31 = __builtin_amdgcn_readlane(y, 31), y63 = __builtin_amdgcn_readlane(y, 63);
+        return make_float2(__uint_as_float(hi ? x63 : x31), __uint_as_float(hi ? y63 : y31));
     } else {
-        v.x = dpp_max<0x143, 0xc>(v.x);  // row_bcast:31 -> lane 63 holds the wave max
-        v.y = dpp_max<0x143, 0xc>(v.y);
-        const float2 w = make_float2(lane_f(v.x, 63), lane_f(v.y, 63));
+        x = dpp_umax<0x143, 0xc>(x);  // row_bcast:31 -> lane 63 holds the wave max
+        y = dpp_umax<0x143, 0xc>(y);
+        const float2 w = make_float2(__uint_as_float(__builtin_amdgcn_readlane(x, 63)),
+                                     __uint_as_float(__builtin_amdgcn_readlane(y, 63)));
         if constexpr (GROUP == 64) {
             return w;
         } else {

@@ -47,8 +47,13 @@ struct StepArgs {
 };
 static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must stay below 4 KiB");
 
-// Elements per tile (one workgroup iteration) for a given blocksize.
+// Elements per tile (one workgroup iteration) for a given blocksize, for the
+// persistent kernels and the one-shot quantize kernel.
 constexpr int tile_elems(int blocksize) { return blocksize >= 2048 ? blocksize : 2048; }
+
+// Elements per tile of the one-shot step kernel (every blocksize): 512
+// threads x 8 elements, i.e. 4096 / B whole blocks.
+constexpr int kStepTile = 4096;
 
 // Prepared codebook: decision tables of one map in device memory, built once
 // by the prepare kernel and copied into LDS by every workgroup.

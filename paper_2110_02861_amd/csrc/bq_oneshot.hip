@@ -119,66 +119,48 @@ __device__ inline void requantize_norm(const Tables &M, const BlockNorm &b, cons
     nearest_codes<N, NONNEG>(M, y, c);
 }
 
-// LDS layout of the one-shot step workgroup.  The bucket tables sit above
-// kBucketLo bytes so that "bucket - kBucketLo" folds into the LDS instruction's
-// immediate offset.
-constexpr int kLdsQ1 = 0;                                   // float q1[256]
-constexpr int kLdsT1 = 1024;                                // float t1[256]
-constexpr int kLdsQ2 = 2048;                                // float q2[256]
-constexpr int kLdsT2 = 3072;                                // float t2[256]
-constexpr int kLdsSlots = 4096;                             // float2 slots[8]
-constexpr int kLdsNorms = 4160;                             // BlockNorm norms[8][2]
-constexpr int kLdsBase2 = (int)kBucketLo;                   // uint8 base2[+, kBuckets]
-constexpr int kLdsBase1 = kLdsBase2 + (int)kBuckets;        // uint8 base1[+/-, 2 kBuckets]
-constexpr int kLdsBytes = kLdsBase1 + 2 * (int)kBuckets;
-static_assert(kLdsNorms + 8 * 2 * (int)sizeof(BlockNorm) <= kLdsBase2, "LDS layout");
-static_assert(kLdsBase1 % 16 == 0 && kLdsBase2 % 16 == 0, "16 B granules");
-
-// Granule g (16 B) of the staged tables: source offset in the prepared pair,
-// destination offset in LDS.  Map 1: q, t, base(+/-); map 2: q, t, base(+).
-__device__ inline void granule_route(int g, bool two, int &src, int &dst)
-{
-    constexpr int kQT = 2048 / 16;                       // q and t of one map
-    constexpr int kB1 = 2 * (int)kBuckets / 16;          // both halves of map 1
-    constexpr int kB2 = (int)kBuckets / 16;              // + half of map 2
-    if (g < kQT) {                                       // map 1 q, t
-        src = 16 * g;
-        dst = kLdsQ1 + 16 * g;
-    } else if (g < kQT + kB1) {                          // map 1 base
-        src = kPreparedOffBase + 16 * (g - kQT);
-        dst = kLdsBase1 + 16 * (g - kQT);
-    } else if (two && g < 2 * kQT + kB1) {               // map 2 q, t
-        src = kPreparedBytes + 16 * (g - kQT - kB1);
-        dst = kLdsQ2 + 16 * (g - kQT - kB1);
-    } else {                                             // map 2 base (+)
-        src = kPreparedBytes + kPreparedOffBase + 16 * (g - 2 * kQT - kB1);
-        dst = kLdsBase2 + 16 * (g - 2 * kQT - kB1);
-    }
-}
+// LDS layout of the one-shot step workgroup: the prepared bytes of map 1 (q, t,
+// both bucket halves) followed by those of map 2 (q, t, + half), placed so that
+// map 1's bucket table starts at byte kBucketLo: "bucket - kBucketLo" then folds
+// into the LDS instruction's immediate offset.  The pad in front holds the
+// reduction slots and the per-block normalizers.
+constexpr int kLdsSlots = 0;                                    // uint2 slots[16]
+constexpr int kLdsNorms = 128;                                  // BlockNorm norms[16][2]
+constexpr int kLdsMap1 = (int)kBucketLo - kPreparedOffBase;     // 11008
+constexpr int kLdsMap2 = kLdsMap1 + kPreparedSignedBytes;
+constexpr int kLdsBytes = kLdsMap2 + kPreparedNonnegBytes;
+static_assert(kLdsNorms + 16 * 2 * (int)sizeof(BlockNorm) <= kLdsMap1, "LDS layout");
+static_assert(kLdsMap1 % 16 == 0 && kLdsMap2 % 16 == 0, "16 B granules");
 
 // ---------------------------------------------------------------------------
 // Fused 8-bit optimizer step, one tile per workgroup
 // ---------------------------------------------------------------------------
 
+// One tile of the step: 4096 elements, 512 threads, two chunks of 4 contiguous
+// elements per thread (chunk c of thread t starts at element c*2048 + 4t).
+// Element groups of 256 (one wave and chunk) are "segments"; segment s = 8c + w
+// covers tile elements [256 s, 256 s + 256), so block b of the tile is made of
+// segments [b B/256, (b+1) B/256).
 template <int OPT, int GRAD, int B>
 struct StepOS {
-    using S = OSShape<B>;
-    static constexpr int C = S::CHUNKS;
-    static constexpr int N = S::EPT;
+    static constexpr int C = 2;                         // chunks per thread
+    static constexpr int N = 4 * C;                     // elements per thread
+    static constexpr int TILE = kStepTile;
+    static_assert(TILE == kOS * N, "tile size");
     static constexpr bool kTwo = (OPT != kMomentum);
-    static constexpr int kBPT = S::TILE / B > 0 ? S::TILE / B : 1;   // blocks per tile
-    static constexpr int kWPB = kOSWaves / kBPT;                       // waves per block
-    static constexpr int kGran = (2048 + 2 * (int)kBuckets) / 16 +
-                                 (kTwo ? (2048 + (int)kBuckets) / 16 : 0);
-    static constexpr int kGPT = (kGran + kOS - 1) / kOS;              // granules per thread
+    static constexpr int kBPT = TILE / B;               // blocks per tile
+    static constexpr int kSPB = B / 256;                // segments per block
+    static constexpr int kGran1 = kPreparedSignedBytes / 16;      // map 1 granules
+    static constexpr int kGran = kGran1 + (kTwo ? kPreparedNonnegBytes / 16 : 0);
+    static constexpr int kGPT = (kGran + kOS - 1) / kOS;          // granules per thread
 
-    // One tile.  gran / gdst: this thread's decision-table granules, loaded by
-    // the caller before anything else so their L2 latency overlaps the HBM loads.
+    // One tile.  gran: this thread's decision-table granules, loaded by the
+    // caller before anything else so their L2 latency overlaps the HBM loads.
     template <bool FULL>
     __device__ static void tile(const PlanArgs &a, const TensorDesc &D, int64_t t0, uint8_t *lds,
-                                const vu4 (&gran)[kGPT], const int (&gdst)[kGPT])
+                                const vu4 (&gran)[kGPT])
     {
-        float2 *slots = reinterpret_cast<float2 *>(lds + kLdsSlots);
+        uint2 *slots = reinterpret_cast<uint2 *>(lds + kLdsSlots);
         BlockNorm *norms = reinterpret_cast<BlockNorm *>(lds + kLdsNorms);
         const int tid = threadIdx.x;
         const int wave = tid >> 6;
@@ -226,32 +208,38 @@ struct StepOS {
                 k2r[c] = a2;
             }
         }
-        // every wave lies inside one block, so the block index and the old
-        // absmax are wave-uniform
-        const int blk = __builtin_amdgcn_readfirstlane((int)((t0 + tid * 4) / B));
-        const bool live =
-            FULL || __builtin_amdgcn_readfirstlane((int)(t0 + (tid & ~63) * 4 < D.numel));
-        const float n1 = live ? G(D.a1)[blk] : 0.0f;
-        const float n2 = (kTwo && live) ? G(D.a2)[blk] : 0.0f;
+        // old absmax of the block of each chunk (wave-uniform: a segment lies
+        // inside one block); a block exists iff its first element does
+        const int blk0 = (int)(t0 / B);
+        float n1[C], n2[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int seg = 8 * c + wave;
+            const int b = seg / kSPB;
+            const bool live = FULL || t0 + (int64_t)b * B < D.numel;
+            n1[c] = live ? G(D.a1)[blk0 + b] : 0.0f;
+            n2[c] = (kTwo && live) ? G(D.a2)[blk0 + b] : 0.0f;
+        }
         const int km1 = prepared_kmax(a.tables);
         const int km2 = kTwo ? prepared_kmax(a.tables + kPreparedBytes) : 0;
 
         // tables into LDS (threads past the last granule rewrite it, same bytes)
 #pragma unroll
         for (int k = 0; k < kGPT; ++k)
-            *reinterpret_cast<vu4 *>(lds + gdst[k]) = gran[k];
+            reinterpret_cast<vu4 *>(lds + kLdsMap1)[min((int)threadIdx.x + k * kOS, kGran - 1)] =
+                gran[k];
         __syncthreads();
         Tables T1, T2;
-        T1.q = reinterpret_cast<const float *>(lds + kLdsQ1);
-        T1.t = reinterpret_cast<const float *>(lds + kLdsT1);
-        T1.base = lds + kLdsBase1;
+        T1.q = reinterpret_cast<const float *>(lds + kLdsMap1 + kPreparedOffQ);
+        T1.t = reinterpret_cast<const float *>(lds + kLdsMap1 + kPreparedOffT);
+        T1.base = lds + kLdsMap1 + kPreparedOffBase;
         T1.kmax = km1;
-        T2.q = reinterpret_cast<const float *>(lds + kLdsQ2);
-        T2.t = reinterpret_cast<const float *>(lds + kLdsT2);
-        T2.base = lds + kLdsBase2;
+        T2.q = reinterpret_cast<const float *>(lds + kLdsMap2 + kPreparedOffQ);
+        T2.t = reinterpret_cast<const float *>(lds + kLdsMap2 + kPreparedOffT);
+        T2.base = lds + kLdsMap2 + kPreparedOffBase;
         T2.kmax = km2;
 
-        // unpack, dequantize, 32-bit update, new absmax
+        // unpack, dequantize, 32-bit update, new absmax per chunk
         float w[N], g[N], m[N], v[N];
         uint32_t c1[N], c2[N];
 #pragma unroll
@@ -283,67 +271,90 @@ struct StepOS {
             for (int i = 0; i < N; ++i)
                 g[i] = g[i] + sc.wd * w[i];
         }
-        float mx1 = 0.0f, mx2 = 0.0f;
+        float mx1[C], mx2[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            mx1[c] = 0.0f;
+            mx2[c] = 0.0f;
+        }
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-            const bool ok = FULL || (i & 3) < valid[i / 4];
+            const int c = i / 4;
+            const bool ok = FULL || (i & 3) < valid[c];
             float wi = w[i];
             const float gi = g[i];
-            float mi = T1.q[c1[i]] * n1;
+            float mi = T1.q[c1[i]] * n1[c];
             if constexpr (OPT == kMomentum) {
                 mi = sc.b1 * mi + gi;
                 wi = wi - sc.lr * mi;
             } else {
-                float vi = T2.q[c2[i]] * n2;
+                float vi = T2.q[c2[i]] * n2[c];
                 if constexpr (OPT == kAdamW)
                     wi = wi * sc.decay;
                 mi = sc.b1 * mi + sc.omb1 * gi;
                 vi = sc.b2 * vi + sc.omb2 * (gi * gi);
-                const float denom = __builtin_amdgcn_sqrtf(vi) * sc.inv_sqrt_bc2 + sc.eps;
                 // the param update is not rounded like the oracle's anyway
                 // (hardware sqrt and reciprocal), so it may fuse
+                const float denom =
+                    __builtin_fmaf(__builtin_amdgcn_sqrtf(vi), sc.inv_sqrt_bc2, sc.eps);
                 wi = __builtin_fmaf(-sc.step_size, mi * __builtin_amdgcn_rcpf(denom), wi);
                 v[i] = ok ? vi : 0.0f;
-                mx2 = fmaxf(mx2, fabsf(v[i]));
+                mx2[c] = fmaxf(mx2[c], fabsf(v[i]));
             }
             m[i] = ok ? mi : 0.0f;
             w[i] = wi;
-            mx1 = fmaxf(mx1, fabsf(m[i]));
+            mx1[c] = fmaxf(mx1[c], fabsf(m[i]));
         }
 
-        // block absmax: wave max -> slot; wave 0 finishes each block and
-        // computes its normalizers once
-        mx1 = row_max(mx1);
-        mx2 = row_max(mx2);
-        mx1 = dpp_max<0x142, 0xa>(mx1);
-        mx2 = dpp_max<0x142, 0xa>(mx2);
-        mx1 = dpp_max<0x143, 0xc>(mx1);
-        mx2 = dpp_max<0x143, 0xc>(mx2);
-        if ((tid & 63) == 63)
-            slots[wave] = make_float2(mx1, mx2);
+        // block absmax (on the bit patterns of the non-negative maxima): wave
+        // max per segment -> slot; wave 0 finishes each block, computes its
+        // normalizers once and stores the new absmax
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const uint32_t u1 = wave_umax_lane63(__float_as_uint(mx1[c]));
+            const uint32_t u2 = kTwo ? wave_umax_lane63(__float_as_uint(mx2[c])) : 0u;
+            if ((tid & 63) == 63)
+                slots[8 * c + wave] = make_uint2(u1, u2);
+        }
         __syncthreads();
         if (wave == 0 && tid < kBPT) {
-            float2 r = slots[tid * kWPB];
+            uint2 r = slots[tid * kSPB];
 #pragma unroll
-            for (int k = 1; k < kWPB; ++k) {
-                const float2 o = slots[tid * kWPB + k];
-                r.x = fmaxf(r.x, o.x);
-                r.y = fmaxf(r.y, o.y);
+            for (int k = 1; k < kSPB; ++k) {
+                const uint2 o = slots[tid * kSPB + k];
+                r.x = max(r.x, o.x);
+                r.y = max(r.y, o.y);
             }
-            norms[2 * tid] = block_norm(r.x);
+            norms[2 * tid] = block_norm(__uint_as_float(r.x));
             if constexpr (kTwo)
-                norms[2 * tid + 1] = block_norm(r.y);
+                norms[2 * tid + 1] = block_norm(__uint_as_float(r.y));
+            if (FULL || t0 + (int64_t)tid * B < D.numel) {
+                G(D.a1)[blk0 + tid] = __uint_as_float(r.x);
+                if constexpr (kTwo)
+                    G(D.a2)[blk0 + tid] = __uint_as_float(r.y);
+            }
         }
         __syncthreads();
-        const int bit = wave / kWPB;  // block of this wave inside the tile
-        const BlockNorm b1 = norms[2 * bit];
 
-        // requantize
-        requantize_norm<N, false>(T1, b1, m, c1);
-        BlockNorm b2;
-        if constexpr (kTwo) {
-            b2 = norms[2 * bit + 1];
-            requantize_norm<N, true>(T2, b2, v, c2);
+        // requantize, chunk by chunk (each chunk lies in one block)
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int b = (8 * c + wave) / kSPB;
+            float mc[4], vc[4];
+            uint32_t q1[4], q2[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                mc[r] = m[4 * c + r];
+                vc[r] = v[4 * c + r];
+            }
+            requantize_norm<4, false>(T1, norms[2 * b], mc, q1);
+            if constexpr (kTwo)
+                requantize_norm<4, true>(T2, norms[2 * b + 1], vc, q2);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                c1[4 * c + r] = q1[r];
+                c2[4 * c + r] = kTwo ? q2[r] : 0u;
+            }
         }
 
         // store
@@ -372,11 +383,6 @@ struct StepOS {
                 }
             }
         }
-        if (live && (tid & (S::GROUP - 1)) == 0) {
-            G(D.a1)[blk] = b1.a;
-            if constexpr (kTwo)
-                G(D.a2)[blk] = b2.a;
-        }
     }
 };
 
@@ -387,14 +393,14 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
     __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
     const int tid = threadIdx.x;
 
-    // decision-table granules (L2 resident), issued first
+    // decision-table granules (L2 resident), issued first: granule g of the
+    // LDS image comes from prepared byte 16 g (map 1) or 16 g + 16 (map 2,
+    // which starts 16 B after map 1's last staged byte)
     vu4 gran[K::kGPT];
-    int gdst[K::kGPT];
 #pragma unroll
     for (int k = 0; k < K::kGPT; ++k) {
         const int gi = min(tid + k * kOS, K::kGran - 1);
-        int src;
-        granule_route(gi, K::kTwo, src, gdst[k]);
+        const int src = 16 * gi + (gi >= K::kGran1 ? kPreparedBytes - kPreparedSignedBytes : 0);
         gran[k] = *G(reinterpret_cast<const vu4 *>(a.tables + src));
     }
 
@@ -410,11 +416,11 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
     D.a2 = dp->a2;
     D.numel = dp->numel;
     D.tile_begin = dp->tile_begin;
-    const int64_t t0 = (int64_t)(tile - D.tile_begin) * K::S::TILE;
-    if (t0 + K::S::TILE <= D.numel)
-        K::template tile<true>(a, D, t0, lds, gran, gdst);
+    const int64_t t0 = (int64_t)(tile - D.tile_begin) * K::TILE;
+    if (t0 + K::TILE <= D.numel)
+        K::template tile<true>(a, D, t0, lds, gran);
     else
-        K::template tile<false>(a, D, t0, lds, gran, gdst);
+        K::template tile<false>(a, D, t0, lds, gran);
 }
 
 // ---------------------------------------------------------------------------

@@ -182,8 +182,8 @@ def test_step_plan_argument_checks(L):
     assert c(0, 2048, 1, _tensors(dict(_good_row(), param=MIS)), 1,
              ctypes.byref(h)) == bq.BQ_ERR_ALIGN
     # tile count beyond one grid
-    big = _tensors(*[dict(_good_row(), numel=(1 << 31)) for _ in range(9)])
-    assert c(0, 2048, 1, big, 9, ctypes.byref(h)) == bq.BQ_ERR_SIZE
+    big = _tensors(*[dict(_good_row(), numel=(1 << 31)) for _ in range(17)])
+    assert c(0, 2048, 1, big, 17, ctypes.byref(h)) == bq.BQ_ERR_SIZE
     hp = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 1)
     r = L.bq_step_plan_run
     assert r(None, ctypes.byref(hp), A16, A16, None) == bq.BQ_ERR_NULL
