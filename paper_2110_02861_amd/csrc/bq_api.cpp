@@ -46,6 +46,14 @@ bq::StepScalars make_scalars(const bq_hparams &hp)
     s.step_size = static_cast<float>(lr / (1.0 - beta_pow(b1, hp.step)));
     s.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - beta_pow(b2, hp.step)));
     s.decay = static_cast<float>(1.0 - lr * wd);
+    const double ss = static_cast<double>(s.step_size), fmax = 3.4028234663852886e38;
+    if (ss == 0.0) {
+        s.sdiv_c = 0.0f;
+        s.sdiv_eps = INFINITY;
+    } else {
+        s.sdiv_c = static_cast<float>(std::fmax(-fmax, std::fmin(fmax, s.inv_sqrt_bc2 / ss)));
+        s.sdiv_eps = static_cast<float>(std::fmax(-fmax, std::fmin(fmax, hp.eps / ss)));
+    }
     return s;
 }
 
@@ -54,8 +62,9 @@ bq_status from_hip(hipError_t e) { return e == hipSuccess ? BQ_OK : BQ_ERR_HIP; 
 // Checks every descriptor of a tensor list (no HIP call).
 bq_status check_tensors(const bq_tensor *tensors, int32_t ntensors, int32_t blocksize, bool two)
 {
-    const int64_t tile = bq::tile_elems(blocksize) < bq::kStepTile ? bq::tile_elems(blocksize)
-                                                                    : bq::kStepTile;
+    const int64_t tile = bq::tile_elems(blocksize) < bq::step_tile(blocksize)
+                             ? bq::tile_elems(blocksize)
+                             : bq::step_tile(blocksize);
     for (int32_t i = 0; i < ntensors; ++i) {
         const bq_tensor &t = tensors[i];
         if (t.numel < 0)
@@ -103,9 +112,8 @@ struct bq_step_plan_s {
     bq_dtype grad_dtype;
     int32_t ntensors;      // non-empty tensors
     int64_t total_tiles;
-    bq::TensorDesc *desc;  // device
-    int32_t *tile_tensor;  // device, tensor index of every tile
-    uint8_t *tables;       // device, two prepared maps
+    bq::TensorDesc *tiles;  // device, one record per tile
+    uint8_t *tables;        // device, two prepared maps
 };
 
 extern "C" {
@@ -284,20 +292,34 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
     if (st != BQ_OK)
         return st;
 
-    const int64_t tile = bq::kStepTile;
-    std::vector<bq::TensorDesc> desc;
-    std::vector<int32_t> tile_tensor;
-    int64_t tiles = 0;
+    const int64_t tile = bq::step_tile(blocksize);
+    const size_t gbytes = grad_dtype == BQ_F16 ? 2 : 4;
+    int64_t total = 0;
+    int32_t nonempty = 0;
+    for (int32_t i = 0; i < ntensors; ++i) {
+        total += (tensors[i].numel + tile - 1) / tile;
+        nonempty += tensors[i].numel > 0 ? 1 : 0;
+        if (total > kMaxOneShotTiles)
+            return BQ_ERR_SIZE;
+    }
+    std::vector<bq::TensorDesc> recs;
+    recs.reserve((size_t)total);
     for (int32_t i = 0; i < ntensors; ++i) {
         const bq_tensor &t = tensors[i];
-        if (t.numel == 0)
-            continue;
         const int64_t nt = (t.numel + tile - 1) / tile;
-        if (tiles + nt > kMaxOneShotTiles)
-            return BQ_ERR_SIZE;
-        desc.push_back(make_desc(t, two, tiles));
-        tile_tensor.insert(tile_tensor.end(), (size_t)nt, (int32_t)(desc.size() - 1));
-        tiles += nt;
+        for (int64_t k = 0; k < nt; ++k) {
+            const int64_t t0 = k * tile;
+            bq::TensorDesc d;
+            d.param = t.param + t0;
+            d.grad = static_cast<const char *>(t.grad) + t0 * gbytes;
+            d.s1 = t.state1 + t0;
+            d.s2 = two ? t.state2 + t0 : nullptr;
+            d.a1 = t.absmax1 + t0 / blocksize;
+            d.a2 = two ? t.absmax2 + t0 / blocksize : nullptr;
+            d.numel = t.numel - t0;
+            d.tile_begin = 0;
+            recs.push_back(d);
+        }
     }
 
     bq_step_plan_s *p = new (std::nothrow) bq_step_plan_s();
@@ -306,21 +328,15 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
     p->opt = opt;
     p->blocksize = blocksize;
     p->grad_dtype = grad_dtype;
-    p->ntensors = (int32_t)desc.size();
-    p->total_tiles = tiles;
+    p->ntensors = nonempty;
+    p->total_tiles = (int64_t)recs.size();
     hipError_t e = hipGetDevice(&p->device);
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&p->tables), 2 * bq::kPreparedBytes);
-    if (e == hipSuccess && !desc.empty()) {
-        e = hipMalloc(reinterpret_cast<void **>(&p->desc), desc.size() * sizeof(bq::TensorDesc));
+    if (e == hipSuccess && !recs.empty()) {
+        e = hipMalloc(reinterpret_cast<void **>(&p->tiles), recs.size() * sizeof(bq::TensorDesc));
         if (e == hipSuccess)
-            e = hipMalloc(reinterpret_cast<void **>(&p->tile_tensor),
-                          tile_tensor.size() * sizeof(int32_t));
-        if (e == hipSuccess)
-            e = hipMemcpy(p->desc, desc.data(), desc.size() * sizeof(bq::TensorDesc),
-                          hipMemcpyHostToDevice);
-        if (e == hipSuccess)
-            e = hipMemcpy(p->tile_tensor, tile_tensor.data(), tile_tensor.size() * sizeof(int32_t),
+            e = hipMemcpy(p->tiles, recs.data(), recs.size() * sizeof(bq::TensorDesc),
                           hipMemcpyHostToDevice);
     }
     if (e != hipSuccess) {
@@ -354,8 +370,7 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
     bq::PlanArgs a;
     std::memset(&a, 0, sizeof(a));
     a.tables = plan->tables;
-    a.desc = plan->desc;
-    a.tile_tensor = plan->tile_tensor;
+    a.tiles = plan->tiles;
     a.sc = make_scalars(*hp);
     a.use_wd = (hp->weight_decay != 0.0f && plan->opt != BQ_ADAMW) ? 1 : 0;
     a.total_tiles = (int32_t)plan->total_tiles;
@@ -371,8 +386,7 @@ bq_status bq_step_plan_destroy(bq_step_plan plan)
     if (!plan)
         return BQ_OK;
     hipError_t e = hipSuccess;
-    for (void *ptr : {static_cast<void *>(plan->desc), static_cast<void *>(plan->tile_tensor),
-                      static_cast<void *>(plan->tables)}) {
+    for (void *ptr : {static_cast<void *>(plan->tiles), static_cast<void *>(plan->tables)}) {
         if (ptr && hipFree(ptr) != hipSuccess)
             e = hipErrorUnknown;
     }

@@ -150,8 +150,13 @@ __device__ inline uint32_t bucket_of(float y)
     if constexpr (NONNEG) {
         return min(max(u >> kBucketShift, kBucketLo), kBucketHi) - kBucketLo;
     } else {
+        // sign half by one 24-bit multiply-add (written out: the compiler
+        // would turn the 0/1 multiplier into a compare and a select)
         const uint32_t a = (u & 0x7fffffffu) >> kBucketShift;
-        return (u >> 31) * kBuckets + (min(max(a, kBucketLo), kBucketHi) - kBucketLo);
+        const uint32_t m = min(max(a, kBucketLo), kBucketHi);
+        uint32_t r;
+        asm("v_mad_u32_u24 %0, %1, %2, %3" : "=v"(r) : "v"(u >> 31), "s"(kBuckets), "v"(m));
+        return r - kBucketLo;
     }
 }
 
@@ -235,6 +240,15 @@ __device__ inline uint32_t dpp_umax(uint32_t v)
 {
     const uint32_t o = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, ROW_MASK, 0xf, true);
     return max(v, o);
+}
+
+// Max of non-negative bit patterns over each row of 16 lanes, in every lane.
+__device__ inline uint32_t row_umax(uint32_t v)
+{
+    v = dpp_umax<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
+    v = dpp_umax<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
+    v = dpp_umax<0x141, 0xf>(v);  // row_half_mirror
+    return dpp_umax<0x140, 0xf>(v);  // row_mirror
 }
 
 // Max of non-negative bit patterns over the wave, valid in lane 63 only.

@@ -15,6 +15,11 @@ struct StepScalars {
     float step_size;       // lr / (1 - beta1^t)
     float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
     float decay;           // 1 - lr * wd  (AdamW)
+    // Adam denominator divided by step_size, so that the param update is
+    // w - m / (sqrt(v) * sdiv_c + sdiv_eps) without a separate multiply:
+    // sdiv_c = inv_sqrt_bc2 / step_size, sdiv_eps = eps / step_size (each
+    // clamped to the finite range; lr = 0 gives 0 and +inf: no update).
+    float sdiv_c, sdiv_eps;
 };
 
 // One tensor of a multi-tensor launch.  tile_begin is the index of the
@@ -51,9 +56,13 @@ static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must stay below 4
 // persistent kernels and the one-shot quantize kernel.
 constexpr int tile_elems(int blocksize) { return blocksize >= 2048 ? blocksize : 2048; }
 
-// Elements per tile of the one-shot step kernel (every blocksize): 512
-// threads x 8 elements, i.e. 4096 / B whole blocks.
-constexpr int kStepTile = 4096;
+// Elements per tile of the one-shot step kernel: 512 threads x 4 elements per
+// chunk, kStepChunks chunks (two for 4096 blocks, which must fit one tile).
+constexpr int kStepChunks = 2;
+constexpr int step_tile(int blocksize)
+{
+    return 2048 * (blocksize > 2048 * kStepChunks ? blocksize / 2048 : kStepChunks);
+}
 
 // Prepared codebook: decision tables of one map in device memory, built once
 // by the prepare kernel and copied into LDS by every workgroup.
@@ -75,8 +84,10 @@ static_assert(kPreparedBytes % 16 == 0 && kPreparedNonnegBytes % 16 == 0, "16 B 
 // Arguments of the one-shot step kernel (one workgroup per tile).
 struct PlanArgs {
     const uint8_t *tables;        // prepared map of state 1, then of state 2
-    const TensorDesc *desc;       // device array of descriptors
-    const int32_t *tile_tensor;   // device array: tensor index of every tile
+    // device array, one record per tile: pointers at the tile's first element
+    // (param, grad, states) and first block (absmax), numel = elements from
+    // the tile start to the tensor end (a full tile when >= the tile size)
+    const TensorDesc *tiles;
     StepScalars sc;
     int32_t use_wd;
     int32_t total_tiles;

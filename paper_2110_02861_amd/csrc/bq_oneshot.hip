@@ -98,6 +98,14 @@ __device__ inline BlockNorm block_norm(float A)
     return b;
 }
 
+// x / A, exactly rounded, for a block that needs no rescale (s == 1).
+__device__ inline float normalize_plain(const BlockNorm &b, float x)
+{
+    const float q = x * b.r;
+    const float e = __builtin_fmaf(-q, b.n, x);
+    return __builtin_fmaf(e, b.r, q);
+}
+
 template <int N, bool NONNEG>
 __device__ inline void requantize_norm(const Tables &M, const BlockNorm &b, const float (&x)[N],
                                        uint32_t (&c)[N])
@@ -124,12 +132,14 @@ __device__ inline void requantize_norm(const Tables &M, const BlockNorm &b, cons
 // map 1's bucket table starts at byte kBucketLo: "bucket - kBucketLo" then folds
 // into the LDS instruction's immediate offset.  The pad in front holds the
 // reduction slots and the per-block normalizers.
-constexpr int kLdsSlots = 0;                                    // uint2 slots[16]
-constexpr int kLdsNorms = 128;                                  // BlockNorm norms[16][2]
+constexpr int kMaxBlocksPerTile = step_tile(256) / 256;
+constexpr int kLdsSlots = 0;                                    // uint32 slots[blocks][2]
+constexpr int kLdsNorms = kMaxBlocksPerTile * 2 * 4;            // BlockNorm norms[blocks][2]
 constexpr int kLdsMap1 = (int)kBucketLo - kPreparedOffBase;     // 11008
 constexpr int kLdsMap2 = kLdsMap1 + kPreparedSignedBytes;
 constexpr int kLdsBytes = kLdsMap2 + kPreparedNonnegBytes;
-static_assert(kLdsNorms + 16 * 2 * (int)sizeof(BlockNorm) <= kLdsMap1, "LDS layout");
+static_assert(kLdsNorms + kMaxBlocksPerTile * 2 * (int)sizeof(BlockNorm) <= kLdsMap1,
+              "LDS layout");
 static_assert(kLdsMap1 % 16 == 0 && kLdsMap2 % 16 == 0, "16 B granules");
 
 // ---------------------------------------------------------------------------
@@ -143,9 +153,9 @@ static_assert(kLdsMap1 % 16 == 0 && kLdsMap2 % 16 == 0, "16 B granules");
 // segments [b B/256, (b+1) B/256).
 template <int OPT, int GRAD, int B>
 struct StepOS {
-    static constexpr int C = 2;                         // chunks per thread
+    static constexpr int C = step_tile(B) / 2048;       // chunks per thread
     static constexpr int N = 4 * C;                     // elements per thread
-    static constexpr int TILE = kStepTile;
+    static constexpr int TILE = step_tile(B);
     static_assert(TILE == kOS * N, "tile size");
     static constexpr bool kTwo = (OPT != kMomentum);
     static constexpr int kBPT = TILE / B;               // blocks per tile
@@ -160,7 +170,7 @@ struct StepOS {
     __device__ static void tile(const PlanArgs &a, const TensorDesc &D, int64_t t0, uint8_t *lds,
                                 const vu4 (&gran)[kGPT])
     {
-        uint2 *slots = reinterpret_cast<uint2 *>(lds + kLdsSlots);
+        uint32_t *slots = reinterpret_cast<uint32_t *>(lds + kLdsSlots);
         BlockNorm *norms = reinterpret_cast<BlockNorm *>(lds + kLdsNorms);
         const int tid = threadIdx.x;
         const int wave = tid >> 6;
@@ -220,14 +230,21 @@ struct StepOS {
             n1[c] = live ? G(D.a1)[blk0 + b] : 0.0f;
             n2[c] = (kTwo && live) ? G(D.a2)[blk0 + b] : 0.0f;
         }
+        // the loads are issued: the rest of the tile runs at raised wave
+        // priority, so tiles that hold loaded data finish (and free their
+        // slot for a new tile's loads) ahead of tiles still waiting
+        __builtin_amdgcn_s_setprio(2);
         const int km1 = prepared_kmax(a.tables);
         const int km2 = kTwo ? prepared_kmax(a.tables + kPreparedBytes) : 0;
 
-        // tables into LDS (threads past the last granule rewrite it, same bytes)
+        // tables into LDS (threads past the last granule rewrite it, same bytes);
+        // block max slots cleared
 #pragma unroll
         for (int k = 0; k < kGPT; ++k)
             reinterpret_cast<vu4 *>(lds + kLdsMap1)[min((int)threadIdx.x + k * kOS, kGran - 1)] =
                 gran[k];
+        if (tid < 2 * kBPT)
+            slots[tid] = 0u;
         __syncthreads();
         Tables T1, T2;
         T1.q = reinterpret_cast<const float *>(lds + kLdsMap1 + kPreparedOffQ);
@@ -294,10 +311,11 @@ struct StepOS {
                 mi = sc.b1 * mi + sc.omb1 * gi;
                 vi = sc.b2 * vi + sc.omb2 * (gi * gi);
                 // the param update is not rounded like the oracle's anyway
-                // (hardware sqrt and reciprocal), so it may fuse
+                // (hardware sqrt and reciprocal), so it may fuse and take
+                // step_size into the denominator
                 const float denom =
-                    __builtin_fmaf(__builtin_amdgcn_sqrtf(vi), sc.inv_sqrt_bc2, sc.eps);
-                wi = __builtin_fmaf(-sc.step_size, mi * __builtin_amdgcn_rcpf(denom), wi);
+                    __builtin_fmaf(__builtin_amdgcn_sqrtf(vi), sc.sdiv_c, sc.sdiv_eps);
+                wi = __builtin_fmaf(-mi, __builtin_amdgcn_rcpf(denom), wi);
                 v[i] = ok ? vi : 0.0f;
                 mx2[c] = fmaxf(mx2[c], fabsf(v[i]));
             }
@@ -306,64 +324,114 @@ struct StepOS {
             mx1[c] = fmaxf(mx1[c], fabsf(m[i]));
         }
 
-        // block absmax (on the bit patterns of the non-negative maxima): wave
-        // max per segment -> slot; wave 0 finishes each block, computes its
-        // normalizers once and stores the new absmax
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            const uint32_t u1 = wave_umax_lane63(__float_as_uint(mx1[c]));
-            const uint32_t u2 = kTwo ? wave_umax_lane63(__float_as_uint(mx2[c])) : 0u;
-            if ((tid & 63) == 63)
-                slots[8 * c + wave] = make_uint2(u1, u2);
-        }
-        __syncthreads();
-        if (wave == 0 && tid < kBPT) {
-            uint2 r = slots[tid * kSPB];
-#pragma unroll
-            for (int k = 1; k < kSPB; ++k) {
-                const uint2 o = slots[tid * kSPB + k];
-                r.x = max(r.x, o.x);
-                r.y = max(r.y, o.y);
-            }
-            norms[2 * tid] = block_norm(__uint_as_float(r.x));
-            if constexpr (kTwo)
-                norms[2 * tid + 1] = block_norm(__uint_as_float(r.y));
-            if (FULL || t0 + (int64_t)tid * B < D.numel) {
-                G(D.a1)[blk0 + tid] = __uint_as_float(r.x);
-                if constexpr (kTwo)
-                    G(D.a2)[blk0 + tid] = __uint_as_float(r.y);
-            }
-        }
-        __syncthreads();
-
-        // requantize, chunk by chunk (each chunk lies in one block)
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            const int b = (8 * c + wave) / kSPB;
-            float mc[4], vc[4];
-            uint32_t q1[4], q2[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                mc[r] = m[4 * c + r];
-                vc[r] = v[4 * c + r];
-            }
-            requantize_norm<4, false>(T1, norms[2 * b], mc, q1);
-            if constexpr (kTwo)
-                requantize_norm<4, true>(T2, norms[2 * b + 1], vc, q2);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                c1[4 * c + r] = q1[r];
-                c2[4 * c + r] = kTwo ? q2[r] : 0u;
-            }
-        }
-
-        // store
+        // the params are final: store them now, so their writes overlap the
+        // block reduction
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const int64_t e = t0 + c * (kOS * 4) + tid * 4;
             if (FULL) {
                 st_nt(reinterpret_cast<vf4 *>(D.param + e),
                       vf4{w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]});
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (r < valid[c])
+                        G(D.param)[e + r] = w[4 * c + r];
+            }
+        }
+
+        // block absmax on the bit patterns of the non-negative maxima: row
+        // (16-lane) max by DPP, one LDS max per row and value into the block's
+        // slot (zeroed before the table barrier); wave 0 then computes each
+        // block's normalizers once and stores the new absmax
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int b = (8 * c + wave) / kSPB;
+            const uint32_t u1 = row_umax(__float_as_uint(mx1[c]));
+            const uint32_t u2 = kTwo ? row_umax(__float_as_uint(mx2[c])) : 0u;
+            if ((tid & 15) == 0) {
+                atomicMax(&slots[2 * b], u1);
+                if constexpr (kTwo)
+                    atomicMax(&slots[2 * b + 1], u2);
+            }
+        }
+        __syncthreads();
+        if (wave == 0 && tid < kBPT) {
+            const float A1 = __uint_as_float(slots[2 * tid]);
+            const float A2 = kTwo ? __uint_as_float(slots[2 * tid + 1]) : 0.0f;
+            norms[2 * tid] = block_norm(A1);
+            if constexpr (kTwo)
+                norms[2 * tid + 1] = block_norm(A2);
+            if (FULL || t0 + (int64_t)tid * B < D.numel) {
+                G(D.a1)[blk0 + tid] = A1;
+                if constexpr (kTwo)
+                    G(D.a2)[blk0 + tid] = A2;
+            }
+        }
+        __syncthreads();
+
+        // requantize.  Common case (every map resolves a bucket with at most
+        // one threshold, no block needs the power-of-two rescale): one
+        // straight-line pass over all chunks and both states.
+        BlockNorm nb1[C], nb2[C];
+        bool plain = (km1 == 1) && (!kTwo || km2 == 1);
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int b = (8 * c + wave) / kSPB;
+            nb1[c] = norms[2 * b];
+            nb2[c] = kTwo ? norms[2 * b + 1] : nb1[c];
+            plain = plain && __builtin_amdgcn_readfirstlane(__float_as_int(nb1[c].s)) ==
+                                 __float_as_int(1.0f);
+            if constexpr (kTwo)
+                plain = plain && __builtin_amdgcn_readfirstlane(__float_as_int(nb2[c].s)) ==
+                                     __float_as_int(1.0f);
+        }
+        if (plain) {
+            float y1[N], y2[N];
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                y1[i] = normalize_plain(nb1[i / 4], m[i]);
+                if constexpr (kTwo)
+                    y2[i] = normalize_plain(nb2[i / 4], v[i]);
+            }
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                c1[i] = T1.base[bucket_of<false>(y1[i])];
+                if constexpr (kTwo)
+                    c2[i] = T2.base[bucket_of<true>(y2[i])];
+            }
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                c1[i] += (y1[i] >= T1.t[c1[i]]) ? 1u : 0u;
+                if constexpr (kTwo)
+                    c2[i] += (y2[i] >= T2.t[c2[i]]) ? 1u : 0u;
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                float mc[4], vc[4];
+                uint32_t q1[4], q2[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    mc[r] = m[4 * c + r];
+                    vc[r] = v[4 * c + r];
+                }
+                requantize_norm<4, false>(T1, nb1[c], mc, q1);
+                if constexpr (kTwo)
+                    requantize_norm<4, true>(T2, nb2[c], vc, q2);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    c1[4 * c + r] = q1[r];
+                    c2[4 * c + r] = kTwo ? q2[r] : 0u;
+                }
+            }
+        }
+
+        // store the codes
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            if (FULL) {
                 st_nt(reinterpret_cast<uint32_t *>(D.s1 + e),
                       c1[4 * c] | (c1[4 * c + 1] << 8) | (c1[4 * c + 2] << 16) |
                           (c1[4 * c + 3] << 24));
@@ -375,7 +443,6 @@ struct StepOS {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     if (r < valid[c]) {
-                        G(D.param)[e + r] = w[4 * c + r];
                         G(D.s1)[e + r] = (uint8_t)c1[4 * c + r];
                         if constexpr (kTwo)
                             G(D.s2)[e + r] = (uint8_t)c2[4 * c + r];
@@ -404,9 +471,7 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
         gran[k] = *G(reinterpret_cast<const vu4 *>(a.tables + src));
     }
 
-    const int tile = blockIdx.x;
-    const int ti = __builtin_amdgcn_readfirstlane(G(a.tile_tensor)[tile]);
-    const gptr<const TensorDesc> dp = G(a.desc) + ti;
+    const gptr<const TensorDesc> dp = G(a.tiles) + blockIdx.x;
     TensorDesc D;
     D.param = dp->param;
     D.grad = dp->grad;
@@ -415,8 +480,7 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
     D.a1 = dp->a1;
     D.a2 = dp->a2;
     D.numel = dp->numel;
-    D.tile_begin = dp->tile_begin;
-    const int64_t t0 = (int64_t)(tile - D.tile_begin) * K::TILE;
+    const int64_t t0 = 0;
     if (t0 + K::TILE <= D.numel)
         K::template tile<true>(a, D, t0, lds, gran);
     else
