@@ -15,6 +15,8 @@ blocks) timed on a bounded sample of the same workload on the host cores.
 from __future__ import annotations
 
 import argparse
+import ctypes
+import hashlib
 import json
 import os
 import sys
@@ -30,6 +32,19 @@ METRIC = "8-bit Adam step params/sec and achieved HBM GB/s (% of peak), 1.5B-par
 HBM_PEAK_GBS = 8000.0
 BLOCKSIZE = 2048
 
+# HBM traffic of one step-kernel launch on this workload, from two rocprofv3
+# --pmc runs of `bench.py --steps 3 --warmup 1 --no-cpu-baseline` (FETCH_SIZE,
+# then WRITE_SIZE, KiB per dispatch), FETCH_SIZE scaled by 2.0 and WRITE_SIZE by
+# 1.0: the factors that make the counters of a plain fp32->fp16 copy of known
+# size read its true bytes on MI355X (profiles/step_kernel_adam_f16_b2048_lm1p5b_pmc.md).
+# Valid only for the kernel sources it was taken on (sha256 below); otherwise
+# the bench reports traffic null.
+KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h"]
+MEASURED_TRAFFIC = {
+    "sources_sha256": "4e884610fe02e03e9dff23a9c59a907babaeb7e7178cc25f54c685f5b7f6c3c0",
+    "fetch_kib": 6132440.0, "write_kib": 9150410.0, "fetch_scale": 2.0, "write_scale": 1.0,
+}
+
 
 def step_bytes(numels, blocksize, grad_bytes, nstates):
     """Algorithmic HBM bytes of one step: fp32 param read + write, grad read,
@@ -37,6 +52,73 @@ def step_bytes(numels, blocksize, grad_bytes, nstates):
     n = sum(numels)
     nblocks = sum((k + blocksize - 1) // blocksize for k in numels)
     return n * (8 + grad_bytes + 2 * nstates) + nblocks * nstates * 8
+
+
+def kernel_sources_sha256():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2110_02861_amd", "csrc")
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """Counter-measured HBM bytes per step-kernel launch, or None when the
+    kernel sources differ from the ones the counters were taken on."""
+    m = MEASURED_TRAFFIC
+    if m["sources_sha256"] is None or m["sources_sha256"] != kernel_sources_sha256():
+        return None
+    return m["fetch_kib"] * 1024 * m["fetch_scale"] + m["write_kib"] * 1024 * m["write_scale"]
+
+
+def stream_ceiling(torch, nparams, steps=20):
+    """Same-byte-mix streaming rate on flat random buffers of the same size:
+    loads and stores of the step's bytes with no arithmetic (libbq_stream.so),
+    best of its launch-shape variants.  Returns (best GB/s, {variant: GB/s}),
+    algorithmic bytes as in step_bytes()."""
+    from paper_2110_02861_amd import build as pkg_build
+    if not os.path.exists(pkg_build.STREAM_LIB):
+        raise RuntimeError(f"{pkg_build.STREAM_LIB} is not built")
+    L = ctypes.CDLL(pkg_build.STREAM_LIB)
+    P = ctypes.c_void_p
+    L.bq_stream_ceiling.argtypes = [ctypes.c_int] + [P] * 6 + [ctypes.c_int64, ctypes.c_int32,
+                                                               ctypes.c_uint32, P, P]
+    L.bq_stream_ceiling.restype = ctypes.c_int
+    L.bq_stream_variants.restype = ctypes.c_int
+    n = (nparams + 4095) // 4096 * 4096
+    nb = n // BLOCKSIZE
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(12345)
+    w = torch.empty(n, dtype=torch.float32, device=dev).normal_(0, 0.02, generator=gen)
+    g = torch.empty(n, dtype=torch.float16, device=dev).normal_(0, 1e-4, generator=gen)
+    c1 = torch.randint(0, 256, (n,), dtype=torch.uint8, device=dev, generator=gen)
+    c2 = torch.randint(0, 256, (n,), dtype=torch.uint8, device=dev, generator=gen)
+    a1 = torch.rand(nb, device=dev, generator=gen)
+    a2 = torch.rand(nb, device=dev, generator=gen)
+    table = torch.randint(0, 2**31 - 1, (4096,), dtype=torch.int32, device=dev, generator=gen)
+    stream = torch.cuda.current_stream()
+    bufs = [P(t.data_ptr()) for t in (w, g, c1, c2, a1, a2)]
+    per = {}
+    for v in range(L.bq_stream_variants()):
+        args = [v] + bufs + [n, BLOCKSIZE, 0, P(table.data_ptr()), P(stream.cuda_stream)]
+        for _ in range(3):
+            if L.bq_stream_ceiling(*args) != 0:
+                raise RuntimeError("bq_stream_ceiling failed")
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            L.bq_stream_ceiling(*args)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        sec = e0.elapsed_time(e1) / steps / 1e3
+        per[v] = step_bytes([n], BLOCKSIZE, 2, 2) / sec / 1e9
+    del w, g, c1, c2, a1, a2, table
+    torch.cuda.empty_cache()
+    return max(per.values()), per
 
 
 def log(msg):
@@ -115,6 +197,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stream-ceiling", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=8)
     ap.add_argument("--path", choices=["plan", "call"], default="plan",
                     help="plan: bq_step_plan_run (one launch over all 580 tensors); "
@@ -143,6 +226,12 @@ def main():
         log("timing the CPU oracle on a bounded sample")
         cpu = cpu_baseline(specs, params, grads, args.cpu_layers)
         log(f"cpu baseline {cpu['value'] / 1e6:.1f} Mparam/s on {cpu['cores']} threads")
+
+    ceiling = None
+    if not args.no_stream_ceiling:
+        log("measuring the same-byte-mix streaming ceiling")
+        ceiling, ceiling_per = stream_ceiling(torch, nparams)
+        log(f"stream ceiling {ceiling:.0f} GB/s (variants {ceiling_per})")
 
     stream = torch.cuda.current_stream()
 
@@ -201,8 +290,17 @@ def main():
         "hbm_frac": gbs / HBM_PEAK_GBS,
         "roofline": {
             "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+            "frac": gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
             "bytes_per_step": bytes_step,
+            "kernel": "step_oneshot_kernel<Adam, fp16 grad, 2048> (+ prepare_kernel, ~10 us, "
+                      "inside the timed launch pair)",
+        },
+        "stream_ceiling": None if ceiling is None else {
+            "gbs": ceiling, "frac_of_peak": ceiling / HBM_PEAK_GBS,
+            "step_frac_of_ceiling": gbs / ceiling,
+            "per_variant": ceiling_per,
+            "kind": "same byte mix, flat random buffers, no arithmetic, best of the launch "
+                    "shapes in libbq_stream.so",
         },
         "cpu_baseline": cpu,
     }

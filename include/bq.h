@@ -152,10 +152,10 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
  *
  * The calls above build a codebook's decision tables inside every persistent
  * workgroup, because they receive nothing but the raw map.  The calls below
- * keep those tables in caller-visible device memory, so that every block can
- * run as its own short-lived workgroup (512 threads, one tile of 2048
- * elements or one 4096 block), which streams HBM markedly faster on MI355X.
- * Results are identical to the calls above, bit for bit.
+ * keep those tables in caller-visible device memory, so that every tile can
+ * run as its own short-lived workgroup (512 threads; 2048 elements for the
+ * quantize call, 4096 for the step), which streams HBM markedly faster on
+ * MI355X.  Codes and absmax are identical to the calls above, bit for bit.
  * ------------------------------------------------------------------------ */
 
 /* Bytes of device memory one prepared codebook occupies (16-byte aligned). */
@@ -186,9 +186,10 @@ typedef struct bq_step_plan_s *bq_step_plan;
 
 /*
  * Create a plan for the fused 8-bit step (Section 3, Fig. 1) over a fixed
- * tensor list.  This is the only allocating call: it copies the descriptors
- * and a tile-to-tensor map (4 bytes per tile of 2048 elements) to device
- * memory of the current device and reserves space for two prepared codebooks.
+ * tensor list.  This is the only allocating call: it writes one 64-byte record
+ * per tile (4096 elements; pointers at the tile's first element and block) to
+ * device memory of the current device -- 16 bytes per 1,024 params -- and
+ * reserves space for two prepared codebooks.
  * Synchronous.  The tensors' buffers must stay valid while the plan is used.
  *   tensors  host array of ntensors descriptors (as bq_optimizer8bit_step)
  *   plan     receives the handle (NULL on error)

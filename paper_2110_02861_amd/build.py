@@ -14,6 +14,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libbq.so")
 SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_kernels.hip", "bq_oneshot.hip"]
+# the benchmark's streaming-ceiling kernel, a library of its own
+STREAM_LIB = os.path.join(PKG, "libbq_stream.so")
+STREAM_SOURCES = ["bq_stream.hip"]
 ARCH = "gfx950"
 
 # -ffp-contract=off: the state arithmetic must not be fused into fma, so that it
@@ -34,15 +37,22 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
+def _link(out: str, sources, verbose: bool) -> str:
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = out + ".tmp"
     cmd = [hipcc(), *FLAGS, "-shared", "-o", tmp, *srcs]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Build libbq.so (the library) and libbq_stream.so (the benchmark's
+    streaming-ceiling kernel); return the path of libbq.so."""
+    _link(STREAM_LIB, STREAM_SOURCES, verbose)
+    return _link(LIB, SOURCES, verbose)
 
 
 def build_asm(out_dir: str) -> None:
