@@ -147,6 +147,30 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
                                 const bq_hparams *hp, const float *qmap1,
                                 const float *qmap2, hipStream_t stream);
 
+/* One tensor with 32-bit states; all pointers are device pointers. */
+typedef struct bq_tensor32 {
+    float *param;       /* numel fp32, updated in place */
+    const void *grad;   /* numel fp32 or fp16 (see grad_dtype), read only */
+    float *state1;      /* numel fp32 first state (m), in place */
+    float *state2;      /* numel fp32 second state (r); NULL for Momentum */
+    int64_t numel;
+} bq_tensor32;
+
+/*
+ * The same optimizer step with 32-bit states (Section 3.3 keeps the embedding
+ * layer's states in 32 bit): the update of bq_optimizer8bit_step without
+ * dequantization and requantization, states fp32 in the same operation order.
+ * For tensors exempted from 8-bit states by the caller.
+ *   tensors  host array of ntensors descriptors; every non-empty tensor's
+ *            pointers 16-byte aligned
+ *   hp       host pointer to the hyperparameters (step >= 1)
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_ENUM, BQ_ERR_DTYPE, BQ_ERR_ALIGN,
+ * BQ_ERR_ARG (step < 1), BQ_ERR_HIP.
+ */
+bq_status bq_optimizer32bit_step(bq_optimizer opt, bq_dtype grad_dtype,
+                                 const bq_tensor32 *tensors, int32_t ntensors,
+                                 const bq_hparams *hp, hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * Prepared codebooks and step plans: the fast path.
  *

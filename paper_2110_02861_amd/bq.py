@@ -23,7 +23,8 @@ BQ_F32, BQ_F16 = 0, 1
 OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM}
 
 EXPORTS = ("bq_make_dynamic_codebook", "bq_quantize_blockwise", "bq_dequantize_blockwise",
-           "bq_optimizer8bit_step", "bq_prepare_codebook", "bq_quantize_blockwise_prepared",
+           "bq_optimizer8bit_step", "bq_optimizer32bit_step", "bq_prepare_codebook",
+           "bq_quantize_blockwise_prepared",
            "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_destroy",
            "bq_status_string")
 BQ_PREPARED_CODEBOOK_BYTES = 8720
@@ -39,6 +40,12 @@ class bq_tensor(ctypes.Structure):
     _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
                 ("state1", ctypes.c_void_p), ("state2", ctypes.c_void_p),
                 ("absmax1", ctypes.c_void_p), ("absmax2", ctypes.c_void_p),
+                ("numel", ctypes.c_int64)]
+
+
+class bq_tensor32(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("state1", ctypes.c_void_p), ("state2", ctypes.c_void_p),
                 ("numel", ctypes.c_int64)]
 
 
@@ -68,6 +75,8 @@ def lib() -> ctypes.CDLL:
         L.bq_dequantize_blockwise.restype = I
         L.bq_optimizer8bit_step.argtypes = [I, I32, I, P, I32, P, P, P, P]
         L.bq_optimizer8bit_step.restype = I
+        L.bq_optimizer32bit_step.argtypes = [I, I, P, I32, P, P]
+        L.bq_optimizer32bit_step.restype = I
         L.bq_prepare_codebook.argtypes = [P, P, P]
         L.bq_prepare_codebook.restype = I
         L.bq_quantize_blockwise_prepared.argtypes = [P, P, I64, I32, P, P, P]
@@ -183,6 +192,30 @@ def bq_optimizer8bit_step(opt, blocksize: int, grad_dtype: int, tensors, hp: dic
                                        None if qmap2 is None else _dev_ptr(qmap2, "qmap2"),
                                        _stream(stream)),
            "bq_optimizer8bit_step")
+
+
+def make_tensor32_array(tensors):
+    """Pack (param, grad, state1, state2) tuples of GPU tensors (state2 may be
+    None) into a ctypes bq_tensor32 array."""
+    arr = (bq_tensor32 * max(1, len(tensors)))()
+    for i, (p, g, m, v) in enumerate(tensors):
+        arr[i].param = _dev_ptr(p, "param")
+        arr[i].grad = _dev_ptr(g, "grad")
+        arr[i].state1 = _dev_ptr(m, "state1")
+        arr[i].state2 = None if v is None else _dev_ptr(v, "state2")
+        arr[i].numel = p.numel()
+    return arr
+
+
+def bq_optimizer32bit_step(opt, grad_dtype: int, tensors, hp: dict, stream=None):
+    """One step with fp32 states over (param, grad, state1, state2) tuples."""
+    if isinstance(opt, str):
+        opt = OPTIMIZERS[opt]
+    arr = make_tensor32_array(tensors)
+    h = _hparams(hp)
+    _check(lib().bq_optimizer32bit_step(int(opt), int(grad_dtype), arr, len(tensors),
+                                        ctypes.byref(h), _stream(stream)),
+           "bq_optimizer32bit_step")
 
 
 def _hparams(hp: dict) -> bq_hparams:

@@ -241,6 +241,73 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
     return BQ_OK;
 }
 
+bq_status bq_optimizer32bit_step(bq_optimizer opt, bq_dtype grad_dtype,
+                                 const bq_tensor32 *tensors, int32_t ntensors,
+                                 const bq_hparams *hp, hipStream_t stream)
+{
+    if (!valid_opt(opt))
+        return BQ_ERR_ENUM;
+    if (!valid_dtype(grad_dtype))
+        return BQ_ERR_DTYPE;
+    if (ntensors < 0)
+        return BQ_ERR_SIZE;
+    if (ntensors == 0)
+        return BQ_OK;
+    if (!tensors || !hp)
+        return BQ_ERR_NULL;
+    if (hp->step < 1)
+        return BQ_ERR_ARG;
+    const bool two = (opt != BQ_MOMENTUM);
+    constexpr int64_t tile = 1024;
+    for (int32_t i = 0; i < ntensors; ++i) {
+        const bq_tensor32 &t = tensors[i];
+        if (t.numel < 0 || t.numel / tile >= (int64_t)INT32_MAX / 2)
+            return BQ_ERR_SIZE;
+        if (t.numel == 0)
+            continue;
+        if (!t.param || !t.grad || !t.state1 || (two && !t.state2))
+            return BQ_ERR_NULL;
+        if (!aligned(t.param, 16) || !aligned(t.grad, 16) || !aligned(t.state1, 16) ||
+            (two && !aligned(t.state2, 16)))
+            return BQ_ERR_ALIGN;
+    }
+
+    bq::State32Args args;
+    std::memset(&args, 0, sizeof(args));
+    args.sc = make_scalars(*hp);
+    args.use_wd = (hp->weight_decay != 0.0f && opt != BQ_ADAMW) ? 1 : 0;
+    int32_t i = 0;
+    while (i < ntensors) {
+        int32_t k = 0;
+        int64_t tiles = 0;
+        for (; i < ntensors && k < bq::kMaxDesc32PerLaunch; ++i) {
+            const bq_tensor32 &t = tensors[i];
+            if (t.numel == 0)
+                continue;
+            const int64_t nt = (t.numel + tile - 1) / tile;
+            if (k > 0 && tiles + nt > (int64_t)INT32_MAX / 2)
+                break;
+            bq::Desc32 &d = args.d[k++];
+            d.param = t.param;
+            d.grad = t.grad;
+            d.m = t.state1;
+            d.v = two ? t.state2 : nullptr;
+            d.numel = t.numel;
+            d.tile_begin = tiles;
+            tiles += nt;
+        }
+        if (k == 0)
+            continue;
+        args.ntensors = k;
+        args.total_tiles = static_cast<int32_t>(tiles);
+        const hipError_t e = bq::launch_step32(static_cast<int>(opt), static_cast<int>(grad_dtype),
+                                               args, stream);
+        if (e != hipSuccess)
+            return BQ_ERR_HIP;
+    }
+    return BQ_OK;
+}
+
 bq_status bq_prepare_codebook(const float *qmap, void *prepared, hipStream_t stream)
 {
     if (!qmap || !prepared)

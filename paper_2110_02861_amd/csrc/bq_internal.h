@@ -93,6 +93,29 @@ struct PlanArgs {
     int32_t total_tiles;
 };
 
+// One tensor of a 32-bit-state launch (states are fp32 arrays).
+struct Desc32 {
+    float *param;
+    const void *grad;
+    float *m;
+    float *v;  // nullptr for Momentum
+    int64_t numel;
+    int64_t tile_begin;  // first tile of the tensor in the launch (1024 elements per tile)
+};
+constexpr int kMaxDesc32PerLaunch = 72;
+
+struct State32Args {
+    StepScalars sc;
+    int32_t ntensors;
+    int32_t total_tiles;
+    int32_t use_wd;
+    int32_t pad;
+    Desc32 d[kMaxDesc32PerLaunch];
+};
+static_assert(sizeof(State32Args) <= 4096, "kernel argument block must stay below 4 KiB");
+
+hipError_t launch_step32(int opt, int grad_dtype, const State32Args &args, hipStream_t stream);
+
 hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *tables,
                           hipStream_t stream);
 hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const PlanArgs &args,

@@ -1,0 +1,243 @@
+"""Drop-in PyTorch optimizers with 8-bit block-wise states, over libbq.
+
+The paper's 8-bit optimizers replace their 32-bit counterparts without
+hyperparameter changes (Section 1, Section 4): Adam (Eq. 2 with bias
+correction), AdamW, and SGD with momentum (Eq. 1).  Each state is stored as one
+uint8 code per element plus one fp32 absmax per block of ``blocksize`` elements
+(Section 3.1); the signed dynamic map holds the first state and the unsigned
+dynamic map the second (Section 3.2).  Tensors can keep 32-bit states instead:
+Section 3.3 keeps the embedding layer's states in 32 bit, and tensors below
+``min_8bit_size`` elements may be exempted as well.
+
+Every update runs in the HIP kernels of libbq:
+- 8-bit tensors go through a cached step plan (``bq_step_plan_run``: one launch
+  over every tile of every tensor), rebuilt whenever a tensor's storage moves,
+  or through ``bq_optimizer8bit_step`` when ``use_plans=False``;
+- 32-bit tensors go through ``bq_optimizer32bit_step``.
+
+Params must be fp32 CUDA tensors, contiguous and 16-byte aligned; grads fp32 or
+fp16 of the same shape.  ``state_dict`` / ``load_state_dict`` carry the codes,
+the absmax arrays and the step count of every tensor.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import bq
+
+_CODEBOOKS: dict = {}
+
+
+def dynamic_codebooks(device: torch.device):
+    """(signed map, unsigned map) as fp32 device tensors, built once per device."""
+    key = (device.type, device.index)
+    if key not in _CODEBOOKS:
+        qs = bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)
+        qu = bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)
+        _CODEBOOKS[key] = (torch.from_numpy(qs).to(device), torch.from_numpy(qu).to(device),
+                           int(np.flatnonzero(qs == 0.0)[0]), int(np.flatnonzero(qu == 0.0)[0]))
+    return _CODEBOOKS[key]
+
+
+class Optimizer8bit(torch.optim.Optimizer):
+    """Base class: state management, grouping, kernel dispatch."""
+
+    OPT: int = -1  # bq.BQ_ADAM / BQ_ADAMW / BQ_MOMENTUM
+    MAX_PLANS = 8  # cached step plans per optimizer (one per param subset)
+
+    def __init__(self, params, defaults: dict, blocksize: int = 2048, min_8bit_size: int = 0,
+                 use_plans: bool = True):
+        if blocksize not in (256, 512, 1024, 2048, 4096):
+            raise ValueError(f"blocksize must be a power of two in [256, 4096], got {blocksize}")
+        if min_8bit_size < 0:
+            raise ValueError("min_8bit_size must be >= 0")
+        self.blocksize = int(blocksize)
+        self.min_8bit_size = int(min_8bit_size)
+        self.use_plans = bool(use_plans)
+        self._override32: set = set()
+        self._plans: dict = {}
+        super().__init__(params, defaults)
+
+    # -- configuration --------------------------------------------------------
+
+    def override_32bit(self, param: torch.Tensor) -> None:
+        """Keep this param's states in 32 bit (e.g. an embedding layer, Section
+        3.3).  Call before the param's first step."""
+        if param in self.state and self.state[param]:
+            raise RuntimeError("override_32bit must be called before the param's first step")
+        self._override32.add(id(param))
+
+    def _is_8bit(self, p: torch.Tensor) -> bool:
+        return id(p) not in self._override32 and p.numel() >= self.min_8bit_size
+
+    # -- hyperparameters of one group (subclasses) ------------------------------
+
+    def _hparams(self, group: dict, step: int) -> dict:
+        raise NotImplementedError
+
+    @property
+    def _two_states(self) -> bool:
+        return self.OPT != bq.BQ_MOMENTUM
+
+    # -- state ------------------------------------------------------------------
+
+    def _init_state(self, p: torch.Tensor, state: dict) -> None:
+        state["step"] = 0
+        if self._is_8bit(p):
+            _, _, z1, z2 = dynamic_codebooks(p.device)
+            nb = (p.numel() + self.blocksize - 1) // self.blocksize
+            state["state1"] = torch.full((p.numel(),), z1, dtype=torch.uint8, device=p.device)
+            state["absmax1"] = torch.zeros(nb, dtype=torch.float32, device=p.device)
+            if self._two_states:
+                state["state2"] = torch.full((p.numel(),), z2, dtype=torch.uint8, device=p.device)
+                state["absmax2"] = torch.zeros(nb, dtype=torch.float32, device=p.device)
+        else:
+            state["exp_avg"] = torch.zeros(p.numel(), dtype=torch.float32, device=p.device)
+            if self._two_states:
+                state["exp_avg_sq"] = torch.zeros(p.numel(), dtype=torch.float32,
+                                                  device=p.device)
+
+    @staticmethod
+    def _check_param(p: torch.Tensor) -> None:
+        if not p.is_cuda:
+            raise TypeError("8-bit optimizers need GPU tensors (libbq runs on the GPU only)")
+        if p.dtype != torch.float32:
+            raise TypeError(f"params must be fp32, got {p.dtype}")
+        if not p.is_contiguous():
+            raise ValueError("params must be contiguous")
+        g = p.grad
+        if g.is_sparse:
+            raise TypeError("sparse gradients are not supported")
+        if g.dtype not in (torch.float32, torch.float16):
+            raise TypeError(f"grads must be fp32 or fp16, got {g.dtype}")
+        if g.shape != p.shape or not g.is_contiguous():
+            raise ValueError("grads must be contiguous and shaped like their params")
+
+    # -- the step -----------------------------------------------------------------
+
+    @torch.no_grad()
+    def step(self, closure=None):
+        loss = None
+        if closure is not None:
+            with torch.enable_grad():
+                loss = closure()
+        for gi, group in enumerate(self.param_groups):
+            buckets: dict = {}
+            for p in group["params"]:
+                if p.grad is None:
+                    continue
+                self._check_param(p)
+                state = self.state[p]
+                if not state:
+                    self._init_state(p, state)
+                state["step"] += 1
+                eight = "state1" in state
+                gdt = bq.BQ_F16 if p.grad.dtype == torch.float16 else bq.BQ_F32
+                buckets.setdefault((eight, gdt, state["step"], p.device), []).append(p)
+            for (eight, gdt, step, device), ps in buckets.items():
+                hp = self._hparams(group, step)
+                if eight:
+                    self._step8(gi, gdt, device, ps, hp)
+                else:
+                    rows = [(p, p.grad, self.state[p]["exp_avg"],
+                             self.state[p].get("exp_avg_sq")) for p in ps]
+                    bq.bq_optimizer32bit_step(self.OPT, gdt, rows, hp)
+        return loss
+
+    def _step8(self, gi: int, gdt: int, device, ps, hp: dict) -> None:
+        q1, q2, _, _ = dynamic_codebooks(device)
+        rows = []
+        for p in ps:
+            s = self.state[p]
+            rows.append((p, p.grad, s["state1"], s.get("state2"), s["absmax1"], s.get("absmax2")))
+        q2 = q2 if self._two_states else None
+        if not self.use_plans:
+            bq.bq_optimizer8bit_step(self.OPT, self.blocksize, gdt, rows, hp, q1, q2)
+            return
+        # a plan holds device pointers: reuse it while every storage stays put
+        key = tuple(0 if t is None else t.data_ptr() for row in rows for t in row)
+        key += tuple(p.numel() for p in ps)
+        slot = (gi, gdt, device.index, tuple(id(p) for p in ps))
+        cached = self._plans.pop(slot, None)
+        if cached is None or cached[0] != key:
+            if cached is not None:
+                cached[1].close()
+            cached = (key, bq.StepPlan(self.OPT, self.blocksize, gdt, rows))
+        self._plans[slot] = cached  # most recently used last
+        while len(self._plans) > self.MAX_PLANS:
+            oldest = next(iter(self._plans))
+            self._plans.pop(oldest)[1].close()
+        cached[1].run(hp, q1, q2)
+
+    def load_state_dict(self, state_dict):
+        for _, plan in self._plans.values():
+            plan.close()
+        self._plans = {}
+        super().load_state_dict(state_dict)
+        # torch casts every non-step state tensor to the param's dtype; the
+        # codes (0..255) come through fp32 exactly and go back to uint8
+        for s in self.state.values():
+            for k in ("state1", "state2"):
+                if k in s:
+                    s[k] = s[k].to(torch.uint8)
+
+
+class Adam8bit(Optimizer8bit):
+    """Adam with 8-bit states (Eq. 2 with bias correction).  weight_decay adds
+    an L2 term to the gradient, as torch.optim.Adam does."""
+
+    OPT = bq.BQ_ADAM
+
+    def __init__(self, params, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.0,
+                 **kw):
+        _check_hparams(lr, betas, eps, weight_decay)
+        super().__init__(params, dict(lr=lr, betas=tuple(betas), eps=eps,
+                                      weight_decay=weight_decay), **kw)
+
+    def _hparams(self, group, step):
+        b1, b2 = group["betas"]
+        return dict(lr=group["lr"], beta1=b1, beta2=b2, eps=group["eps"],
+                    wd=group["weight_decay"], step=step)
+
+
+class AdamW8bit(Adam8bit):
+    """AdamW with 8-bit states: decoupled decay w *= 1 - lr * weight_decay,
+    then the Adam update, as torch.optim.AdamW."""
+
+    OPT = bq.BQ_ADAMW
+
+    def __init__(self, params, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2, **kw):
+        super().__init__(params, lr=lr, betas=betas, eps=eps, weight_decay=weight_decay, **kw)
+
+
+class SGD8bit(Optimizer8bit):
+    """SGD with momentum and an 8-bit momentum buffer (Eq. 1): m = beta m + g,
+    w -= lr m, with weight_decay as an L2 term; torch.optim.SGD with
+    dampening 0 and nesterov False."""
+
+    OPT = bq.BQ_MOMENTUM
+
+    def __init__(self, params, lr=1e-2, momentum=0.9, weight_decay=0.0, **kw):
+        if lr < 0.0:
+            raise ValueError(f"invalid learning rate {lr}")
+        if not 0.0 <= momentum < 1.0:
+            raise ValueError(f"invalid momentum {momentum}")
+        if weight_decay < 0.0:
+            raise ValueError(f"invalid weight_decay {weight_decay}")
+        super().__init__(params, dict(lr=lr, momentum=momentum, weight_decay=weight_decay), **kw)
+
+    def _hparams(self, group, step):
+        return dict(lr=group["lr"], beta1=group["momentum"], beta2=0.0, eps=0.0,
+                    wd=group["weight_decay"], step=step)
+
+
+def _check_hparams(lr, betas, eps, weight_decay):
+    if lr < 0.0:
+        raise ValueError(f"invalid learning rate {lr}")
+    if len(betas) != 2 or not all(0.0 <= b < 1.0 for b in betas):
+        raise ValueError(f"invalid betas {betas}")
+    if eps < 0.0:
+        raise ValueError(f"invalid eps {eps}")
+    if weight_decay < 0.0:
+        raise ValueError(f"invalid weight_decay {weight_decay}")

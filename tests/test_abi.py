@@ -196,3 +196,33 @@ def test_product_path_has_no_fallback(monkeypatch, tmp_path):
     monkeypatch.setattr(bq, "_lib", None)
     with pytest.raises(RuntimeError):
         bq.lib()
+
+
+def _tensors32(*rows):
+    arr = (bq.bq_tensor32 * len(rows))()
+    for i, r in enumerate(rows):
+        for k, v in r.items():
+            setattr(arr[i], k, v)
+    return arr
+
+
+def test_step32_argument_checks(L):
+    s = L.bq_optimizer32bit_step
+    hp = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 1)
+    hp0 = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 0)
+    H = ctypes.byref(hp)
+    row = dict(param=A16, grad=A16, state1=A16, state2=A16, numel=100)
+    good = _tensors32(row)
+    assert s(3, 0, good, 1, H, None) == bq.BQ_ERR_ENUM
+    assert s(0, 5, good, 1, H, None) == bq.BQ_ERR_DTYPE
+    assert s(0, 0, good, -1, H, None) == bq.BQ_ERR_SIZE
+    assert s(0, 0, None, 1, H, None) == bq.BQ_ERR_NULL
+    assert s(0, 0, good, 1, None, None) == bq.BQ_ERR_NULL
+    assert s(0, 0, good, 1, ctypes.byref(hp0), None) == bq.BQ_ERR_ARG
+    assert s(0, 0, _tensors32(dict(row, state2=None)), 1, H, None) == bq.BQ_ERR_NULL
+    assert s(0, 0, _tensors32(dict(row, grad=MIS)), 1, H, None) == bq.BQ_ERR_ALIGN
+    assert s(0, 0, _tensors32(dict(row, state1=A16 + 8)), 1, H, None) == bq.BQ_ERR_ALIGN
+    assert s(0, 0, _tensors32(dict(row, numel=-1)), 1, H, None) == bq.BQ_ERR_SIZE
+    # Momentum needs no second state; empty tensors and empty lists are no-ops
+    assert s(2, 0, _tensors32(dict(row, state2=None, numel=0)), 1, H, None) == bq.BQ_OK
+    assert s(0, 0, None, 0, H, None) == bq.BQ_OK

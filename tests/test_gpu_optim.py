@@ -1,0 +1,258 @@
+"""The drop-in optimizers (paper_2110_02861_amd.optim) against the oracle.
+
+Each step is checked from the same state on both sides (the oracle starts from
+the optimizer's state before the step): codes and absmax bit-exact, params
+within 1e-6 of |w| plus 1e-6 of the update.  32-bit-state tensors (Section 3.3)
+are checked against the oracle's step with fp32 states.
+"""
+from __future__ import annotations
+
+import io
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import host, needs_gpu, param_close, say
+from paper_2110_02861_amd import bq, optim, workloads
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+# ragged sizes: partial blocks, a tensor below one block, an exact multiple
+SHAPES = [(37, 129), (5000,), (3, 2048), (300,), (1,)]
+B = 2048
+
+CASES = {
+    "adam": (optim.Adam8bit, dict(lr=1e-3, betas=(0.9, 0.995), eps=1e-8, weight_decay=0.0),
+             oracle.ADAM),
+    "adam_l2": (optim.Adam8bit, dict(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.01),
+                oracle.ADAM),
+    "adamw": (optim.AdamW8bit, dict(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.01),
+              oracle.ADAMW),
+    "sgd": (optim.SGD8bit, dict(lr=0.1, momentum=0.9, weight_decay=1e-4), oracle.MOMENTUM),
+}
+
+
+def oracle_hp(kw):
+    if "momentum" in kw:
+        return dict(lr=kw["lr"], beta1=kw["momentum"], beta2=0.0, eps=0.0, wd=kw["weight_decay"])
+    return dict(lr=kw["lr"], beta1=kw["betas"][0], beta2=kw["betas"][1], eps=kw["eps"],
+                wd=kw["weight_decay"])
+
+
+def init_params(seed):
+    out = []
+    for i, s in enumerate(SHAPES):
+        rng = workloads.host_rng(seed, "c1", i, 0)
+        w = (rng.standard_normal(int(np.prod(s)), dtype=np.float32) * np.float32(0.02))
+        out.append(torch.nn.Parameter(torch.from_numpy(w.reshape(s)).cuda()))
+    return out
+
+
+def grads(seed, step, dtype):
+    out = []
+    for i, s in enumerate(SHAPES):
+        rng = workloads.host_rng(seed, "c1", i, step)
+        g = rng.standard_normal(int(np.prod(s))) * 1e-3
+        g[rng.random(g.size) < 1e-3] *= 100.0
+        out.append(g.astype(dtype).reshape(s))
+    return out
+
+
+def set_grad(p, g):
+    """Attach a host grad; an fp16 grad on an fp32 param needs grad_dtype None."""
+    t = torch.from_numpy(np.ascontiguousarray(g)).cuda()
+    if t.dtype != p.dtype and hasattr(p, "grad_dtype"):
+        p.grad_dtype = None
+    p.grad = t
+
+
+def snapshot(opt, p):
+    """Host copy of one param's optimizer state (None before its first step)."""
+    s = opt.state.get(p)
+    if not s:
+        return None
+    return {k: (host(v).copy() if isinstance(v, torch.Tensor) else v) for k, v in s.items()}
+
+
+def oracle_step8(kind, hp, w, g, snap, n, two, t):
+    q1 = bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)
+    q2 = bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)
+    nb = (n + B - 1) // B
+    if snap is None:
+        c1, a1 = np.full(n, 127, np.uint8), np.zeros(nb, np.float32)
+        c2 = np.zeros(n, np.uint8) if two else None
+        a2 = np.zeros(nb, np.float32) if two else None
+    else:
+        c1, a1 = snap["state1"].copy(), snap["absmax1"].copy()
+        c2 = snap["state2"].copy() if two else None
+        a2 = snap["absmax2"].copy() if two else None
+    w = w.copy()
+    oracle.step8(kind, B, w, g, c1, a1, q1, c2, a2, q2 if two else None, hp["lr"], hp["beta1"],
+                 hp["beta2"], hp["eps"], hp["wd"], t)
+    return w, c1, a1, c2, a2
+
+
+@pytest.mark.parametrize("use_plans", [True, False])
+@pytest.mark.parametrize("gdt", [np.float32, np.float16])
+@pytest.mark.parametrize("case", list(CASES))
+def test_optimizer_matches_oracle(case, gdt, use_plans):
+    cls, kw, kind = CASES[case]
+    hp = oracle_hp(kw)
+    two = kind != oracle.MOMENTUM
+    params = init_params(7)
+    opt = cls(params, blocksize=B, use_plans=use_plans, **kw)
+    for t in range(1, 4):
+        gs = grads(7, t, gdt)
+        refs = []
+        for p, g in zip(params, gs):
+            refs.append(oracle_step8(kind, hp, host(p).ravel(), g.ravel(), snapshot(opt, p),
+                                     p.numel(), two, t))
+            set_grad(p, g)
+        say(f"optim {case} {np.dtype(gdt).name} plans={use_plans} step {t}")
+        w_before = [host(p).ravel().astype(np.float64) for p in params]
+        opt.step()
+        torch.cuda.synchronize()
+        for i, (p, ref) in enumerate(zip(params, refs)):
+            s = opt.state[p]
+            w_ref, c1, a1, c2, a2 = ref
+            assert s["step"] == t
+            assert np.array_equal(host(s["state1"]), c1), f"{case} tensor {i} step {t}: state1"
+            assert np.array_equal(host(s["absmax1"]), a1), f"{case} tensor {i} step {t}: absmax1"
+            if two:
+                assert np.array_equal(host(s["state2"]), c2), f"tensor {i} step {t}: state2"
+                assert np.array_equal(host(s["absmax2"]), a2), f"tensor {i} step {t}: absmax2"
+            upd = np.abs(w_before[i] - w_ref.astype(np.float64))
+            ok, worst = param_close(host(p).ravel(), w_ref, 1e-6 * upd)
+            assert ok, f"{case} tensor {i} step {t}: params off by {worst}"
+
+
+@pytest.mark.parametrize("case", ["adam", "adamw", "sgd"])
+def test_32bit_override_and_min_size(case):
+    """override_32bit and min_8bit_size keep fp32 states, updated like the
+    oracle's step with fp32 states; the other tensors stay 8-bit."""
+    cls, kw, kind = CASES[case]
+    hp = oracle_hp(kw)
+    two = kind != oracle.MOMENTUM
+    params = init_params(11)
+    opt = cls(params, blocksize=B, min_8bit_size=400, **kw)
+    opt.override_32bit(params[1])
+    for t in range(1, 3):
+        gs = grads(11, t, np.float32)
+        refs = {}
+        for i, (p, g) in enumerate(zip(params, gs)):
+            snap = snapshot(opt, p)
+            if i in (1, 3, 4):  # overridden, and below min_8bit_size
+                w = host(p).ravel().copy()
+                m = snap["exp_avg"].copy() if snap else np.zeros(p.numel(), np.float32)
+                v = (snap["exp_avg_sq"].copy() if snap else np.zeros(p.numel(), np.float32)) \
+                    if two else None
+                oracle.step32(kind, w, g.ravel(), m, v, hp["lr"], hp["beta1"], hp["beta2"],
+                              hp["eps"], hp["wd"], t)
+                refs[i] = (w, m, v)
+            set_grad(p, g)
+        say(f"optim override {case} step {t}")
+        w_before = [host(p).ravel().astype(np.float64) for p in params]
+        opt.step()
+        torch.cuda.synchronize()
+        for i, p in enumerate(params):
+            s = opt.state[p]
+            if i not in refs:
+                assert "state1" in s and s["state1"].dtype == torch.uint8
+                continue
+            assert "exp_avg" in s and "state1" not in s
+            w, m, v = refs[i]
+            assert np.array_equal(host(s["exp_avg"]), m), f"tensor {i} step {t}: m"
+            if two:
+                assert np.array_equal(host(s["exp_avg_sq"]), v), f"tensor {i} step {t}: v"
+            upd = np.abs(w_before[i] - w.astype(np.float64))
+            ok, worst = param_close(host(p).ravel(), w, 1e-6 * upd)
+            assert ok, f"tensor {i} step {t}: params off by {worst}"
+    with pytest.raises(RuntimeError):
+        opt.override_32bit(params[0])
+
+
+def test_state_dict_round_trip_resumes_bit_exactly():
+    """Save after 2 steps, load into a fresh optimizer over copied params, and
+    both continue identically (codes, absmax, params, step count)."""
+    params_a = init_params(3)
+    opt_a = optim.Adam8bit(params_a, lr=1e-3, betas=(0.9, 0.995))
+    opt_a.override_32bit(params_a[2])
+    for t in (1, 2):
+        for p, g in zip(params_a, grads(3, t, np.float32)):
+            set_grad(p, g)
+        opt_a.step()
+    buf = io.BytesIO()
+    torch.save(opt_a.state_dict(), buf)
+    buf.seek(0)
+    sd = torch.load(buf, weights_only=True)
+    params_b = [torch.nn.Parameter(p.detach().clone()) for p in params_a]
+    opt_b = optim.Adam8bit(params_b, lr=1e-3, betas=(0.9, 0.995))
+    opt_b.override_32bit(params_b[2])
+    opt_b.load_state_dict(sd)
+    for t in (3, 4):
+        gs = grads(3, t, np.float32)
+        for pa, pb, g in zip(params_a, params_b, gs):
+            set_grad(pa, g)
+            set_grad(pb, g)
+        say(f"optim state_dict resume step {t}")
+        opt_a.step()
+        opt_b.step()
+    torch.cuda.synchronize()
+    for pa, pb in zip(params_a, params_b):
+        assert torch.equal(pa, pb)
+        sa, sb = opt_a.state[pa], opt_b.state[pb]
+        assert sa["step"] == sb["step"] == 4
+        for k in sa:
+            if isinstance(sa[k], torch.Tensor):
+                assert sa[k].dtype == sb[k].dtype, k
+                assert torch.equal(sa[k], sb[k]), k
+
+
+def test_plans_follow_reallocated_grads():
+    """Fresh grad tensors every step (as zero_grad(set_to_none=True) gives)
+    rebuild the cached plan; codes equal the plan-free path."""
+    params_a = init_params(5)
+    params_b = [torch.nn.Parameter(p.detach().clone()) for p in params_a]
+    opt_a = optim.Adam8bit(params_a, use_plans=True)
+    opt_b = optim.Adam8bit(params_b, use_plans=False)
+    for t in range(1, 4):
+        gs = grads(5, t, np.float16)
+        for pa, pb, g in zip(params_a, params_b, gs):
+            set_grad(pa, g)
+            set_grad(pb, g)
+        # grab a block so that the next grads land elsewhere
+        keep = torch.empty(1 << 20, device="cuda")
+        say(f"optim plans follow grads step {t}")
+        opt_a.step()
+        opt_b.step()
+        del keep
+    torch.cuda.synchronize()
+    assert len(opt_a._plans) <= optim.Optimizer8bit.MAX_PLANS
+    for pa, pb in zip(params_a, params_b):
+        sa, sb = opt_a.state[pa], opt_b.state[pb]
+        for k in ("state1", "absmax1", "state2", "absmax2"):
+            assert torch.equal(sa[k], sb[k]), k
+        upd = 1e-3 * torch.ones_like(pa)
+        assert torch.all((pa - pb).abs() <= 1e-6 * pa.abs() + 1e-6 * upd)
+
+
+def test_training_loop_reduces_loss():
+    """A least-squares fit with 8-bit Adam: the loss falls by orders of magnitude."""
+    torch.manual_seed(0)
+    x = torch.randn(4096, 64, device="cuda")
+    w_true = torch.randn(64, 16, device="cuda")
+    y = x @ w_true
+    model = torch.nn.Linear(64, 16, bias=True).cuda()
+    opt = optim.Adam8bit(model.parameters(), lr=3e-2)
+    say("optim training loop")
+    first = None
+    for _ in range(300):
+        opt.zero_grad(set_to_none=True)
+        loss = torch.nn.functional.mse_loss(model(x), y)
+        loss.backward()
+        opt.step()
+        first = first if first is not None else float(loss)
+    final = float(loss)
+    assert final < 1e-3 * first, (first, final)

@@ -1,0 +1,57 @@
+"""Host-side behaviour of the drop-in optimizers (no GPU needed)."""
+from __future__ import annotations
+
+import pytest
+import torch
+
+from paper_2110_02861_amd import optim
+
+
+def test_hyperparameter_checks():
+    p = [torch.nn.Parameter(torch.zeros(4))]
+    with pytest.raises(ValueError):
+        optim.Adam8bit(p, lr=-1.0)
+    with pytest.raises(ValueError):
+        optim.Adam8bit(p, betas=(0.9, 1.0))
+    with pytest.raises(ValueError):
+        optim.AdamW8bit(p, eps=-1e-8)
+    with pytest.raises(ValueError):
+        optim.SGD8bit(p, momentum=1.5)
+    with pytest.raises(ValueError):
+        optim.Adam8bit(p, blocksize=1000)
+    with pytest.raises(ValueError):
+        optim.Adam8bit(p, min_8bit_size=-1)
+
+
+def test_defaults_follow_torch():
+    p = [torch.nn.Parameter(torch.zeros(4))]
+    a = optim.Adam8bit(p)
+    assert a.defaults == dict(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.0)
+    w = optim.AdamW8bit(p)
+    assert w.defaults["weight_decay"] == 1e-2
+    s = optim.SGD8bit(p, lr=0.1)
+    assert s.defaults == dict(lr=0.1, momentum=0.9, weight_decay=0.0)
+    assert a.blocksize == 2048 and a.min_8bit_size == 0 and a.use_plans
+
+
+def test_cpu_tensors_fail_loudly():
+    """No CPU fallback: a step on CPU params raises instead of computing."""
+    m = torch.nn.Linear(4, 3)
+    opt = optim.Adam8bit(m.parameters())
+    m(torch.randn(2, 4)).sum().backward()
+    with pytest.raises(TypeError, match="GPU"):
+        opt.step()
+
+
+def test_hparams_per_group():
+    a = torch.nn.Parameter(torch.zeros(4))
+    b = torch.nn.Parameter(torch.zeros(4))
+    opt = optim.Adam8bit([{"params": [a]}, {"params": [b], "lr": 5e-4, "betas": (0.8, 0.99)}],
+                         weight_decay=0.1)
+    h0 = opt._hparams(opt.param_groups[0], 3)
+    h1 = opt._hparams(opt.param_groups[1], 7)
+    assert h0 == dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.1, step=3)
+    assert h1 == dict(lr=5e-4, beta1=0.8, beta2=0.99, eps=1e-8, wd=0.1, step=7)
+    sgd = optim.SGD8bit([a], lr=0.2, momentum=0.5, weight_decay=1e-4)
+    assert sgd._hparams(sgd.param_groups[0], 1) == dict(lr=0.2, beta1=0.5, beta2=0.0, eps=0.0,
+                                                        wd=1e-4, step=1)
