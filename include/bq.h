@@ -51,7 +51,14 @@ typedef enum bq_status {
     BQ_ERR_ARG = 8        /* a scalar argument is out of range (e.g. step < 1) */
 } bq_status;
 
-typedef enum bq_codebook_kind { BQ_SIGNED = 0, BQ_UNSIGNED = 1 } bq_codebook_kind;
+typedef enum bq_codebook_kind {
+    BQ_SIGNED = 0,            /* dynamic tree map, signed (Section 2.3) */
+    BQ_UNSIGNED = 1,          /* dynamic map, unsigned (Section 3.2) */
+    BQ_INVERSE_SIGNED = 2,    /* inverse dynamic map, signed (App. F.1) */
+    BQ_INVERSE_UNSIGNED = 3,  /* inverse dynamic map, unsigned (App. F.1) */
+    BQ_LINEAR_SIGNED = 4,     /* 256 evenly spaced values in [-1, 1] */
+    BQ_LINEAR_UNSIGNED = 5    /* 256 evenly spaced values in [0, 1] */
+} bq_codebook_kind;
 typedef enum bq_optimizer { BQ_ADAM = 0, BQ_ADAMW = 1, BQ_MOMENTUM = 2 } bq_optimizer;
 typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1 } bq_dtype;
 
@@ -69,6 +76,35 @@ typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1 } bq_dtype;
  * Errors: BQ_ERR_NULL (out == NULL), BQ_ERR_ENUM (unknown kind).
  */
 bq_status bq_make_dynamic_codebook(bq_codebook_kind kind, float out[256]);
+
+/*
+ * Any of the fixed codebooks of bq_codebook_kind (host, synchronous), sorted
+ * ascending, each entry the exact rational rounded once to fp32.
+ *   BQ_SIGNED, BQ_UNSIGNED: as bq_make_dynamic_codebook.
+ *   BQ_INVERSE_SIGNED, BQ_INVERSE_UNSIGNED (App. F.1): the dynamic layout with
+ *     the exponent run counted from the other end -- E zero bits select decade
+ *     10^-(Emax - E) (Emax = 6 signed, 7 unsigned) and keep F = Emax - E
+ *     fraction bits, so the smallest decade gets the most values:
+ *     signed ±10^-k (0.1 + 0.9 j / 2^k), j = 1..2^k, k = 0..6, plus 0 and
+ *     +1e-7; unsigned k = 0..7 plus 0.  Both reach exactly 1.
+ *   BQ_LINEAR_SIGNED: (2i - 255) / 255; BQ_LINEAR_UNSIGNED: i / 255.
+ * Errors: BQ_ERR_NULL, BQ_ERR_ENUM.
+ */
+bq_status bq_make_codebook(bq_codebook_kind kind, float out[256]);
+
+/*
+ * Quantile map of a sample (App. F.2, lossy minimum-entropy encoding), host,
+ * synchronous: with the sample quantile Q(p) = sorted[floor(p n)],
+ *   q_i = (Q(i / 257) + Q((i + 1) / 257)) / 2,   i = 0..255,
+ * computed in double, divided by max_i |q_i| (so the map spans [-1, 1], or
+ * [0, 1] for a non-negative sample) and rounded once to fp32.  Entries that
+ * come out equal (ties in the sample) are separated upward by one ulp so the
+ * map stays strictly increasing.
+ *   sample  host array of n fp32 values (read), all finite
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE (n < 1), BQ_ERR_ARG (a non-finite value,
+ * or every q_i zero).
+ */
+bq_status bq_make_quantile_codebook(const float *sample, int64_t n, float out[256]);
 
 /*
  * Block-wise quantization (Section 3.1, Eq. 4).  For each block b:

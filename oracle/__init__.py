@@ -50,6 +50,10 @@ def lib() -> ctypes.CDLL:
                              ctypes.c_int64, ctypes.c_float)
         L.oracle_dynamic_codebook.argtypes = [I, P]
         L.oracle_dynamic_codebook.restype = I
+        L.oracle_codebook.argtypes = [I, P]
+        L.oracle_codebook.restype = I
+        L.oracle_quantile_codebook.argtypes = [P, ctypes.c_int64, P]
+        L.oracle_quantile_codebook.restype = I
         L.oracle_nearest_brute.argtypes = [P, F]
         L.oracle_nearest_brute.restype = I
         L.oracle_nearest_bsearch.argtypes = [P, F]
@@ -84,6 +88,23 @@ def dynamic_codebook(kind: int) -> np.ndarray:
     out = np.empty(256, np.float32)
     if lib().oracle_dynamic_codebook(int(kind), out.ctypes.data) != 0:
         raise ValueError(f"unknown codebook kind {kind}")
+    return out
+
+
+def codebook(kind: int) -> np.ndarray:
+    """Fixed maps: 0/1 dynamic, 2/3 inverse dynamic, 4/5 linear (signed/unsigned)."""
+    out = np.empty(256, np.float32)
+    if lib().oracle_codebook(int(kind), out.ctypes.data) != 0:
+        raise ValueError(f"unknown codebook kind {kind}")
+    return out
+
+
+def quantile_codebook(sample) -> np.ndarray:
+    """Quantile map (App. F.2) of a host sample."""
+    x = np.ascontiguousarray(sample, dtype=np.float32).ravel()
+    out = np.empty(256, np.float32)
+    if lib().oracle_quantile_codebook(x.ctypes.data, x.size, out.ctypes.data) != 0:
+        raise ValueError("quantile map: empty or non-finite sample, or all-zero map")
     return out
 
 

@@ -97,41 +97,152 @@ ORACLE_API int oracle_dynamic_codebook(int kind, float out[256])
     return 0;
 }
 
+/*
+ * Further fixed maps (App. F):
+ * kind 2 / 3 = inverse dynamic, signed / unsigned (App. F.1).  Reading: the
+ *   exponent run is counted from the small end -- with E zero bits the value
+ *   lies in decade 10^-(Emax - E) (Emax = 6 signed, 7 unsigned) and keeps
+ *   F = Emax - E fraction bits, so decade 10^-k holds 2^k values:
+ *   signed: +-10^-k (0.1 + 0.9 j / 2^k), j = 1..2^k, k = 0..6, plus 0 and
+ *   +1e-7 (the base); unsigned: k = 0..7, plus 0.
+ * kind 4 / 5 = linear, signed / unsigned (the ablation baseline): 256 evenly
+ *   spaced values, (2i - 255) / 255 or i / 255, i = 0..255.
+ * kinds 0 and 1 are the dynamic maps above.  Sorted ascending.  Returns 0, or
+ * -1 for an unknown kind.
+ */
+ORACLE_API int oracle_codebook(int kind, float out[256])
+{
+    int k = 0;
+    if (kind == 0 || kind == 1)
+        return oracle_dynamic_codebook(kind, out);
+    if (kind == 2) {
+        for (int dec = 0; dec <= 6; ++dec)
+            for (int j = 1; j <= (1 << dec); ++j) {
+                float v = decade_value(dec, dec, j);
+                out[k++] = v;
+                out[k++] = -v;
+            }
+        out[k++] = 0.0f;
+        out[k++] = decade_value(7, 0, 1); /* 1e-7 */
+    } else if (kind == 3) {
+        for (int dec = 0; dec <= 7; ++dec)
+            for (int j = 1; j <= (1 << dec); ++j)
+                out[k++] = decade_value(dec, dec, j);
+        out[k++] = 0.0f;
+    } else if (kind == 4 || kind == 5) {
+        for (int i = 0; i < 256; ++i)
+            out[k++] = (float)((kind == 4 ? (double)(2 * i - 255) : (double)i) / 255.0);
+    } else {
+        return -1;
+    }
+    qsort(out, 256, sizeof(float), cmp_float);
+    return 0;
+}
+
+static int cmp_double(const void *a, const void *b)
+{
+    double x = *(const double *)a, y = *(const double *)b;
+    return (x > y) - (x < y);
+}
+
+/*
+ * Quantile map of a sample (App. F.2, Eq. 5): with the sample quantile
+ * Q(p) = sorted[floor(p n)] (the value at index p n of the sorted sample),
+ *   q_i = (Q(i / (2^k + 1)) + Q((i + 1) / (2^k + 1))) / 2,  i = 0..2^k - 1,
+ * k = 8, in double; then divided by max |q_i| so the map spans [-1, 1]
+ * (Fig. of the data types normalizes the map that way) and rounded to fp32.
+ * Reading: equal entries (ties in the sample) are moved up by one ulp in
+ * order, keeping code = rank well defined.  Returns 0, or -1 for n < 1, a
+ * non-finite value or an all-zero map.
+ */
+ORACLE_API int oracle_quantile_codebook(const float *x, int64_t n, float out[256])
+{
+    if (n < 1)
+        return -1;
+    double *s = (double *)malloc(sizeof(double) * (size_t)n);
+    if (!s)
+        return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        if (!isfinite(x[i])) {
+            free(s);
+            return -1;
+        }
+        s[i] = x[i];
+    }
+    qsort(s, (size_t)n, sizeof(double), cmp_double);
+    double q[256], amax = 0.0;
+    for (int i = 0; i < 256; ++i) {
+        int64_t a = (int64_t)((__int128)i * n / 257);
+        int64_t b = (int64_t)((__int128)(i + 1) * n / 257);
+        if (a > n - 1)
+            a = n - 1;
+        if (b > n - 1)
+            b = n - 1;
+        q[i] = (s[a] + s[b]) / 2.0;
+        if (fabs(q[i]) > amax)
+            amax = fabs(q[i]);
+    }
+    free(s);
+    if (!(amax > 0.0))
+        return -1;
+    for (int i = 0; i < 256; ++i) {
+        out[i] = (float)(q[i] / amax);
+        if (i > 0 && !(out[i] > out[i - 1]))
+            out[i] = nextafterf(out[i - 1], INFINITY);
+    }
+    return 0;
+}
+
 /* ------------------------------------------------------------------------- */
 /* Nearest code: Eq. 3 / Eq. 4 argmin over the 256 map entries.               */
 /* ------------------------------------------------------------------------- */
 
 /*
+ * Exact sign of 2y - (a + b) for binary32 y, a, b.  For a < b,
+ * |y - a| < |y - b|  <=>  (y - a)^2 < (y - b)^2  <=>  2y (b - a) < b^2 - a^2
+ *                    <=>  2y < a + b,
+ * so this decides which of two codes is nearer, with no rounding: a + b is
+ * split exactly into s + e (Knuth's two-sum in double), t = 2y is exact, and
+ * t - s is exact when t and s are within a factor 2 of each other (Sterbenz);
+ * otherwise |t - s| exceeds |e| and decides alone.
+ */
+static int sign_twice_y_minus_sum(float y, float a, float b)
+{
+    double A = a, B = b;
+    double s = A + B;
+    double bv = s - A;
+    double e = (A - (s - bv)) + (B - bv);
+    double t = 2.0 * (double)y;
+    if ((s > 0.0 && t >= 0.5 * s && t <= 2.0 * s) || (s < 0.0 && t <= 0.5 * s && t >= 2.0 * s)) {
+        double d = t - s;
+        return (d > e) - (d < e);
+    }
+    return (t > s) - (t < s);
+}
+
+/*
  * Definition of Eq. 3: argmin_j |q_j - y| over j = 0..255 (Reading: the
  * printed upper limit 2^n means the last index 2^k - 1).  Ties go to the lower
  * index (Reading: the paper is silent; exact ties happen because many
- * midpoints of adjacent codes are binary32 numbers).
- *
- * Distances are taken in double.  For the two codes bracketing y the operands
- * are within a factor of 2^4 of each other (or one is zero), so y - q is exact
- * and the comparison between them is exact; every other code is farther away
- * by at least one whole code gap, far beyond a double rounding error.
+ * midpoints of adjacent codes are binary32 numbers).  A linear scan keeps the
+ * nearest code so far and moves to a later (larger) code only when that one is
+ * strictly nearer, decided exactly by sign_twice_y_minus_sum.  Requires a
+ * strictly increasing map.
  */
 ORACLE_API int oracle_nearest_brute(const float *qmap, float y)
 {
     int best = 0;
-    double bestd = fabs((double)y - (double)qmap[0]);
-    for (int j = 1; j < 256; ++j) {
-        double d = fabs((double)y - (double)qmap[j]);
-        if (d < bestd) {
-            bestd = d;
+    for (int j = 1; j < 256; ++j)
+        if (sign_twice_y_minus_sum(y, qmap[best], qmap[j]) > 0)
             best = j;
-        }
-    }
     return best;
 }
 
 /*
  * The same argmin by binary search (Section 2.2 finds the closest value "via a
  * binary search"): locate i with q_i <= y < q_{i+1}, then take i + 1 when y
- * lies strictly above the midpoint (q_i + q_{i+1}) / 2, else i.  The midpoint
- * is formed in double, where it is exact for adjacent codes within a factor
- * 2^29 of each other.  Requires a strictly increasing map.
+ * lies strictly above the midpoint of q_i and q_{i+1} (the exact predicate
+ * above), else i.  Requires a strictly increasing map.
  */
 ORACLE_API int oracle_nearest_bsearch(const float *qmap, float y)
 {
@@ -147,8 +258,7 @@ ORACLE_API int oracle_nearest_bsearch(const float *qmap, float y)
         else
             hi = mid;
     }
-    double m = ((double)qmap[lo] + (double)qmap[lo + 1]) * 0.5;
-    return ((double)y > m) ? lo + 1 : lo;
+    return sign_twice_y_minus_sum(y, qmap[lo], qmap[lo + 1]) > 0 ? lo + 1 : lo;
 }
 
 /* ------------------------------------------------------------------------- */

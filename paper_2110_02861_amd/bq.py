@@ -18,11 +18,17 @@ LIB_PATH = os.path.join(_PKG, "libbq.so")
 BQ_OK, BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_BLOCKSIZE, BQ_ERR_ENUM = 0, 1, 2, 3, 4
 BQ_ERR_DTYPE, BQ_ERR_ALIGN, BQ_ERR_HIP, BQ_ERR_ARG = 5, 6, 7, 8
 BQ_SIGNED, BQ_UNSIGNED = 0, 1
+BQ_INVERSE_SIGNED, BQ_INVERSE_UNSIGNED = 2, 3
+BQ_LINEAR_SIGNED, BQ_LINEAR_UNSIGNED = 4, 5
+CODEBOOKS = {"dynamic": (BQ_SIGNED, BQ_UNSIGNED),
+             "inverse_dynamic": (BQ_INVERSE_SIGNED, BQ_INVERSE_UNSIGNED),
+             "linear": (BQ_LINEAR_SIGNED, BQ_LINEAR_UNSIGNED)}
 BQ_ADAM, BQ_ADAMW, BQ_MOMENTUM = 0, 1, 2
 BQ_F32, BQ_F16 = 0, 1
 OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM}
 
-EXPORTS = ("bq_make_dynamic_codebook", "bq_quantize_blockwise", "bq_dequantize_blockwise",
+EXPORTS = ("bq_make_dynamic_codebook", "bq_make_codebook", "bq_make_quantile_codebook",
+           "bq_quantize_blockwise", "bq_dequantize_blockwise",
            "bq_optimizer8bit_step", "bq_optimizer32bit_step", "bq_prepare_codebook",
            "bq_quantize_blockwise_prepared",
            "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_destroy",
@@ -69,6 +75,10 @@ def lib() -> ctypes.CDLL:
         P, I32, I64, I = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int
         L.bq_make_dynamic_codebook.argtypes = [I, P]
         L.bq_make_dynamic_codebook.restype = I
+        L.bq_make_codebook.argtypes = [I, P]
+        L.bq_make_codebook.restype = I
+        L.bq_make_quantile_codebook.argtypes = [P, I64, P]
+        L.bq_make_quantile_codebook.restype = I
         L.bq_quantize_blockwise.argtypes = [P, P, I64, I32, P, P, P]
         L.bq_quantize_blockwise.restype = I
         L.bq_dequantize_blockwise.argtypes = [P, P, P, I64, I32, P, P]
@@ -122,6 +132,22 @@ def bq_make_dynamic_codebook(kind: int) -> np.ndarray:
     """Host call: the 256-entry signed (0) or unsigned (1) dynamic codebook."""
     out = np.empty(256, np.float32)
     _check(lib().bq_make_dynamic_codebook(int(kind), out.ctypes.data), "bq_make_dynamic_codebook")
+    return out
+
+
+def bq_make_codebook(kind: int) -> np.ndarray:
+    """Host call: any fixed codebook (BQ_SIGNED ... BQ_LINEAR_UNSIGNED)."""
+    out = np.empty(256, np.float32)
+    _check(lib().bq_make_codebook(int(kind), out.ctypes.data), "bq_make_codebook")
+    return out
+
+
+def bq_make_quantile_codebook(sample) -> np.ndarray:
+    """Host call: the quantile map of a host fp32 sample (App. F.2)."""
+    x = np.ascontiguousarray(sample, dtype=np.float32).ravel()
+    out = np.empty(256, np.float32)
+    _check(lib().bq_make_quantile_codebook(x.ctypes.data if x.size else None, x.size,
+                                           out.ctypes.data), "bq_make_quantile_codebook")
     return out
 
 

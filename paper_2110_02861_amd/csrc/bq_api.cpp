@@ -143,6 +143,24 @@ bq_status bq_make_dynamic_codebook(bq_codebook_kind kind, float out[256])
     return bq::build_dynamic_codebook(static_cast<int>(kind), out) == 0 ? BQ_OK : BQ_ERR_ENUM;
 }
 
+bq_status bq_make_codebook(bq_codebook_kind kind, float out[256])
+{
+    if (out == nullptr)
+        return BQ_ERR_NULL;
+    if (static_cast<int>(kind) < BQ_SIGNED || static_cast<int>(kind) > BQ_LINEAR_UNSIGNED)
+        return BQ_ERR_ENUM;
+    return bq::build_dynamic_codebook(static_cast<int>(kind), out) == 0 ? BQ_OK : BQ_ERR_ENUM;
+}
+
+bq_status bq_make_quantile_codebook(const float *sample, int64_t n, float out[256])
+{
+    if (!sample || !out)
+        return BQ_ERR_NULL;
+    if (n < 1)
+        return BQ_ERR_SIZE;
+    return bq::build_quantile_codebook(sample, n, out) == 0 ? BQ_OK : BQ_ERR_ARG;
+}
+
 bq_status bq_quantize_blockwise(const float *qmap, const float *x, int64_t n, int32_t blocksize,
                                 uint8_t *codes, float *absmax, hipStream_t stream)
 {

@@ -54,6 +54,27 @@ __device__ inline float next_up(float f)
     return __uint_as_float(f > 0.0f ? u + 1u : u - 1u);
 }
 
+__device__ inline float next_down(float f)
+{
+    return -next_up(-f);
+}
+
+// True when y lies strictly above the exact midpoint of a and b, i.e. when
+// 2y > a + b without rounding: for a < b this is "y is strictly nearer b".
+// a + b = s + e exactly (two-sum in double); 2y - s is exact when 2y and s are
+// within a factor 2 of each other, and otherwise outweighs e.
+__device__ inline bool above_midpoint(float y, float a, float b)
+{
+    const double A = a, Bd = b;
+    const double s = A + Bd;
+    const double bv = s - A;
+    const double e = (A - (s - bv)) + (Bd - bv);
+    const double t = 2.0 * (double)y;
+    const bool close = (s > 0.0 && t >= 0.5 * s && t <= 2.0 * s) ||
+                       (s < 0.0 && t <= 0.5 * s && t >= 2.0 * s);
+    return close ? (t - s) > e : t > s;
+}
+
 // #{j : t_j <= v} for finite v (at most 255 since t_255 = +inf).
 __device__ inline uint32_t count_le(const float *t, float v)
 {
@@ -88,12 +109,18 @@ __device__ void build_tables(const float *__restrict__ qmap, float *q, float *t,
         q[j] = qj;
         float thr = __builtin_inff();
         if (j < 255) {
-            // adjacent codes of a valid map are within 2^29 of each other, so
-            // the double sum is exact
-            const double mid = ((double)qj + (double)qmap[j + 1]) * 0.5;
+            // the smallest fp32 strictly above the exact midpoint: start from
+            // the double midpoint (exact unless the codes are 2^29 apart in
+            // magnitude) and settle it with the exact comparison
+            const float qn = qmap[j + 1];
+            const double mid = ((double)qj + (double)qn) * 0.5;
             float f = (float)mid;
             if ((double)f <= mid)
                 f = next_up(f);
+            for (int k = 0; k < 4 && !above_midpoint(f, qj, qn); ++k)
+                f = next_up(f);
+            for (int k = 0; k < 4 && above_midpoint(next_down(f), qj, qn); ++k)
+                f = next_down(f);
             thr = f;
         }
         t[j] = thr;

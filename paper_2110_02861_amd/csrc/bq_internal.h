@@ -136,5 +136,6 @@ hipError_t launch_dequantize(const float *qmap, const uint8_t *codes, const floa
 
 // Host-side codebook construction (bq_codebook.cpp).
 int build_dynamic_codebook(int kind, float out[256]);
+int build_quantile_codebook(const float *sample, int64_t n, float out[256]);
 
 }  // namespace bq

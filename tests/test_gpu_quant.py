@@ -140,3 +140,94 @@ def test_non_default_stream_ordering():
     c_ref, a_ref = oracle.quantize_blockwise(qs, x, 2048)
     np.testing.assert_array_equal(host(c_d), c_ref)
     np.testing.assert_array_equal(host(out), oracle.dequantize_blockwise(qs, c_ref, a_ref, 2048))
+
+
+# --- other codebooks (App. F): the same kernels with any sorted 256-entry map ---
+
+def _other_maps():
+    """name -> (host map from the oracle, signed input?)."""
+    normal = workloads.host_rng(0, "c2", 1, 0).standard_normal(200_001).astype(np.float32)
+    heavy = np.abs(workloads.student_t_host(200_001, seed=11))
+    return {
+        "inverse_signed": (oracle.codebook(2), True),
+        "inverse_unsigned": (oracle.codebook(3), False),
+        "linear_signed": (oracle.codebook(4), True),
+        "linear_unsigned": (oracle.codebook(5), False),
+        "quantile_normal": (oracle.quantile_codebook(normal), True),
+        "quantile_abs_t": (oracle.quantile_codebook(heavy), False),
+    }
+
+
+OTHER = ["inverse_signed", "inverse_unsigned", "linear_signed", "linear_unsigned",
+         "quantile_normal", "quantile_abs_t"]
+
+
+@pytest.mark.parametrize("B", [256, 2048, 4096])
+@pytest.mark.parametrize("name", OTHER)
+def test_other_codebooks_ragged(name, B):
+    q, signed = _other_maps()[name]
+    n = 3 * max(B, 2048) + 1234
+    x = workloads.student_t_host(n, seed=B + 1)
+    run_pair(q, dev(q), x if signed else np.abs(x), B)
+
+
+@pytest.mark.parametrize("name", OTHER)
+def test_other_codebooks_ties_and_round_trip(name):
+    """Midpoints of adjacent codes and one ulp either side (ties to the lower
+    code), and dequantize -> quantize returns every code."""
+    q, _ = _other_maps()[name]
+    q_d = dev(q)
+    ys = []
+    for j in range(255):
+        m = np.float32((float(q[j]) + float(q[j + 1])) / 2.0)
+        ys += [np.nextafter(m, np.float32(-np.inf), dtype=np.float32), m,
+               np.nextafter(m, np.float32(np.inf), dtype=np.float32)]
+    ys = np.array(ys, np.float32)
+    B = 2048
+    amax = np.float32(np.max(np.abs(q)))
+    blocks = []
+    for s0 in range(0, ys.size, B - 1):
+        chunk = ys[s0:s0 + B - 1]
+        blk = np.zeros(B, np.float32)
+        blk[:chunk.size] = chunk
+        blk[-1] = amax           # absmax = max |q|: the quotients stay as built
+        blocks.append(blk)
+    run_pair(q, q_d, np.concatenate(blocks), B)
+    codes = np.tile(np.arange(256, dtype=np.uint8), 4)
+    absmax = np.array([1.0, 0.37, 3e-5, 12345.678], np.float32)
+    say(f"round trip {name}")
+    x = bq.bq_dequantize_blockwise(q_d, dev(codes), dev(absmax), 256)
+    c2, _ = bq.bq_quantize_blockwise(q_d, x, 256)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(c2), codes)
+
+
+def test_exact_thresholds_for_uneven_maps():
+    """Maps with adjacent codes of very different magnitude (where a double
+    midpoint is inexact): decisions at and around those midpoints stay exact."""
+    q = oracle.codebook(4).copy()
+    q2 = q.copy()
+    q2[127] = np.float32(-1e-43)
+    q3 = q2.copy()
+    q3[128] = np.float32(0.5)
+    q3[129:] = np.linspace(0.5, 1.0, 128, dtype=np.float32)[1:]
+    for qm in (q, q2, q3):
+        assert np.all(np.diff(qm) > 0)
+        ys = [np.float32(0.0), np.float32(2.0 ** -149), np.float32(-2.0 ** -149)]
+        for j in range(255):
+            m = np.float32((float(qm[j]) + float(qm[j + 1])) / 2.0)
+            for k in range(-2, 3):
+                y = m
+                for _ in range(abs(k)):
+                    y = np.nextafter(y, np.float32(np.sign(k)), dtype=np.float32)
+                ys.append(y)
+        x = np.array(ys, np.float32)
+        B = 2048
+        blocks = []
+        for s0 in range(0, x.size, B - 1):
+            blk = np.zeros(B, np.float32)
+            chunk = x[s0:s0 + B - 1]
+            blk[:chunk.size] = chunk
+            blk[-1] = 1.0
+            blocks.append(blk)
+        run_pair(qm, dev(qm), np.concatenate(blocks), B)

@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from paper_2110_02861_amd import bq, workloads
 from tests.gpu_helpers import (DevState, HostState, codebooks_on_device, codes_agree, host,
                                needs_gpu, param_close, say)
@@ -25,8 +26,12 @@ HPS = {
 }
 
 
-def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=True, path="plan"):
+def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=True, path="plan",
+              maps=None):
     qs, qu, qs_d, qu_d = codebooks_on_device()
+    if maps is not None:  # (state-1 map, state-2 map), host fp32
+        qs, qu = maps
+        qs_d, qu_d = torch.from_numpy(qs).cuda(), torch.from_numpy(qu).cuda()
     two = opt != "momentum"
     hp = dict(HPS[opt] if hp is None else hp)
     tdt = torch.float16 if grad_dtype == bq.BQ_F16 else torch.float32
@@ -198,3 +203,24 @@ def test_determinism_and_resume():
     run(c, 3, 5)
     for x, y in zip((a.w, a.c1, a.c2, a.a1, a.a2), (c.w, c.c1, c.c2, c.a1, c.a2)):
         assert torch.equal(x, y)
+
+
+def _map_families():
+    normal = workloads.host_rng(0, "c2", 2, 0).standard_normal(100_001).astype(np.float32)
+    heavy = np.abs(workloads.student_t_host(100_001, seed=13))
+    return {
+        "inverse_dynamic": (oracle.codebook(2), oracle.codebook(3)),
+        "linear": (oracle.codebook(4), oracle.codebook(5)),
+        "quantile": (oracle.quantile_codebook(normal), oracle.quantile_codebook(heavy)),
+    }
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("family", ["inverse_dynamic", "linear", "quantile"])
+@pytest.mark.parametrize("opt", ["adam", "momentum"])
+def test_other_codebooks_step(opt, family, path):
+    """The step with the App. F maps (the inverse unsigned map puts up to 28
+    thresholds in one bucket: the general search path)."""
+    q1, q2 = _map_families()[family]
+    run_lists(opt, 2048, bq.BQ_F16, [1, 2047, 4097, 3 * 4096 + 77], 3, seed=5, path=path,
+              maps=(q1, q2))
