@@ -5,7 +5,7 @@
  * "8-bit Optimizers via Block-wise Quantization" (ICLR 2022):
  *   - the dynamic (tree) quantization codebooks          (Sections 2.3, 3.2)
  *   - block-wise quantization and dequantization         (Sections 2.2, 3.1, Eq. 3-4)
- *   - the fused 8-bit Adam / AdamW / Momentum step       (Section 3, Eq. 1-2)
+ *   - the fused 8-bit Adam / AdamW / Momentum / AdaGrad step (Section 3, Eq. 1-2, App. H)
  *
  * Conventions shared by every call
  *   - Pointers named "device" must point to GPU memory of the current HIP
@@ -59,7 +59,7 @@ typedef enum bq_codebook_kind {
     BQ_LINEAR_SIGNED = 4,     /* 256 evenly spaced values in [-1, 1] */
     BQ_LINEAR_UNSIGNED = 5    /* 256 evenly spaced values in [0, 1] */
 } bq_codebook_kind;
-typedef enum bq_optimizer { BQ_ADAM = 0, BQ_ADAMW = 1, BQ_MOMENTUM = 2 } bq_optimizer;
+typedef enum bq_optimizer { BQ_ADAM = 0, BQ_ADAMW = 1, BQ_MOMENTUM = 2, BQ_ADAGRAD = 3 } bq_optimizer;
 typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1 } bq_dtype;
 
 /*
@@ -142,9 +142,9 @@ typedef struct bq_tensor {
     float *param;       /* numel fp32, updated in place */
     const void *grad;   /* numel fp32 or fp16 (see grad_dtype), read only */
     uint8_t *state1;    /* numel codes of the first state (m), in place */
-    uint8_t *state2;    /* numel codes of the second state (r); NULL for Momentum */
+    uint8_t *state2;    /* numel codes of the second state (r); NULL for Momentum, AdaGrad */
     float *absmax1;     /* ceil(numel / B) block absmax of state 1, in place */
-    float *absmax2;     /* ceil(numel / B) block absmax of state 2; NULL for Momentum */
+    float *absmax2;     /* ceil(numel / B) block absmax of state 2; NULL for Momentum, AdaGrad */
     int64_t numel;
 } bq_tensor;
 
@@ -166,12 +166,16 @@ typedef struct bq_hparams {
  *   AdamW: w *= (1 - lr * wd) first, then Adam without the L2 term.
  *   Momentum (Eq. 1): g += wd * w (if weight_decay != 0); m' = b1 m + g;
  *       w' = w - lr m'  (beta2 and eps unused).
+ *   AdaGrad (App. H, textbook form): g += wd * w (if weight_decay != 0);
+ *       r' = r + g^2 (state 1, non-negative: pass an unsigned map as qmap1);
+ *       w' = w - lr g / (sqrt(r') + eps)  (betas unused; no state 2).
  * State 1 uses qmap1 (the signed map), state 2 uses qmap2 (the unsigned map;
  * any map for state 2 must have no negative entries, so that r' >= 0).
+ * Momentum and AdaGrad have one state: state2, absmax2 and qmap2 may be NULL.
  * A zero state is every code at the index of 0.0 with absmax 0.
  *   tensors  host array of ntensors descriptors
  *   hp       host pointer to the hyperparameters
- *   qmap1    device, 256 fp32; qmap2 device, 256 fp32 (NULL for Momentum)
+ *   qmap1    device, 256 fp32; qmap2 device, 256 fp32 (NULL for Momentum, AdaGrad)
  * Arithmetic of the states is fp32 in a fixed order without contraction, so
  * codes and absmax are reproducible; the param update uses the hardware square
  * root and reciprocal (relative error a few ulp of the update).
@@ -188,7 +192,7 @@ typedef struct bq_tensor32 {
     float *param;       /* numel fp32, updated in place */
     const void *grad;   /* numel fp32 or fp16 (see grad_dtype), read only */
     float *state1;      /* numel fp32 first state (m), in place */
-    float *state2;      /* numel fp32 second state (r); NULL for Momentum */
+    float *state2;      /* numel fp32 second state (r); NULL for Momentum, AdaGrad */
     int64_t numel;
 } bq_tensor32;
 

@@ -23,7 +23,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "bq_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-ADAM, ADAMW, MOMENTUM = 0, 1, 2
+ADAM, ADAMW, MOMENTUM, ADAGRAD = 0, 1, 2, 3
 SIGNED, UNSIGNED = 0, 1
 
 
@@ -163,7 +163,7 @@ def step32(opt, w, g, m, v, lr, beta1, beta2, eps, wd, step):
     """Update w, m, v (fp32 states, quantization bypassed) in place."""
     _check(w, np.float32, "w")
     _check(m, np.float32, "m")
-    if opt != MOMENTUM:
+    if opt in (ADAM, ADAMW):
         _check(v, np.float32, "v")
     g = np.ascontiguousarray(g)
     rc = lib().oracle_step32(int(opt), w.size, w.ctypes.data, g.ctypes.data, _grad_kind(g),
@@ -179,7 +179,7 @@ def step8(opt, blocksize, w, g, c1, a1, q1, c2, a2, q2, lr, beta1, beta2, eps, w
     _check(c1, np.uint8, "c1")
     _check(a1, np.float32, "a1")
     _check(q1, np.float32, "q1")
-    if opt != MOMENTUM:
+    if opt in (ADAM, ADAMW):
         _check(c2, np.uint8, "c2")
         _check(a2, np.float32, "a2")
         _check(q2, np.float32, "q2")

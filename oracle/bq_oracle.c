@@ -357,7 +357,7 @@ ORACLE_API void oracle_half_to_float(const uint16_t *h, float *out, int64_t n)
 /* Optimizer update: Eq. 1 (Momentum), Eq. 2 (Adam), AdamW.                   */
 /* ------------------------------------------------------------------------- */
 
-enum { OR_ADAM = 0, OR_ADAMW = 1, OR_MOMENTUM = 2 };
+enum { OR_ADAM = 0, OR_ADAMW = 1, OR_MOMENTUM = 2, OR_ADAGRAD = 3 };
 
 /* beta^t by square-and-multiply in double (t >= 0). */
 static double pow_int(double beta, int64_t t)
@@ -413,11 +413,23 @@ static step_scalars make_scalars(float lr, float beta1, float beta2, float eps,
  *   AdamW:    w *= decay; then Adam with no L2 term
  *   Momentum: g += wd*w (if wd != 0); m' = b1*m + g; w' = w - lr*m'
  *             (with m = 0 at the first step this gives m_0 = g_0, Eq. 1)
+ *   AdaGrad (App. H; reading: the textbook method, no learning-rate decay,
+ *             zero initial accumulator): g += wd*w (if wd != 0);
+ *             m' = m + g*g (m holds the sum of squares);
+ *             w' = w - lr*(g/(sqrt(m') + eps))
  */
 static void update_element(int opt, const step_scalars *s, float *w, float g, float *m,
                            float *v)
 {
     float wv = *w;
+    if (opt == OR_ADAGRAD) {
+        if (s->wd != 0.0f)
+            g = g + s->wd * wv;
+        float mn = *m + g * g;
+        *m = mn;
+        *w = wv - s->lr * (g / (sqrtf(mn) + s->eps));
+        return;
+    }
     if (opt == OR_MOMENTUM) {
         if (s->wd != 0.0f)
             g = g + s->wd * wv;
@@ -452,13 +464,14 @@ ORACLE_API int oracle_step32(int opt, int64_t n, float *w, const void *g, int gr
                              float *m, float *v, float lr, float beta1, float beta2,
                              float eps, float wd, int64_t step)
 {
-    if (opt < OR_ADAM || opt > OR_MOMENTUM || step < 1)
+    if (opt < OR_ADAM || opt > OR_ADAGRAD || step < 1)
         return -1;
+    int two = (opt == OR_ADAM || opt == OR_ADAMW);
     step_scalars s = make_scalars(lr, beta1, beta2, eps, wd, step);
     for (int64_t i = 0; i < n; ++i) {
-        float vi = (opt == OR_MOMENTUM) ? 0.0f : v[i];
+        float vi = two ? v[i] : 0.0f;
         update_element(opt, &s, &w[i], load_grad(g, grad_is_f16, i), &m[i], &vi);
-        if (opt != OR_MOMENTUM)
+        if (two)
             v[i] = vi;
     }
     return 0;
@@ -478,9 +491,9 @@ ORACLE_API int oracle_step8(int opt, int32_t B, int grad_is_f16, int64_t n, floa
                             const float *q1, const float *q2, float lr, float beta1,
                             float beta2, float eps, float wd, int64_t step, int nthreads)
 {
-    if (opt < OR_ADAM || opt > OR_MOMENTUM || step < 1 || B <= 0)
+    if (opt < OR_ADAM || opt > OR_ADAGRAD || step < 1 || B <= 0)
         return -1;
-    int two = (opt != OR_MOMENTUM);
+    int two = (opt == OR_ADAM || opt == OR_ADAMW);
     step_scalars s = make_scalars(lr, beta1, beta2, eps, wd, step);
     int64_t nb = (n + B - 1) / B;
     set_threads(nthreads);

@@ -23,9 +23,10 @@ BQ_LINEAR_SIGNED, BQ_LINEAR_UNSIGNED = 4, 5
 CODEBOOKS = {"dynamic": (BQ_SIGNED, BQ_UNSIGNED),
              "inverse_dynamic": (BQ_INVERSE_SIGNED, BQ_INVERSE_UNSIGNED),
              "linear": (BQ_LINEAR_SIGNED, BQ_LINEAR_UNSIGNED)}
-BQ_ADAM, BQ_ADAMW, BQ_MOMENTUM = 0, 1, 2
+BQ_ADAM, BQ_ADAMW, BQ_MOMENTUM, BQ_ADAGRAD = 0, 1, 2, 3
 BQ_F32, BQ_F16 = 0, 1
-OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM}
+OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM,
+              "adagrad": BQ_ADAGRAD}
 
 EXPORTS = ("bq_make_dynamic_codebook", "bq_make_codebook", "bq_make_quantile_codebook",
            "bq_quantize_blockwise", "bq_dequantize_blockwise",

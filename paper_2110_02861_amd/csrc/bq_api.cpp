@@ -16,7 +16,11 @@ namespace {
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
 bool valid_blocksize(int32_t b) { return b >= 256 && b <= 4096 && (b & (b - 1)) == 0; }
-bool valid_opt(bq_optimizer o) { return o == BQ_ADAM || o == BQ_ADAMW || o == BQ_MOMENTUM; }
+bool valid_opt(bq_optimizer o)
+{
+    return o == BQ_ADAM || o == BQ_ADAMW || o == BQ_MOMENTUM || o == BQ_ADAGRAD;
+}
+bool two_states(bq_optimizer o) { return o == BQ_ADAM || o == BQ_ADAMW; }
 bool valid_dtype(bq_dtype d) { return d == BQ_F32 || d == BQ_F16; }
 
 // beta^t in double by right-to-left binary exponentiation.
@@ -31,8 +35,10 @@ double beta_pow(double beta, int64_t t)
 
 // Bias-corrected Adam (the paper's Eq. 2 omits the correction constants),
 // decoupled AdamW decay, and the L2 weight-decay term; each scalar is formed in
-// double from the fp32 inputs and rounded once to fp32.
-bq::StepScalars make_scalars(const bq_hparams &hp)
+// double from the fp32 inputs and rounded once to fp32.  AdaGrad has neither
+// bias correction nor momentum: its update w - lr g / (sqrt(r) + eps) uses
+// step_size = lr and inv_sqrt_bc2 = 1.
+bq::StepScalars make_scalars(const bq_hparams &hp, bq_optimizer opt)
 {
     const double lr = hp.lr, b1 = hp.beta1, b2 = hp.beta2, wd = hp.weight_decay;
     bq::StepScalars s;
@@ -43,8 +49,13 @@ bq::StepScalars make_scalars(const bq_hparams &hp)
     s.eps = hp.eps;
     s.lr = hp.lr;
     s.wd = hp.weight_decay;
-    s.step_size = static_cast<float>(lr / (1.0 - beta_pow(b1, hp.step)));
-    s.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - beta_pow(b2, hp.step)));
+    if (opt == BQ_ADAGRAD) {
+        s.step_size = hp.lr;
+        s.inv_sqrt_bc2 = 1.0f;
+    } else {
+        s.step_size = static_cast<float>(lr / (1.0 - beta_pow(b1, hp.step)));
+        s.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - beta_pow(b2, hp.step)));
+    }
     s.decay = static_cast<float>(1.0 - lr * wd);
     const double ss = static_cast<double>(s.step_size), fmax = 3.4028234663852886e38;
     if (ss == 0.0) {
@@ -212,7 +223,7 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
         return BQ_OK;
     if (!tensors || !hp || !qmap1)
         return BQ_ERR_NULL;
-    const bool two = (opt != BQ_MOMENTUM);
+    const bool two = two_states(opt);
     if (two && !qmap2)
         return BQ_ERR_NULL;
     if (hp->step < 1)
@@ -227,7 +238,7 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
     std::memset(&args, 0, sizeof(args));
     args.q1 = qmap1;
     args.q2 = two ? qmap2 : qmap1;
-    args.sc = make_scalars(*hp);
+    args.sc = make_scalars(*hp, opt);
     args.use_wd = (hp->weight_decay != 0.0f && opt != BQ_ADAMW) ? 1 : 0;
 
     // Pack non-empty tensors into launches of at most kMaxDescPerLaunch
@@ -275,7 +286,7 @@ bq_status bq_optimizer32bit_step(bq_optimizer opt, bq_dtype grad_dtype,
         return BQ_ERR_NULL;
     if (hp->step < 1)
         return BQ_ERR_ARG;
-    const bool two = (opt != BQ_MOMENTUM);
+    const bool two = two_states(opt);
     constexpr int64_t tile = 1024;
     for (int32_t i = 0; i < ntensors; ++i) {
         const bq_tensor32 &t = tensors[i];
@@ -292,7 +303,7 @@ bq_status bq_optimizer32bit_step(bq_optimizer opt, bq_dtype grad_dtype,
 
     bq::State32Args args;
     std::memset(&args, 0, sizeof(args));
-    args.sc = make_scalars(*hp);
+    args.sc = make_scalars(*hp, opt);
     args.use_wd = (hp->weight_decay != 0.0f && opt != BQ_ADAMW) ? 1 : 0;
     int32_t i = 0;
     while (i < ntensors) {
@@ -372,7 +383,7 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
         return BQ_ERR_SIZE;
     if (ntensors > 0 && !tensors)
         return BQ_ERR_NULL;
-    const bool two = (opt != BQ_MOMENTUM);
+    const bool two = two_states(opt);
     const bq_status st = check_tensors(tensors, ntensors, blocksize, two);
     if (st != BQ_OK)
         return st;
@@ -437,7 +448,7 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
 {
     if (!plan || !hp || !qmap1)
         return BQ_ERR_NULL;
-    const bool two = (plan->opt != BQ_MOMENTUM);
+    const bool two = two_states(plan->opt);
     if (two && !qmap2)
         return BQ_ERR_NULL;
     if (hp->step < 1)
@@ -456,7 +467,7 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
     std::memset(&a, 0, sizeof(a));
     a.tables = plan->tables;
     a.tiles = plan->tiles;
-    a.sc = make_scalars(*hp);
+    a.sc = make_scalars(*hp, plan->opt);
     a.use_wd = (hp->weight_decay != 0.0f && plan->opt != BQ_ADAMW) ? 1 : 0;
     a.total_tiles = (int32_t)plan->total_tiles;
     hipError_t e = bq::launch_prepare(qmap1, two ? qmap2 : nullptr, plan->tables, stream);

@@ -124,7 +124,9 @@ hipError_t launch_quantize_prepared(const uint8_t *tables, const float *x, int64
                                     int blocksize, uint8_t *codes, float *absmax,
                                     hipStream_t stream);
 
-enum { kAdam = 0, kAdamW = 1, kMomentum = 2 };
+enum { kAdam = 0, kAdamW = 1, kMomentum = 2, kAdaGrad = 3 };
+// optimizers with a second state (Adam, AdamW)
+constexpr bool has_two_states(int opt) { return opt == kAdam || opt == kAdamW; }
 enum { kF32 = 0, kF16 = 1 };
 
 hipError_t launch_step(int opt, int grad_dtype, int blocksize, const StepArgs &args,

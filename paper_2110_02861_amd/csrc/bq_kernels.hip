@@ -126,7 +126,7 @@ template <int OPT, int GRAD, int B>
 struct StepTile {
     using S = Shape<B>;
     static constexpr int EPT = S::EPT;
-    static constexpr bool kTwo = (OPT != kMomentum);
+    static constexpr bool kTwo = has_two_states(OPT);
 
     // One tile of one tensor: e0 is this thread's first element, valid the
     // number of its elements inside the tensor (EPT on full tiles).
@@ -186,6 +186,10 @@ struct StepTile {
             if constexpr (OPT == kMomentum) {
                 mi = sc.b1 * mi + gi;
                 wi = wi - sc.lr * mi;
+            } else if constexpr (OPT == kAdaGrad) {
+                mi = mi + gi * gi;
+                const float denom = __builtin_amdgcn_sqrtf(mi) * sc.inv_sqrt_bc2 + sc.eps;
+                wi = wi - sc.step_size * (gi * __builtin_amdgcn_rcpf(denom));
             } else {
                 float vi = T2.q[c2[i]] * n2;
                 if constexpr (OPT == kAdamW)
@@ -419,6 +423,7 @@ hipError_t launch_step(int opt, int grad_dtype, int blocksize, const StepArgs &a
     case kAdam: return launch_step_g<kAdam>(grad_dtype, blocksize, a, stream);
     case kAdamW: return launch_step_g<kAdamW>(grad_dtype, blocksize, a, stream);
     case kMomentum: return launch_step_g<kMomentum>(grad_dtype, blocksize, a, stream);
+    case kAdaGrad: return launch_step_g<kAdaGrad>(grad_dtype, blocksize, a, stream);
     default: return hipErrorInvalidValue;
     }
 }

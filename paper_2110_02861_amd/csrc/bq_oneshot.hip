@@ -157,7 +157,7 @@ struct StepOS {
     static constexpr int N = 4 * C;                     // elements per thread
     static constexpr int TILE = step_tile(B);
     static_assert(TILE == kOS * N, "tile size");
-    static constexpr bool kTwo = (OPT != kMomentum);
+    static constexpr bool kTwo = has_two_states(OPT);
     static constexpr int kBPT = TILE / B;               // blocks per tile
     static constexpr int kSPB = B / 256;                // segments per block
     static constexpr int kGran1 = kPreparedSignedBytes / 16;      // map 1 granules
@@ -304,6 +304,11 @@ struct StepOS {
             if constexpr (OPT == kMomentum) {
                 mi = sc.b1 * mi + gi;
                 wi = wi - sc.lr * mi;
+            } else if constexpr (OPT == kAdaGrad) {
+                mi = mi + gi * gi;
+                const float denom =
+                    __builtin_fmaf(__builtin_amdgcn_sqrtf(mi), sc.sdiv_c, sc.sdiv_eps);
+                wi = __builtin_fmaf(-gi, __builtin_amdgcn_rcpf(denom), wi);
             } else {
                 float vi = T2.q[c2[i]] * n2[c];
                 if constexpr (OPT == kAdamW)
@@ -645,6 +650,7 @@ hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const Pla
     case kAdam: return launch_os_g<kAdam>(grad_dtype, blocksize, a, stream);
     case kAdamW: return launch_os_g<kAdamW>(grad_dtype, blocksize, a, stream);
     case kMomentum: return launch_os_g<kMomentum>(grad_dtype, blocksize, a, stream);
+    case kAdaGrad: return launch_os_g<kAdaGrad>(grad_dtype, blocksize, a, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -1,6 +1,6 @@
 // Optimizer step with 32-bit states, for tensors whose states stay in fp32
 // (Section 3.3: the embedding layer keeps 32-bit optimizer states).  The same
-// update as the 8-bit step (Eq. 1, Eq. 2, AdamW) without quantization: the
+// update as the 8-bit step (Eq. 1, Eq. 2, AdamW, AdaGrad) without quantization: the
 // states m, r are fp32 arrays updated in place.  One 256-thread workgroup per
 // tile of 1024 elements, 4 contiguous elements per thread; the workgroup finds
 // its tensor by a binary search over the launch's descriptors.
@@ -32,7 +32,7 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
     if (e0 >= D.numel)
         return;
     const int nv = D.numel - e0 >= 4 ? 4 : (int)(D.numel - e0);
-    constexpr bool kTwo = (OPT != kMomentum);
+    constexpr bool kTwo = has_two_states(OPT);
     const StepScalars &sc = a.sc;
 
     float w[4], g[4], m[4], v[4];
@@ -76,6 +76,11 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
         if constexpr (OPT == kMomentum) {
             m[r] = sc.b1 * m[r] + gi;
             w[r] = w[r] - sc.lr * m[r];
+        } else if constexpr (OPT == kAdaGrad) {
+            m[r] = m[r] + gi * gi;
+            const float denom =
+                __builtin_fmaf(__builtin_amdgcn_sqrtf(m[r]), sc.sdiv_c, sc.sdiv_eps);
+            w[r] = __builtin_fmaf(-gi, __builtin_amdgcn_rcpf(denom), w[r]);
         } else {
             if constexpr (OPT == kAdamW)
                 w[r] = w[r] * sc.decay;
@@ -125,6 +130,7 @@ hipError_t launch_step32(int opt, int grad_dtype, const State32Args &a, hipStrea
     case kAdam: return launch32_g<kAdam>(grad_dtype, a, stream);
     case kAdamW: return launch32_g<kAdamW>(grad_dtype, a, stream);
     case kMomentum: return launch32_g<kMomentum>(grad_dtype, a, stream);
+    case kAdaGrad: return launch32_g<kAdaGrad>(grad_dtype, a, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -2,10 +2,11 @@
 
 The paper's 8-bit optimizers replace their 32-bit counterparts without
 hyperparameter changes (Section 1, Section 4): Adam (Eq. 2 with bias
-correction), AdamW, and SGD with momentum (Eq. 1).  Each state is stored as one
+correction), AdamW, SGD with momentum (Eq. 1), and AdaGrad (App. H).  Each state is stored as one
 uint8 code per element plus one fp32 absmax per block of ``blocksize`` elements
 (Section 3.1); the signed dynamic map holds the first state and the unsigned
-dynamic map the second (Section 3.2).  Tensors can keep 32-bit states instead:
+dynamic map the second (Section 3.2); AdaGrad's single, non-negative state
+(the running sum of squared gradients) uses the unsigned map.  Tensors can keep 32-bit states instead:
 Section 3.3 keeps the embedding layer's states in 32 bit, and tensors below
 ``min_8bit_size`` elements may be exempted as well.
 
@@ -78,14 +79,25 @@ class Optimizer8bit(torch.optim.Optimizer):
 
     @property
     def _two_states(self) -> bool:
-        return self.OPT != bq.BQ_MOMENTUM
+        return self.OPT in (bq.BQ_ADAM, bq.BQ_ADAMW)
+
+    @property
+    def _state1_unsigned(self) -> bool:
+        return self.OPT == bq.BQ_ADAGRAD
+
+    def _maps(self, device):
+        """(state-1 map, state-2 map or None, state-1 zero code, state-2 zero code)."""
+        qs, qu, zs, zu = dynamic_codebooks(device)
+        if self._state1_unsigned:
+            return qu, None, zu, zu
+        return qs, (qu if self._two_states else None), zs, zu
 
     # -- state ------------------------------------------------------------------
 
     def _init_state(self, p: torch.Tensor, state: dict) -> None:
         state["step"] = 0
         if self._is_8bit(p):
-            _, _, z1, z2 = dynamic_codebooks(p.device)
+            _, _, z1, z2 = self._maps(p.device)
             nb = (p.numel() + self.blocksize - 1) // self.blocksize
             state["state1"] = torch.full((p.numel(),), z1, dtype=torch.uint8, device=p.device)
             state["absmax1"] = torch.zeros(nb, dtype=torch.float32, device=p.device)
@@ -146,12 +158,11 @@ class Optimizer8bit(torch.optim.Optimizer):
         return loss
 
     def _step8(self, gi: int, gdt: int, device, ps, hp: dict) -> None:
-        q1, q2, _, _ = dynamic_codebooks(device)
+        q1, q2, _, _ = self._maps(device)
         rows = []
         for p in ps:
             s = self.state[p]
             rows.append((p, p.grad, s["state1"], s.get("state2"), s["absmax1"], s.get("absmax2")))
-        q2 = q2 if self._two_states else None
         if not self.use_plans:
             bq.bq_optimizer8bit_step(self.OPT, self.blocksize, gdt, rows, hp, q1, q2)
             return
@@ -229,6 +240,22 @@ class SGD8bit(Optimizer8bit):
 
     def _hparams(self, group, step):
         return dict(lr=group["lr"], beta1=group["momentum"], beta2=0.0, eps=0.0,
+                    wd=group["weight_decay"], step=step)
+
+
+class Adagrad8bit(Optimizer8bit):
+    """AdaGrad with an 8-bit sum of squared gradients (App. H): r += g^2,
+    w -= lr g / (sqrt(r) + eps), weight_decay as an L2 term; torch.optim.Adagrad
+    with lr_decay 0 and initial_accumulator_value 0."""
+
+    OPT = bq.BQ_ADAGRAD
+
+    def __init__(self, params, lr=1e-2, eps=1e-10, weight_decay=0.0, **kw):
+        _check_hparams(lr, (0.0, 0.0), eps, weight_decay)
+        super().__init__(params, dict(lr=lr, eps=eps, weight_decay=weight_decay), **kw)
+
+    def _hparams(self, group, step):
+        return dict(lr=group["lr"], beta1=0.0, beta2=0.0, eps=group["eps"],
                     wd=group["weight_decay"], step=step)
 
 

@@ -12,7 +12,8 @@ from paper_2110_02861_amd import bq
 
 needs_gpu = pytest.mark.skipif(not torch.cuda.is_available(), reason="no GPU visible")
 
-OPT_ID = {"adam": oracle.ADAM, "adamw": oracle.ADAMW, "momentum": oracle.MOMENTUM}
+OPT_ID = {"adam": oracle.ADAM, "adamw": oracle.ADAMW, "momentum": oracle.MOMENTUM,
+          "adagrad": oracle.ADAGRAD}
 
 
 def say(*a):

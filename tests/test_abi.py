@@ -108,7 +108,7 @@ def test_step_argument_checks(L):
     hp0 = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 0)
     good = _tensors(_good_row())
     H = ctypes.byref(hp)
-    assert s(3, 2048, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_ENUM
+    assert s(4, 2048, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_ENUM
     assert s(-1, 2048, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_ENUM
     assert s(0, 2048, 2, good, 1, H, A16, A16, None) == bq.BQ_ERR_DTYPE
     assert s(0, 1536, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_BLOCKSIZE
@@ -213,7 +213,7 @@ def test_step32_argument_checks(L):
     H = ctypes.byref(hp)
     row = dict(param=A16, grad=A16, state1=A16, state2=A16, numel=100)
     good = _tensors32(row)
-    assert s(3, 0, good, 1, H, None) == bq.BQ_ERR_ENUM
+    assert s(4, 0, good, 1, H, None) == bq.BQ_ERR_ENUM
     assert s(0, 5, good, 1, H, None) == bq.BQ_ERR_DTYPE
     assert s(0, 0, good, -1, H, None) == bq.BQ_ERR_SIZE
     assert s(0, 0, None, 1, H, None) == bq.BQ_ERR_NULL

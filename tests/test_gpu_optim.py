@@ -31,10 +31,13 @@ CASES = {
     "adamw": (optim.AdamW8bit, dict(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.01),
               oracle.ADAMW),
     "sgd": (optim.SGD8bit, dict(lr=0.1, momentum=0.9, weight_decay=1e-4), oracle.MOMENTUM),
+    "adagrad": (optim.Adagrad8bit, dict(lr=1e-2, eps=1e-10, weight_decay=0.0), oracle.ADAGRAD),
 }
 
 
 def oracle_hp(kw):
+    if "betas" not in kw and "momentum" not in kw:  # AdaGrad
+        return dict(lr=kw["lr"], beta1=0.0, beta2=0.0, eps=kw["eps"], wd=kw["weight_decay"])
     if "momentum" in kw:
         return dict(lr=kw["lr"], beta1=kw["momentum"], beta2=0.0, eps=0.0, wd=kw["weight_decay"])
     return dict(lr=kw["lr"], beta1=kw["betas"][0], beta2=kw["betas"][1], eps=kw["eps"],
@@ -79,6 +82,8 @@ def snapshot(opt, p):
 def oracle_step8(kind, hp, w, g, snap, n, two, t):
     q1 = bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)
     q2 = bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)
+    if kind == oracle.ADAGRAD:  # one non-negative state: the unsigned map
+        q1 = q2
     nb = (n + B - 1) // B
     if snap is None:
         c1, a1 = np.full(n, 127, np.uint8), np.zeros(nb, np.float32)
@@ -100,7 +105,7 @@ def oracle_step8(kind, hp, w, g, snap, n, two, t):
 def test_optimizer_matches_oracle(case, gdt, use_plans):
     cls, kw, kind = CASES[case]
     hp = oracle_hp(kw)
-    two = kind != oracle.MOMENTUM
+    two = kind in (oracle.ADAM, oracle.ADAMW)
     params = init_params(7)
     opt = cls(params, blocksize=B, use_plans=use_plans, **kw)
     for t in range(1, 4):
@@ -128,13 +133,13 @@ def test_optimizer_matches_oracle(case, gdt, use_plans):
             assert ok, f"{case} tensor {i} step {t}: params off by {worst}"
 
 
-@pytest.mark.parametrize("case", ["adam", "adamw", "sgd"])
+@pytest.mark.parametrize("case", ["adam", "adamw", "sgd", "adagrad"])
 def test_32bit_override_and_min_size(case):
     """override_32bit and min_8bit_size keep fp32 states, updated like the
     oracle's step with fp32 states; the other tensors stay 8-bit."""
     cls, kw, kind = CASES[case]
     hp = oracle_hp(kw)
-    two = kind != oracle.MOMENTUM
+    two = kind in (oracle.ADAM, oracle.ADAMW)
     params = init_params(11)
     opt = cls(params, blocksize=B, min_8bit_size=400, **kw)
     opt.override_32bit(params[1])

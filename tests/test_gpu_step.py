@@ -23,16 +23,19 @@ HPS = {
     "adam": dict(lr=1e-3, beta1=0.9, beta2=0.995, eps=1e-8, wd=0.0),
     "adamw": dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.01),
     "momentum": dict(lr=0.1, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4),
+    "adagrad": dict(lr=1e-2, beta1=0.0, beta2=0.0, eps=1e-10, wd=0.0),
 }
 
 
 def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=True, path="plan",
               maps=None):
     qs, qu, qs_d, qu_d = codebooks_on_device()
+    if opt == "adagrad":  # one non-negative state: the unsigned map
+        qs, qs_d = qu, qu_d
     if maps is not None:  # (state-1 map, state-2 map), host fp32
         qs, qu = maps
         qs_d, qu_d = torch.from_numpy(qs).cuda(), torch.from_numpy(qu).cuda()
-    two = opt != "momentum"
+    two = opt in ("adam", "adamw")
     hp = dict(HPS[opt] if hp is None else hp)
     tdt = torch.float16 if grad_dtype == bq.BQ_F16 else torch.float32
     ndt = np.float16 if grad_dtype == bq.BQ_F16 else np.float32
@@ -84,7 +87,7 @@ PATHS = ["call", "plan"]
 
 
 @pytest.mark.parametrize("path", PATHS)
-@pytest.mark.parametrize("opt", ["adam", "adamw", "momentum"])
+@pytest.mark.parametrize("opt", ["adam", "adamw", "momentum", "adagrad"])
 @pytest.mark.parametrize("grad_dtype", [bq.BQ_F16, bq.BQ_F32])
 @pytest.mark.parametrize("B", [256, 512, 1024, 2048, 4096])
 def test_ragged_list(opt, grad_dtype, B, path):

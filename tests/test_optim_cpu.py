@@ -32,6 +32,10 @@ def test_defaults_follow_torch():
     s = optim.SGD8bit(p, lr=0.1)
     assert s.defaults == dict(lr=0.1, momentum=0.9, weight_decay=0.0)
     assert a.blocksize == 2048 and a.min_8bit_size == 0 and a.use_plans
+    g = optim.Adagrad8bit(p)
+    assert g.defaults == dict(lr=1e-2, eps=1e-10, weight_decay=0.0)
+    assert g._hparams(g.param_groups[0], 2) == dict(lr=1e-2, beta1=0.0, beta2=0.0, eps=1e-10,
+                                                    wd=0.0, step=2)
 
 
 def test_cpu_tensors_fail_loudly():

@@ -227,3 +227,66 @@ def test_state_bytes_match_paper():
         want = facts["state_gb_per_1b_params_8bit"]["value"][opt]
         assert abs(eight / 1e9 - want) / want < 0.005
         assert nstates * 4 * n / 1e9 == facts["state_gb_per_1b_params_32bit"]["value"][opt]
+
+
+@pytest.mark.parametrize("wd", [0.0, 1e-3])
+def test_step32_adagrad_equals_torch_optim(wd):
+    """AdaGrad (App. H) with fp32 states equals torch.optim.Adagrad (no lr
+    decay, zero initial accumulator)."""
+    rng = np.random.default_rng(20)
+    n, lr, eps = 4000, 1e-2, 1e-10
+    w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    m = np.zeros(n, np.float32)
+    p = torch.nn.Parameter(torch.from_numpy(w.copy()))
+    o = torch.optim.Adagrad([p], lr=lr, eps=eps, weight_decay=wd, foreach=False)
+    for t in range(1, 8):
+        g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+        oracle.step32(oracle.ADAGRAD, w, g, m, None, lr, 0.0, 0.0, eps, wd, t)
+        p.grad = torch.from_numpy(g)
+        o.step()
+        assert close(w, p.detach().numpy(), lr), t
+        # torch may fuse g + wd*w (one rounding fewer); after squaring and
+        # summing, states agree to a few roundings
+        np.testing.assert_allclose(m, o.state[p]["sum"].numpy(), rtol=8e-6)
+
+
+def test_step8_first_step_closed_form_adagrad():
+    """t = 1 from zero state: r = g^2, w1 = w0 - lr g / (|g| + eps); the stored
+    state is the block-wise quantization of g^2 with the unsigned map."""
+    qu = oracle.dynamic_codebook(1)
+    rng = np.random.default_rng(21)
+    n, B, lr, eps = 5000, 1024, 1e-2, 1e-10
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    w = w0.copy()
+    c1 = np.zeros(n, np.uint8)
+    a1 = np.zeros((n + B - 1) // B, np.float32)
+    oracle.step8(oracle.ADAGRAD, B, w, g, c1, a1, qu, None, None, None, lr, 0.0, 0.0, eps,
+                 0.0, 1)
+    g64 = g.astype(np.float64)
+    assert close(w, w0 - lr * g64 / (np.abs(g64) + eps), lr)
+    ce, ae = exact_quantize_blockwise(qu, (g * g).astype(np.float32), B)
+    np.testing.assert_array_equal(c1, ce)
+    np.testing.assert_array_equal(a1, ae)
+
+
+def test_step8_adagrad_accumulates():
+    """Over steps the 8-bit AdaGrad state tracks the running sum of squares to
+    the quantization error bound of the unsigned map (one code gap, relative to
+    the block absmax, per requantization)."""
+    qu = oracle.dynamic_codebook(1)
+    rng = np.random.default_rng(22)
+    n, B = 3 * 2048 + 5, 2048
+    w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    c1 = np.zeros(n, np.uint8)
+    a1 = np.zeros((n + B - 1) // B, np.float32)
+    s = np.zeros(n, np.float64)
+    for t in range(1, 6):
+        g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+        oracle.step8(oracle.ADAGRAD, B, w, g, c1, a1, qu, None, None, None, 1e-2, 0.0, 0.0,
+                     1e-10, 0.0, t)
+        s += g.astype(np.float64) ** 2
+    r = oracle.dequantize_blockwise(qu, c1, a1, B).astype(np.float64)
+    blk = np.repeat(a1.astype(np.float64), B)[:n]
+    # each of 5 requantizations adds at most half the largest gap times the absmax
+    assert np.all(np.abs(r - s) <= 5 * 0.5 * (0.9 / 128) * blk + 1e-12)
