@@ -106,6 +106,35 @@ bq_status bq_make_codebook(bq_codebook_kind kind, float out[256]);
  */
 bq_status bq_make_quantile_codebook(const float *sample, int64_t n, float out[256]);
 
+/* Values per chunk of the GPU quantile estimator. */
+#define BQ_QUANTILE_CHUNK 4096
+
+/* Bytes of device workspace bq_estimate_quantile_codebook needs for n values
+ * (0 for n < 1): 257 fp32 per chunk, then 257 fp64 per group of 64 chunks. */
+int64_t bq_quantile_workspace_bytes(int64_t n);
+
+/*
+ * Quantile map estimated on the GPU (App. F.2 with App. G's chunked
+ * estimator): x is cut into chunks of BQ_QUANTILE_CHUNK values (the last one
+ * shorter); each chunk is sorted in LDS and gives its sample quantiles
+ * Q_c(i / 257) = sorted_c[floor(i L_c / 257)], i = 0..256; the estimate
+ * Q(i / 257) is their average weighted by chunk length L_c, summed in double
+ * in a fixed order (sequentially within groups of 64 consecutive chunks, then
+ * over the groups), so the result is deterministic, unlike atomic averaging;
+ * then as bq_make_quantile_codebook: q_i = (Q(i / 257) + Q((i + 1) / 257)) / 2,
+ * divided by max |q_i|, rounded to fp32, equal entries moved up by one ulp (an
+ * all-zero x gives 0 and then successive subnormals).  Inputs must be finite.
+ * Stream-ordered; three launches.
+ *   x          device, n fp32 (read), 4-byte aligned
+ *   workspace  device, bq_quantile_workspace_bytes(n) bytes, 8-byte aligned,
+ *              caller-owned
+ *   out        device, 256 fp32 (written)
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE (n < 1, or more than 8,388,607 chunks),
+ * BQ_ERR_ALIGN, BQ_ERR_HIP.
+ */
+bq_status bq_estimate_quantile_codebook(const float *x, int64_t n, void *workspace, float *out,
+                                        hipStream_t stream);
+
 /*
  * Block-wise quantization (Section 3.1, Eq. 4).  For each block b:
  *   N_b = max_i |x_i|                              -> absmax[b]

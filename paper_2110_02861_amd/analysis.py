@@ -23,6 +23,10 @@ from a synthetic run, so the numbers are this workload's, not the paper's:
 
     python -m paper_2110_02861_amd.analysis [--rows 8192 --cols 1024 --steps 20
                                              --row-spread 1024 --outlier 10]
+
+``--time-quantiles N`` instead times the GPU quantile estimator
+(``bq_estimate_quantile_codebook``, App. G) on N seeded normal values and
+prints ns per element.
 """
 from __future__ import annotations
 
@@ -120,6 +124,32 @@ def run(rows=8192, cols=1024, steps=20, blocksize=2048, seed=0, row_spread=1024,
     return out
 
 
+def time_quantile_estimator(n: int, reps: int = 20, seed: int = 0) -> dict:
+    """Average time of bq_estimate_quantile_codebook on n normal values (HIP
+    events on the launch stream), with its workspace preallocated."""
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    x = torch.randn(n, device=dev, generator=gen)
+    ws = torch.empty(bq.lib().bq_quantile_workspace_bytes(n) // 8, dtype=torch.float64,
+                     device=dev)
+    out = torch.empty(256, device=dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        bq.bq_estimate_quantile_codebook(x, out, ws)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        bq.bq_estimate_quantile_codebook(x, out, ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"n": n, "ms": ms, "ns_per_element": ms * 1e6 / n,
+            "gb_per_s": n * 4 / (ms / 1e3) / 1e9}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--rows", type=int, default=8192)
@@ -129,7 +159,11 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--row-spread", type=int, default=1024)
     ap.add_argument("--outlier", type=float, default=10.0)
+    ap.add_argument("--time-quantiles", type=int, default=0, metavar="N")
     a = ap.parse_args()
+    if a.time_quantiles:
+        print(json.dumps(time_quantile_estimator(a.time_quantiles)))
+        return
     res = run(a.rows, a.cols, a.steps, a.blocksize, a.seed, a.row_spread, a.outlier)
     print(f"{'map':16s} {'rel. Adam error':>16s} {'(median)':>10s} {'abs. quant. error':>18s} "
           f"{'r -> 0':>8s}")

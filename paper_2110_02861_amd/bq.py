@@ -29,12 +29,14 @@ OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM,
               "adagrad": BQ_ADAGRAD}
 
 EXPORTS = ("bq_make_dynamic_codebook", "bq_make_codebook", "bq_make_quantile_codebook",
+           "bq_estimate_quantile_codebook", "bq_quantile_workspace_bytes",
            "bq_quantize_blockwise", "bq_dequantize_blockwise",
            "bq_optimizer8bit_step", "bq_optimizer32bit_step", "bq_prepare_codebook",
            "bq_quantize_blockwise_prepared",
            "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_destroy",
            "bq_status_string")
 BQ_PREPARED_CODEBOOK_BYTES = 8720
+BQ_QUANTILE_CHUNK = 4096
 
 
 class BQError(RuntimeError):
@@ -80,6 +82,10 @@ def lib() -> ctypes.CDLL:
         L.bq_make_codebook.restype = I
         L.bq_make_quantile_codebook.argtypes = [P, I64, P]
         L.bq_make_quantile_codebook.restype = I
+        L.bq_estimate_quantile_codebook.argtypes = [P, I64, P, P, P]
+        L.bq_estimate_quantile_codebook.restype = I
+        L.bq_quantile_workspace_bytes.argtypes = [I64]
+        L.bq_quantile_workspace_bytes.restype = I64
         L.bq_quantize_blockwise.argtypes = [P, P, I64, I32, P, P, P]
         L.bq_quantize_blockwise.restype = I
         L.bq_dequantize_blockwise.argtypes = [P, P, P, I64, I32, P, P]
@@ -140,6 +146,24 @@ def bq_make_codebook(kind: int) -> np.ndarray:
     """Host call: any fixed codebook (BQ_SIGNED ... BQ_LINEAR_UNSIGNED)."""
     out = np.empty(256, np.float32)
     _check(lib().bq_make_codebook(int(kind), out.ctypes.data), "bq_make_codebook")
+    return out
+
+
+def bq_estimate_quantile_codebook(x, out=None, workspace=None, stream=None):
+    """GPU quantile map of a device fp32 tensor (App. F.2, App. G); returns the
+    device map (256 fp32).  The workspace (bq_quantile_workspace_bytes) is
+    allocated here by torch unless given."""
+    import torch
+    n = x.numel()
+    if workspace is None:
+        nbytes = max(8, int(lib().bq_quantile_workspace_bytes(n)))
+        workspace = torch.empty(nbytes // 8, dtype=torch.float64, device=x.device)
+    if out is None:
+        out = torch.empty(256, dtype=torch.float32, device=x.device)
+    _check(lib().bq_estimate_quantile_codebook(_dev_ptr(x, "x") if n else None, n,
+                                               _dev_ptr(workspace, "workspace"),
+                                               _dev_ptr(out, "out"), _stream(stream)),
+           "bq_estimate_quantile_codebook")
     return out
 
 

@@ -13,7 +13,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libbq.so")
-SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_kernels.hip", "bq_oneshot.hip", "bq_state32.hip"]
+SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_kernels.hip", "bq_oneshot.hip", "bq_state32.hip",
+           "bq_quantiles.hip"]
 # the benchmark's streaming-ceiling kernel, a library of its own
 STREAM_LIB = os.path.join(PKG, "libbq_stream.so")
 STREAM_SOURCES = ["bq_stream.hip"]

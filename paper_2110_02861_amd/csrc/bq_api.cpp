@@ -172,6 +172,25 @@ bq_status bq_make_quantile_codebook(const float *sample, int64_t n, float out[25
     return bq::build_quantile_codebook(sample, n, out) == 0 ? BQ_OK : BQ_ERR_ARG;
 }
 
+int64_t bq_quantile_workspace_bytes(int64_t n)
+{
+    return n < 1 ? 0 : bq::quantile_workspace_bytes(n);
+}
+
+bq_status bq_estimate_quantile_codebook(const float *x, int64_t n, void *workspace, float *out,
+                                        hipStream_t stream)
+{
+    if (n < 1)
+        return BQ_ERR_SIZE;
+    if (!x || !workspace || !out)
+        return BQ_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(workspace, 8) || !aligned(out, 4))
+        return BQ_ERR_ALIGN;
+    if ((n + bq::kQChunk - 1) / bq::kQChunk > kMaxOneShotTiles)
+        return BQ_ERR_SIZE;
+    return from_hip(bq::launch_quantile_codebook(x, n, workspace, out, stream));
+}
+
 bq_status bq_quantize_blockwise(const float *qmap, const float *x, int64_t n, int32_t blocksize,
                                 uint8_t *codes, float *absmax, hipStream_t stream)
 {

@@ -114,6 +114,26 @@ struct State32Args {
 };
 static_assert(sizeof(State32Args) <= 4096, "kernel argument block must stay below 4 KiB");
 
+// Chunk length of the quantile estimator (values sorted per workgroup in LDS)
+// and chunks per first-level summation group.
+constexpr int kQChunk = 4096;
+constexpr int kQGroup = 64;
+// Workspace: 257 fp32 chunk quantiles per chunk (padded to 8 bytes), then 257
+// fp64 sums per group.
+inline int64_t quantile_partial_bytes(int64_t n)
+{
+    const int64_t nchunks = (n + kQChunk - 1) / kQChunk;
+    return (nchunks * 257 * 4 + 7) / 8 * 8;
+}
+inline int64_t quantile_workspace_bytes(int64_t n)
+{
+    const int64_t nchunks = (n + kQChunk - 1) / kQChunk;
+    const int64_t ngroups = (nchunks + kQGroup - 1) / kQGroup;
+    return quantile_partial_bytes(n) + ngroups * 257 * 8;
+}
+hipError_t launch_quantile_codebook(const float *x, int64_t n, void *workspace, float *out,
+                                    hipStream_t stream);
+
 hipError_t launch_step32(int opt, int grad_dtype, const State32Args &args, hipStream_t stream);
 
 hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *tables,

@@ -226,3 +226,36 @@ def test_step32_argument_checks(L):
     # Momentum needs no second state; empty tensors and empty lists are no-ops
     assert s(2, 0, _tensors32(dict(row, state2=None, numel=0)), 1, H, None) == bq.BQ_OK
     assert s(0, 0, None, 0, H, None) == bq.BQ_OK
+
+
+def test_codebook_call_checks(L):
+    out = (ctypes.c_float * 256)()
+    assert L.bq_make_codebook(0, None) == bq.BQ_ERR_NULL
+    assert L.bq_make_codebook(6, out) == bq.BQ_ERR_ENUM
+    assert L.bq_make_codebook(-1, out) == bq.BQ_ERR_ENUM
+    # the dynamic-only call keeps refusing the other kinds
+    assert L.bq_make_dynamic_codebook(2, out) == bq.BQ_ERR_ENUM
+    x = (ctypes.c_float * 4)(1.0, 2.0, 3.0, float("nan"))
+    assert L.bq_make_quantile_codebook(None, 4, out) == bq.BQ_ERR_NULL
+    assert L.bq_make_quantile_codebook(x, 4, None) == bq.BQ_ERR_NULL
+    assert L.bq_make_quantile_codebook(x, 0, out) == bq.BQ_ERR_SIZE
+    assert L.bq_make_quantile_codebook(x, 4, out) == bq.BQ_ERR_ARG      # NaN
+    z = (ctypes.c_float * 3)(0.0, 0.0, 0.0)
+    assert L.bq_make_quantile_codebook(z, 3, out) == bq.BQ_ERR_ARG      # all-zero map
+    assert L.bq_make_quantile_codebook(x, 3, out) == bq.BQ_OK
+
+
+def test_quantile_estimator_checks(L):
+    e = L.bq_estimate_quantile_codebook
+    assert e(A16, 0, A16, A16, None) == bq.BQ_ERR_SIZE
+    assert e(None, 10, A16, A16, None) == bq.BQ_ERR_NULL
+    assert e(A16, 10, None, A16, None) == bq.BQ_ERR_NULL
+    assert e(A16, 10, A16, None, None) == bq.BQ_ERR_NULL
+    assert e(A16 + 2, 10, A16, A16, None) == bq.BQ_ERR_ALIGN
+    assert e(A16, 10, A16 + 4, A16, None) == bq.BQ_ERR_ALIGN
+    assert e(A16, 1 << 62, A16, A16, None) == bq.BQ_ERR_SIZE
+    w = L.bq_quantile_workspace_bytes
+    assert w(0) == 0
+    assert w(1) == 1032 + 257 * 8          # one chunk: 257 floats padded to 8 B, one group
+    assert w(4096 * 64) == 64 * 257 * 4 + 257 * 8
+    assert w(4096 * 64 + 1) == (65 * 257 * 4 + 7) // 8 * 8 + 2 * 257 * 8

@@ -180,3 +180,44 @@ def test_nearest_code_exact_where_double_rounding_would_tie():
             want = _exact_nearest(qm, y)
             assert oracle.nearest_brute(qm, float(y)) == want, (y, want)
             assert oracle.nearest_bsearch(qm, float(y)) == want, (y, want)
+
+
+# --- chunked quantile estimate (App. G) ---
+
+def test_chunked_quantiles_single_chunk_is_eq5():
+    """With n <= chunk the estimate is the sample's own quantile map (Eq. 5)."""
+    rng = workloads.host_rng(0, "c2", 6, 0)
+    for n in (1, 7, 300, 4096):
+        x = rng.standard_normal(n).astype(np.float32)
+        if n == 1:
+            x[0] = 2.5
+        q = oracle.chunked_quantile_codebook(x)
+        np.testing.assert_array_equal(q, oracle.quantile_codebook(x))
+
+
+def test_chunked_quantiles_identical_chunks():
+    """Chunks holding the same values (in any order) average to those values'
+    quantile map, which is also the whole tensor's (each value repeated)."""
+    rng = workloads.host_rng(0, "c2", 7, 0)
+    base = rng.standard_normal(4096).astype(np.float32)
+    x = np.concatenate([rng.permutation(base) for _ in range(5)])
+    q = oracle.chunked_quantile_codebook(x)
+    np.testing.assert_array_equal(q, oracle.quantile_codebook(base))
+    np.testing.assert_array_equal(q, oracle.quantile_codebook(x))
+
+
+def test_chunked_quantiles_converge_and_scale():
+    rng = workloads.host_rng(0, "c2", 8, 0)
+    x = rng.standard_normal(1_000_003).astype(np.float32)
+    q = oracle.chunked_quantile_codebook(x)
+    exact = oracle.quantile_codebook(x)
+    assert np.all(np.diff(q) > 0)
+    # away from the extreme tails the average of chunk quantiles is close to
+    # the tensor's quantiles; the maps differ in scale, since the first entry
+    # (the sample minimum: of each 4096-chunk, or of the whole tensor) sets
+    # the normalization
+    ratio = float(exact[240]) / float(q[240])
+    np.testing.assert_allclose(q[8:-8].astype(np.float64) * ratio, exact[8:-8], atol=0.01)
+    np.testing.assert_array_equal(oracle.chunked_quantile_codebook(x * np.float32(4.0)), q)
+    z = oracle.chunked_quantile_codebook(np.zeros(5000, np.float32))
+    assert z[0] == 0.0 and np.all(np.diff(z) > 0) and z[-1] < 1e-42
