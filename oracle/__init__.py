@@ -23,7 +23,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "bq_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-ADAM, ADAMW, MOMENTUM, ADAGRAD = 0, 1, 2, 3
+ADAM, ADAMW, MOMENTUM, ADAGRAD, LAMB, LARS = 0, 1, 2, 3, 4, 5
+TWO_STATES = (0, 1, 4)
 SIGNED, UNSIGNED = 0, 1
 
 
@@ -67,10 +68,10 @@ def lib() -> ctypes.CDLL:
         L.oracle_dequantize_blockwise.restype = None
         L.oracle_half_to_float.argtypes = [P, P, I64]
         L.oracle_half_to_float.restype = None
-        L.oracle_step32.argtypes = [I, I64, P, P, I, P, P, F, F, F, F, F, I64]
+        L.oracle_step32.argtypes = [I, I64, P, P, I, P, P, F, F, F, F, F, I64, F]
         L.oracle_step32.restype = I
         L.oracle_step8.argtypes = [I, I32, I, I64, P, P, P, P, P, P, P, P,
-                                   F, F, F, F, F, I64, I]
+                                   F, F, F, F, F, I64, I, F]
         L.oracle_step8.restype = I
         L.oracle_max_threads.argtypes = []
         L.oracle_max_threads.restype = I
@@ -173,27 +174,29 @@ def _grad_kind(g):
     raise TypeError("grad must be float16 or float32")
 
 
-def step32(opt, w, g, m, v, lr, beta1, beta2, eps, wd, step):
-    """Update w, m, v (fp32 states, quantization bypassed) in place."""
+def step32(opt, w, g, m, v, lr, beta1, beta2, eps, wd, step, trust=0.0):
+    """Update w, m, v (fp32 states, quantization bypassed) in place.  trust is
+    LARS's trust coefficient (unused by the other optimizers)."""
     _check(w, np.float32, "w")
     _check(m, np.float32, "m")
-    if opt in (ADAM, ADAMW):
+    if opt in TWO_STATES:
         _check(v, np.float32, "v")
     g = np.ascontiguousarray(g)
     rc = lib().oracle_step32(int(opt), w.size, w.ctypes.data, g.ctypes.data, _grad_kind(g),
-                             m.ctypes.data, _ptr(v), lr, beta1, beta2, eps, wd, int(step))
+                             m.ctypes.data, _ptr(v), lr, beta1, beta2, eps, wd, int(step),
+                             float(trust))
     if rc != 0:
         raise ValueError("oracle_step32: bad argument")
 
 
 def step8(opt, blocksize, w, g, c1, a1, q1, c2, a2, q2, lr, beta1, beta2, eps, wd,
-          step, nthreads=0):
+          step, nthreads=0, trust=0.0):
     """One 8-bit step on one tensor; w, c1, a1, c2, a2 are updated in place."""
     _check(w, np.float32, "w")
     _check(c1, np.uint8, "c1")
     _check(a1, np.float32, "a1")
     _check(q1, np.float32, "q1")
-    if opt in (ADAM, ADAMW):
+    if opt in TWO_STATES:
         _check(c2, np.uint8, "c2")
         _check(a2, np.float32, "a2")
         _check(q2, np.float32, "q2")
@@ -201,7 +204,7 @@ def step8(opt, blocksize, w, g, c1, a1, q1, c2, a2, q2, lr, beta1, beta2, eps, w
     rc = lib().oracle_step8(int(opt), int(blocksize), _grad_kind(g), w.size, w.ctypes.data,
                             g.ctypes.data, c1.ctypes.data, _ptr(c2), a1.ctypes.data,
                             _ptr(a2), q1.ctypes.data, _ptr(q2), lr, beta1, beta2, eps,
-                            wd, int(step), int(nthreads))
+                            wd, int(step), int(nthreads), float(trust))
     if rc != 0:
         raise ValueError("oracle_step8: bad argument")
 

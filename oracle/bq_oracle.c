@@ -419,7 +419,7 @@ ORACLE_API void oracle_half_to_float(const uint16_t *h, float *out, int64_t n)
 /* Optimizer update: Eq. 1 (Momentum), Eq. 2 (Adam), AdamW.                   */
 /* ------------------------------------------------------------------------- */
 
-enum { OR_ADAM = 0, OR_ADAMW = 1, OR_MOMENTUM = 2, OR_ADAGRAD = 3 };
+enum { OR_ADAM = 0, OR_ADAMW = 1, OR_MOMENTUM = 2, OR_ADAGRAD = 3, OR_LAMB = 4, OR_LARS = 5 };
 
 /* beta^t by square-and-multiply in double (t >= 0). */
 static double pow_int(double beta, int64_t t)
@@ -448,6 +448,7 @@ static double pow_int(double beta, int64_t t)
  */
 typedef struct {
     float b1, omb1, b2, omb2, eps, lr, wd, step_size, inv_sqrt_bc2, decay;
+    float bc1_inv; /* 1 / (1 - beta1^t), LAMB's first-moment correction */
 } step_scalars;
 
 static step_scalars make_scalars(float lr, float beta1, float beta2, float eps,
@@ -464,6 +465,7 @@ static step_scalars make_scalars(float lr, float beta1, float beta2, float eps,
     s.step_size = (float)((double)lr / (1.0 - pow_int((double)beta1, t)));
     s.inv_sqrt_bc2 = (float)(1.0 / sqrt(1.0 - pow_int((double)beta2, t)));
     s.decay = (float)(1.0 - (double)lr * (double)wd);
+    s.bc1_inv = (float)(1.0 / (1.0 - pow_int((double)beta1, t)));
     return s;
 }
 
@@ -518,18 +520,95 @@ static float load_grad(const void *g, int grad_is_f16, int64_t i)
 }
 
 /*
+ * LAMB and LARS (App. E times 8-bit versions of both; the paper gives no
+ * equations).  Reading: the textbook methods, with a per-tensor trust ratio
+ * from the norms of the whole tensor, computed before the update:
+ *   LAMB: m' = b1*m + (1-b1)*g;  v' = b2*v + (1-b2)*(g*g);
+ *         u = (m' * bc1_inv) / (sqrt(v') * inv_sqrt_bc2 + eps) + wd*w;
+ *         ratio = |w| / |u|;  w' = w - (lr*ratio) * u
+ *   LARS: ratio = trust * |w| / (|g| + wd*|w|)  (g before weight decay);
+ *         g' = g + wd*w;  m' = b1*m + (lr*ratio) * g';  w' = w - m'
+ * with ratio = 1 when either norm is zero.  Norms are sums of squares in
+ * double; lr*ratio is formed in double and rounded once to fp32.
+ */
+static float lamb_direction(const step_scalars *s, float w, float mn, float vn)
+{
+    float mh = mn * s->bc1_inv;
+    float denom = sqrtf(vn) * s->inv_sqrt_bc2 + s->eps;
+    return mh / denom + s->wd * w;
+}
+
+static float trust_lr(int opt, const step_scalars *s, double nw2, double nx2, float trust)
+{
+    double a = sqrt(nw2), b = sqrt(nx2), ratio = 1.0;
+    if (a > 0.0 && b > 0.0)
+        ratio = (opt == OR_LAMB) ? a / b : (double)trust * a / (b + (double)s->wd * a);
+    return (float)((double)s->lr * ratio);
+}
+
+/* One element of LAMB / LARS given the tensor's lr*ratio. */
+static void trust_update_element(int opt, const step_scalars *s, float lr_r, float *w, float g,
+                                 float *m, float *v)
+{
+    float wv = *w;
+    if (opt == OR_LAMB) {
+        float mn = s->b1 * (*m) + s->omb1 * g;
+        float vn = s->b2 * (*v) + s->omb2 * (g * g);
+        float u = lamb_direction(s, wv, mn, vn);
+        *m = mn;
+        *v = vn;
+        *w = wv - lr_r * u;
+    } else {
+        if (s->wd != 0.0f)
+            g = g + s->wd * wv;
+        float mn = s->b1 * (*m) + lr_r * g;
+        *m = mn;
+        *w = wv - mn;
+    }
+}
+
+/* Squared norms (of w, and of u for LAMB or g for LARS) of one element. */
+static void trust_norm_terms(int opt, const step_scalars *s, float w, float g, float m, float v,
+                             double *nw2, double *nx2)
+{
+    *nw2 += (double)w * (double)w;
+    if (opt == OR_LAMB) {
+        float mn = s->b1 * m + s->omb1 * g;
+        float vn = s->b2 * v + s->omb2 * (g * g);
+        float u = lamb_direction(s, w, mn, vn);
+        *nx2 += (double)u * (double)u;
+    } else {
+        *nx2 += (double)g * (double)g;
+    }
+}
+
+/*
  * 32-bit reference step with quantization bypassed: fp32 states m[n], v[n]
  * (v unused for Momentum).  This is the special case that reduces to the
  * textbook optimizers.
  */
 ORACLE_API int oracle_step32(int opt, int64_t n, float *w, const void *g, int grad_is_f16,
                              float *m, float *v, float lr, float beta1, float beta2,
-                             float eps, float wd, int64_t step)
+                             float eps, float wd, int64_t step, float trust)
 {
-    if (opt < OR_ADAM || opt > OR_ADAGRAD || step < 1)
+    if (opt < OR_ADAM || opt > OR_LARS || step < 1)
         return -1;
-    int two = (opt == OR_ADAM || opt == OR_ADAMW);
+    int two = (opt == OR_ADAM || opt == OR_ADAMW || opt == OR_LAMB);
     step_scalars s = make_scalars(lr, beta1, beta2, eps, wd, step);
+    if (opt == OR_LAMB || opt == OR_LARS) {
+        double nw2 = 0.0, nx2 = 0.0;
+        for (int64_t i = 0; i < n; ++i)
+            trust_norm_terms(opt, &s, w[i], load_grad(g, grad_is_f16, i), m[i],
+                             two ? v[i] : 0.0f, &nw2, &nx2);
+        float lr_r = trust_lr(opt, &s, nw2, nx2, trust);
+        for (int64_t i = 0; i < n; ++i) {
+            float vi = two ? v[i] : 0.0f;
+            trust_update_element(opt, &s, lr_r, &w[i], load_grad(g, grad_is_f16, i), &m[i], &vi);
+            if (two)
+                v[i] = vi;
+        }
+        return 0;
+    }
     for (int64_t i = 0; i < n; ++i) {
         float vi = two ? v[i] : 0.0f;
         update_element(opt, &s, &w[i], load_grad(g, grad_is_f16, i), &m[i], &vi);
@@ -551,13 +630,27 @@ ORACLE_API int oracle_step32(int opt, int64_t n, float *w, const void *g, int gr
 ORACLE_API int oracle_step8(int opt, int32_t B, int grad_is_f16, int64_t n, float *w,
                             const void *g, uint8_t *c1, uint8_t *c2, float *a1, float *a2,
                             const float *q1, const float *q2, float lr, float beta1,
-                            float beta2, float eps, float wd, int64_t step, int nthreads)
+                            float beta2, float eps, float wd, int64_t step, int nthreads,
+                            float trust)
 {
-    if (opt < OR_ADAM || opt > OR_ADAGRAD || step < 1 || B <= 0)
+    if (opt < OR_ADAM || opt > OR_LARS || step < 1 || B <= 0)
         return -1;
-    int two = (opt == OR_ADAM || opt == OR_ADAMW);
+    int two = (opt == OR_ADAM || opt == OR_ADAMW || opt == OR_LAMB);
     step_scalars s = make_scalars(lr, beta1, beta2, eps, wd, step);
     int64_t nb = (n + B - 1) / B;
+    int trust_opt = (opt == OR_LAMB || opt == OR_LARS);
+    float lr_r = 0.0f;
+    if (trust_opt) {
+        /* the tensor's norms, from the dequantized states, before any update */
+        double nw2 = 0.0, nx2 = 0.0;
+        for (int64_t e = 0; e < n; ++e) {
+            int64_t b = e / B;
+            float m = q1[c1[e]] * a1[b];
+            float v = two ? q2[c2[e]] * a2[b] : 0.0f;
+            trust_norm_terms(opt, &s, w[e], load_grad(g, grad_is_f16, e), m, v, &nw2, &nx2);
+        }
+        lr_r = trust_lr(opt, &s, nw2, nx2, trust);
+    }
     set_threads(nthreads);
 #pragma omp parallel
     {
@@ -570,7 +663,11 @@ ORACLE_API int oracle_step8(int opt, int32_t B, int grad_is_f16, int64_t n, floa
                 int64_t e = st + i;
                 float m = q1[c1[e]] * a1[b];
                 float v = two ? q2[c2[e]] * a2[b] : 0.0f;
-                update_element(opt, &s, &w[e], load_grad(g, grad_is_f16, e), &m, &v);
+                if (trust_opt)
+                    trust_update_element(opt, &s, lr_r, &w[e], load_grad(g, grad_is_f16, e), &m,
+                                         &v);
+                else
+                    update_element(opt, &s, &w[e], load_grad(g, grad_is_f16, e), &m, &v);
                 mt[i] = m;
                 vt[i] = v;
             }

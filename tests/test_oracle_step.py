@@ -290,3 +290,110 @@ def test_step8_adagrad_accumulates():
     blk = np.repeat(a1.astype(np.float64), B)[:n]
     # each of 5 requantizations adds at most half the largest gap times the absmax
     assert np.all(np.abs(r - s) <= 5 * 0.5 * (0.9 / 128) * blk + 1e-12)
+
+
+# --- LAMB and LARS (App. E lists 8-bit versions; textbook forms, trust ratios) ---
+
+def _lamb(w, g, m, v, t, lr=1e-3, wd=0.0):
+    oracle.step32(oracle.LAMB, w, g, m, v, lr, 0.9, 0.999, 1e-6, wd, t)
+
+
+@pytest.mark.parametrize("wd", [0.0, 0.01])
+def test_lamb_step_length_is_lr_times_param_norm(wd):
+    """The trust ratio |w| / |u| makes every step exactly lr * |w| long."""
+    rng = np.random.default_rng(30)
+    n, lr = 3000, 1e-3
+    w = rng.standard_normal(n).astype(np.float32) * np.float32(0.05)
+    m = np.zeros(n, np.float32)
+    v = np.zeros(n, np.float32)
+    for t in range(1, 5):
+        g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+        w0 = w.astype(np.float64).copy()
+        _lamb(w, g, m, v, t, lr, wd)
+        step = np.linalg.norm(w.astype(np.float64) - w0)
+        assert abs(step - lr * np.linalg.norm(w0)) <= 1e-4 * lr * np.linalg.norm(w0), t
+
+
+def test_lars_first_step_direction_and_length():
+    """t = 1, no weight decay: the momentum starts at 0, so the step is
+    lr * trust * |w| * g / |g|: along -g, of length lr * trust * |w|, and the
+    same for any scaling of g."""
+    rng = np.random.default_rng(31)
+    n, lr, trust = 4000, 0.5, 1e-3
+    w0 = rng.standard_normal(n).astype(np.float32) * np.float32(0.05)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    outs = []
+    for scale in (1.0, 8.0, 1.0 / 64):
+        w = w0.copy()
+        m = np.zeros(n, np.float32)
+        oracle.step32(oracle.LARS, w, (g * np.float32(scale)).astype(np.float32), m, None, lr,
+                      0.9, 0.0, 0.0, 0.0, 1, trust)
+        outs.append(w.astype(np.float64))
+        d = w0.astype(np.float64) - w
+        L = lr * trust * np.linalg.norm(w0.astype(np.float64))
+        assert abs(np.linalg.norm(d) - L) <= 1e-5 * L
+        cos = d @ g / (np.linalg.norm(d) * np.linalg.norm(g))
+        assert cos > 1 - 1e-6  # w is rounded to fp32 after the step
+    for o in outs[1:]:
+        np.testing.assert_allclose(o, outs[0], rtol=0, atol=1e-6 * lr * trust)
+
+
+def test_lars_weight_decay_ratio():
+    """With weight decay the local rate is trust |w| / (|g| + wd |w|) applied to
+    g + wd w (the first step, zero momentum)."""
+    rng = np.random.default_rng(32)
+    n, lr, trust, wd = 2500, 0.2, 1e-3, 5e-4
+    w0 = rng.standard_normal(n).astype(np.float32) * np.float32(0.05)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    w = w0.copy()
+    m = np.zeros(n, np.float32)
+    oracle.step32(oracle.LARS, w, g, m, None, lr, 0.9, 0.0, 0.0, wd, 1, trust)
+    w64, g64 = w0.astype(np.float64), g.astype(np.float64)
+    nw, ng = np.linalg.norm(w64), np.linalg.norm(g64)
+    expect = lr * trust * nw / (ng + wd * nw) * np.linalg.norm(g64 + wd * w64)
+    assert abs(np.linalg.norm(w64 - w) - expect) <= 1e-5 * expect
+
+
+def test_trust_ratio_one_for_zero_norms():
+    """A zero param tensor has no norm to scale by: LAMB then takes lr * u."""
+    n = 100
+    w = np.zeros(n, np.float32)
+    g = np.linspace(-1e-3, 1e-3, n, dtype=np.float32)
+    m = np.zeros(n, np.float32)
+    v = np.zeros(n, np.float32)
+    _lamb(w, g, m, v, 1, lr=1e-2)
+    g64 = g.astype(np.float64)
+    u = g64 / (np.abs(g64) + 1e-6)          # t = 1: mhat = g, vhat = g^2
+    np.testing.assert_allclose(w, -1e-2 * u, rtol=1e-6, atol=1e-12)
+
+
+@pytest.mark.parametrize("opt", [oracle.LAMB, oracle.LARS])
+def test_step8_trust_equals_dequant_step32_requant(opt):
+    """8-bit LAMB / LARS = dequantize -> 32-bit step (norms from the dequantized
+    states) -> exact requantization."""
+    qs, qu = oracle.dynamic_codebook(0), oracle.dynamic_codebook(1)
+    rng = np.random.default_rng(33)
+    n, B = 3 * 512 + 19, 512
+    two = opt == oracle.LAMB
+    lr, wd, trust = (1e-3, 0.01, 0.0) if two else (0.5, 1e-4, 1e-3)
+    w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    c1 = np.full(n, 127, np.uint8)
+    a1 = np.zeros((n + B - 1) // B, np.float32)
+    c2 = np.zeros(n, np.uint8)
+    a2 = np.zeros_like(a1)
+    for t in range(1, 5):
+        g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+        m = oracle.dequantize_blockwise(qs, c1, a1, B)
+        v = oracle.dequantize_blockwise(qu, c2, a2, B)
+        w32 = w.copy()
+        oracle.step32(opt, w32, g, m, v if two else None, lr, 0.9, 0.999, 1e-6, wd, t, trust)
+        oracle.step8(opt, B, w, g, c1, a1, qs, c2 if two else None, a2 if two else None,
+                     qu if two else None, lr, 0.9, 0.999, 1e-6, wd, t, trust=trust)
+        np.testing.assert_array_equal(w, w32)
+        ce, ae = exact_quantize_blockwise(qs, m, B)
+        np.testing.assert_array_equal(c1, ce)
+        np.testing.assert_array_equal(a1, ae)
+        if two:
+            ce, ae = exact_quantize_blockwise(qu, v, B)
+            np.testing.assert_array_equal(c2, ce)
+            np.testing.assert_array_equal(a2, ae)
