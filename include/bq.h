@@ -59,7 +59,14 @@ typedef enum bq_codebook_kind {
     BQ_LINEAR_SIGNED = 4,     /* 256 evenly spaced values in [-1, 1] */
     BQ_LINEAR_UNSIGNED = 5    /* 256 evenly spaced values in [0, 1] */
 } bq_codebook_kind;
-typedef enum bq_optimizer { BQ_ADAM = 0, BQ_ADAMW = 1, BQ_MOMENTUM = 2, BQ_ADAGRAD = 3 } bq_optimizer;
+typedef enum bq_optimizer {
+    BQ_ADAM = 0,
+    BQ_ADAMW = 1,
+    BQ_MOMENTUM = 2,
+    BQ_ADAGRAD = 3,
+    BQ_LAMB = 4,  /* step plans only */
+    BQ_LARS = 5   /* step plans only */
+} bq_optimizer;
 typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1 } bq_dtype;
 
 /*
@@ -181,6 +188,7 @@ typedef struct bq_tensor {
 typedef struct bq_hparams {
     float lr, beta1, beta2, eps, weight_decay;
     int64_t step;
+    float trust_coeff; /* LARS's trust coefficient; unused by the others */
 } bq_hparams;
 
 /*
@@ -198,6 +206,8 @@ typedef struct bq_hparams {
  *   AdaGrad (App. H, textbook form): g += wd * w (if weight_decay != 0);
  *       r' = r + g^2 (state 1, non-negative: pass an unsigned map as qmap1);
  *       w' = w - lr g / (sqrt(r') + eps)  (betas unused; no state 2).
+ *   LAMB and LARS (App. E, textbook forms) need per-tensor norms and run
+ *   through step plans only; this call returns BQ_ERR_ENUM for them.
  * State 1 uses qmap1 (the signed map), state 2 uses qmap2 (the unsigned map;
  * any map for state 2 must have no negative entries, so that r' >= 0).
  * Momentum and AdaGrad have one state: state2, absmax2 and qmap2 may be NULL.
@@ -233,6 +243,7 @@ typedef struct bq_tensor32 {
  *   tensors  host array of ntensors descriptors; every non-empty tensor's
  *            pointers 16-byte aligned
  *   hp       host pointer to the hyperparameters (step >= 1)
+ * LAMB and LARS are not available here (BQ_ERR_ENUM).
  * Errors: BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_ENUM, BQ_ERR_DTYPE, BQ_ERR_ALIGN,
  * BQ_ERR_ARG (step < 1), BQ_ERR_HIP.
  */
@@ -282,7 +293,17 @@ typedef struct bq_step_plan_s *bq_step_plan;
  * tensor list.  This is the only allocating call: it writes one 64-byte record
  * per tile (4096 elements; pointers at the tile's first element and block) to
  * device memory of the current device -- 16 bytes per 1,024 params -- and
- * reserves space for two prepared codebooks.
+ * reserves space for two prepared codebooks (and, for LAMB and LARS, 16 bytes
+ * of partial norms per tile and one rate per tensor).
+ * Besides the optimizers of bq_optimizer8bit_step, plans run (App. E lists
+ * 8-bit versions of both; textbook forms, one trust ratio per tensor, from
+ * the norms before the update, 1 when a norm is zero):
+ *   LAMB: m' = b1 m + (1 - b1) g;  r' = b2 r + (1 - b2) g^2;
+ *         u = (m' / (1 - b1^t)) / (sqrt(r') / sqrt(1 - b2^t) + eps) + wd w;
+ *         w' = w - lr (|w| / |u|) u   (states: signed and unsigned maps)
+ *   LARS: g' = g + wd w;  m' = b1 m + lr (trust |w| / (|g| + wd |w|)) g';
+ *         w' = w - m'   (one state; trust = hp->trust_coeff)
+ * Each run first takes the norms in an extra pass over the tensors.
  * Synchronous.  The tensors' buffers must stay valid while the plan is used.
  *   tensors  host array of ntensors descriptors (as bq_optimizer8bit_step)
  *   plan     receives the handle (NULL on error)

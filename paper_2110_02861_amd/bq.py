@@ -23,10 +23,10 @@ BQ_LINEAR_SIGNED, BQ_LINEAR_UNSIGNED = 4, 5
 CODEBOOKS = {"dynamic": (BQ_SIGNED, BQ_UNSIGNED),
              "inverse_dynamic": (BQ_INVERSE_SIGNED, BQ_INVERSE_UNSIGNED),
              "linear": (BQ_LINEAR_SIGNED, BQ_LINEAR_UNSIGNED)}
-BQ_ADAM, BQ_ADAMW, BQ_MOMENTUM, BQ_ADAGRAD = 0, 1, 2, 3
+BQ_ADAM, BQ_ADAMW, BQ_MOMENTUM, BQ_ADAGRAD, BQ_LAMB, BQ_LARS = 0, 1, 2, 3, 4, 5
 BQ_F32, BQ_F16 = 0, 1
 OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM,
-              "adagrad": BQ_ADAGRAD}
+              "adagrad": BQ_ADAGRAD, "lamb": BQ_LAMB, "lars": BQ_LARS}
 
 EXPORTS = ("bq_make_dynamic_codebook", "bq_make_codebook", "bq_make_quantile_codebook",
            "bq_estimate_quantile_codebook", "bq_quantile_workspace_bytes",
@@ -61,7 +61,7 @@ class bq_tensor32(ctypes.Structure):
 class bq_hparams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
-                ("step", ctypes.c_int64)]
+                ("step", ctypes.c_int64), ("trust_coeff", ctypes.c_float)]
 
 
 _lib = None
@@ -271,7 +271,8 @@ def bq_optimizer32bit_step(opt, grad_dtype: int, tensors, hp: dict, stream=None)
 
 def _hparams(hp: dict) -> bq_hparams:
     return bq_hparams(hp["lr"], hp["beta1"], hp.get("beta2", 0.0), hp.get("eps", 0.0),
-                      hp.get("wd", hp.get("weight_decay", 0.0)), int(hp["step"]))
+                      hp.get("wd", hp.get("weight_decay", 0.0)), int(hp["step"]),
+                      hp.get("trust", 0.0))
 
 
 def bq_prepare_codebook(qmap, prepared=None, stream=None):

@@ -16,11 +16,15 @@ namespace {
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
 bool valid_blocksize(int32_t b) { return b >= 256 && b <= 4096 && (b & (b - 1)) == 0; }
+// optimizers of the allocation-free calls; LAMB and LARS need per-tensor
+// norms and run through plans only
 bool valid_opt(bq_optimizer o)
 {
     return o == BQ_ADAM || o == BQ_ADAMW || o == BQ_MOMENTUM || o == BQ_ADAGRAD;
 }
-bool two_states(bq_optimizer o) { return o == BQ_ADAM || o == BQ_ADAMW; }
+bool valid_plan_opt(bq_optimizer o) { return valid_opt(o) || o == BQ_LAMB || o == BQ_LARS; }
+bool trust_opt(bq_optimizer o) { return o == BQ_LAMB || o == BQ_LARS; }
+bool two_states(bq_optimizer o) { return o == BQ_ADAM || o == BQ_ADAMW || o == BQ_LAMB; }
 bool valid_dtype(bq_dtype d) { return d == BQ_F32 || d == BQ_F16; }
 
 // beta^t in double by right-to-left binary exponentiation.
@@ -57,6 +61,8 @@ bq::StepScalars make_scalars(const bq_hparams &hp, bq_optimizer opt)
         s.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - beta_pow(b2, hp.step)));
     }
     s.decay = static_cast<float>(1.0 - lr * wd);
+    s.bc1_inv = static_cast<float>(1.0 / (1.0 - beta_pow(b1, hp.step)));
+    s.trust = hp.trust_coeff;
     const double ss = static_cast<double>(s.step_size), fmax = 3.4028234663852886e38;
     if (ss == 0.0) {
         s.sdiv_c = 0.0f;
@@ -125,6 +131,10 @@ struct bq_step_plan_s {
     int64_t total_tiles;
     bq::TensorDesc *tiles;  // device, one record per tile
     uint8_t *tables;        // device, two prepared maps
+    // LAMB / LARS: per-tile partial norms, per-tensor lr * ratio, tile ranges
+    double *partials;
+    float *lr_ratio;
+    int64_t *first_tile;
 };
 
 extern "C" {
@@ -392,7 +402,7 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
     if (!plan)
         return BQ_ERR_NULL;
     *plan = nullptr;
-    if (!valid_opt(opt))
+    if (!valid_plan_opt(opt))
         return BQ_ERR_ENUM;
     if (!valid_dtype(grad_dtype))
         return BQ_ERR_DTYPE;
@@ -418,10 +428,14 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
             return BQ_ERR_SIZE;
     }
     std::vector<bq::TensorDesc> recs;
+    std::vector<int64_t> first_tile;
     recs.reserve((size_t)total);
+    const bool trust = trust_opt(opt);
     for (int32_t i = 0; i < ntensors; ++i) {
         const bq_tensor &t = tensors[i];
         const int64_t nt = (t.numel + tile - 1) / tile;
+        if (nt > 0)
+            first_tile.push_back((int64_t)recs.size());
         for (int64_t k = 0; k < nt; ++k) {
             const int64_t t0 = k * tile;
             bq::TensorDesc d;
@@ -432,10 +446,12 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
             d.a1 = t.absmax1 + t0 / blocksize;
             d.a2 = two ? t.absmax2 + t0 / blocksize : nullptr;
             d.numel = t.numel - t0;
-            d.tile_begin = 0;
+            // LAMB / LARS: the tensor's index, for its lr * ratio
+            d.tile_begin = trust ? (int64_t)first_tile.size() - 1 : 0;
             recs.push_back(d);
         }
     }
+    first_tile.push_back((int64_t)recs.size());
 
     bq_step_plan_s *p = new (std::nothrow) bq_step_plan_s();
     if (!p)
@@ -453,6 +469,18 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
         if (e == hipSuccess)
             e = hipMemcpy(p->tiles, recs.data(), recs.size() * sizeof(bq::TensorDesc),
                           hipMemcpyHostToDevice);
+        if (e == hipSuccess && trust) {
+            e = hipMalloc(reinterpret_cast<void **>(&p->partials), recs.size() * 2 * sizeof(double));
+            if (e == hipSuccess)
+                e = hipMalloc(reinterpret_cast<void **>(&p->lr_ratio),
+                              (size_t)nonempty * sizeof(float));
+            if (e == hipSuccess)
+                e = hipMalloc(reinterpret_cast<void **>(&p->first_tile),
+                              first_tile.size() * sizeof(int64_t));
+            if (e == hipSuccess)
+                e = hipMemcpy(p->first_tile, first_tile.data(), first_tile.size() * sizeof(int64_t),
+                              hipMemcpyHostToDevice);
+        }
     }
     if (e != hipSuccess) {
         bq_step_plan_destroy(p);
@@ -486,10 +514,20 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
     std::memset(&a, 0, sizeof(a));
     a.tables = plan->tables;
     a.tiles = plan->tiles;
+    a.partials = plan->partials;
+    a.lr_ratio = plan->lr_ratio;
+    a.first_tile = plan->first_tile;
+    a.ntensors = plan->ntensors;
     a.sc = make_scalars(*hp, plan->opt);
-    a.use_wd = (hp->weight_decay != 0.0f && plan->opt != BQ_ADAMW) ? 1 : 0;
+    // decoupled decay for AdamW, inside the update direction for LAMB, an L2
+    // term on the gradient otherwise
+    a.use_wd = (hp->weight_decay != 0.0f && plan->opt != BQ_ADAMW && plan->opt != BQ_LAMB) ? 1
+                                                                                          : 0;
     a.total_tiles = (int32_t)plan->total_tiles;
     hipError_t e = bq::launch_prepare(qmap1, two ? qmap2 : nullptr, plan->tables, stream);
+    if (e == hipSuccess && trust_opt(plan->opt))
+        e = bq::launch_trust_ratios((int)plan->opt, (int)plan->grad_dtype, plan->blocksize, a,
+                                    stream);
     if (e == hipSuccess)
         e = bq::launch_step_oneshot((int)plan->opt, (int)plan->grad_dtype, plan->blocksize, a,
                                     stream);
@@ -501,7 +539,9 @@ bq_status bq_step_plan_destroy(bq_step_plan plan)
     if (!plan)
         return BQ_OK;
     hipError_t e = hipSuccess;
-    for (void *ptr : {static_cast<void *>(plan->tiles), static_cast<void *>(plan->tables)}) {
+    for (void *ptr : {static_cast<void *>(plan->tiles), static_cast<void *>(plan->tables),
+                      static_cast<void *>(plan->partials), static_cast<void *>(plan->lr_ratio),
+                      static_cast<void *>(plan->first_tile)}) {
         if (ptr && hipFree(ptr) != hipSuccess)
             e = hipErrorUnknown;
     }

@@ -20,6 +20,8 @@ struct StepScalars {
     // sdiv_c = inv_sqrt_bc2 / step_size, sdiv_eps = eps / step_size (each
     // clamped to the finite range; lr = 0 gives 0 and +inf: no update).
     float sdiv_c, sdiv_eps;
+    float bc1_inv;         // 1 / (1 - beta1^t)  (LAMB)
+    float trust;           // trust coefficient (LARS)
 };
 
 // One tensor of a multi-tensor launch.  tile_begin is the index of the
@@ -87,10 +89,18 @@ struct PlanArgs {
     // device array, one record per tile: pointers at the tile's first element
     // (param, grad, states) and first block (absmax), numel = elements from
     // the tile start to the tensor end (a full tile when >= the tile size)
+    // (for LAMB / LARS plans tile_begin holds the record's tensor index)
     const TensorDesc *tiles;
     StepScalars sc;
     int32_t use_wd;
     int32_t total_tiles;
+    // LAMB / LARS only: per-tile partial squared norms (2 doubles per tile),
+    // per-tensor lr * trust ratio, first tile of each tensor (ntensors + 1)
+    double *partials;
+    float *lr_ratio;
+    const int64_t *first_tile;
+    int32_t ntensors;
+    int32_t pad;
 };
 
 // One tensor of a 32-bit-state launch (states are fp32 arrays).
@@ -140,13 +150,18 @@ hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *table
                           hipStream_t stream);
 hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const PlanArgs &args,
                                hipStream_t stream);
+// LAMB / LARS: per-tile partial norms, then the per-tensor lr * ratio.
+hipError_t launch_trust_ratios(int opt, int grad_dtype, int blocksize, const PlanArgs &args,
+                               hipStream_t stream);
 hipError_t launch_quantize_prepared(const uint8_t *tables, const float *x, int64_t n,
                                     int blocksize, uint8_t *codes, float *absmax,
                                     hipStream_t stream);
 
-enum { kAdam = 0, kAdamW = 1, kMomentum = 2, kAdaGrad = 3 };
-// optimizers with a second state (Adam, AdamW)
-constexpr bool has_two_states(int opt) { return opt == kAdam || opt == kAdamW; }
+enum { kAdam = 0, kAdamW = 1, kMomentum = 2, kAdaGrad = 3, kLamb = 4, kLars = 5 };
+// optimizers with a second state (Adam, AdamW, LAMB)
+constexpr bool has_two_states(int opt) { return opt == kAdam || opt == kAdamW || opt == kLamb; }
+// optimizers with a per-tensor trust ratio (two passes: norms, then the step)
+constexpr bool has_trust_ratio(int opt) { return opt == kLamb || opt == kLars; }
 enum { kF32 = 0, kF16 = 1 };
 
 hipError_t launch_step(int opt, int grad_dtype, int blocksize, const StepArgs &args,

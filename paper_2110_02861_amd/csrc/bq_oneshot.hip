@@ -168,7 +168,7 @@ struct StepOS {
     // caller before anything else so their L2 latency overlaps the HBM loads.
     template <bool FULL>
     __device__ static void tile(const PlanArgs &a, const TensorDesc &D, int64_t t0, uint8_t *lds,
-                                const vu4 (&gran)[kGPT])
+                                const vu4 (&gran)[kGPT], float lr_r)
     {
         uint32_t *slots = reinterpret_cast<uint32_t *>(lds + kLdsSlots);
         BlockNorm *norms = reinterpret_cast<BlockNorm *>(lds + kLdsNorms);
@@ -304,6 +304,9 @@ struct StepOS {
             if constexpr (OPT == kMomentum) {
                 mi = sc.b1 * mi + gi;
                 wi = wi - sc.lr * mi;
+            } else if constexpr (OPT == kLars) {
+                mi = sc.b1 * mi + lr_r * gi;  // lr_r: the tensor's lr * trust ratio
+                wi = wi - mi;
             } else if constexpr (OPT == kAdaGrad) {
                 mi = mi + gi * gi;
                 const float denom =
@@ -316,11 +319,20 @@ struct StepOS {
                 mi = sc.b1 * mi + sc.omb1 * gi;
                 vi = sc.b2 * vi + sc.omb2 * (gi * gi);
                 // the param update is not rounded like the oracle's anyway
-                // (hardware sqrt and reciprocal), so it may fuse and take
-                // step_size into the denominator
-                const float denom =
-                    __builtin_fmaf(__builtin_amdgcn_sqrtf(vi), sc.sdiv_c, sc.sdiv_eps);
-                wi = __builtin_fmaf(-mi, __builtin_amdgcn_rcpf(denom), wi);
+                // (hardware sqrt and reciprocal), so it may fuse
+                if constexpr (OPT == kLamb) {
+                    // u = mhat / (sqrt(vhat) + eps) + wd w;  w -= lr_r u
+                    const float denom =
+                        __builtin_fmaf(__builtin_amdgcn_sqrtf(vi), sc.inv_sqrt_bc2, sc.eps);
+                    const float u = __builtin_fmaf(mi * sc.bc1_inv, __builtin_amdgcn_rcpf(denom),
+                                                   sc.wd * wi);
+                    wi = __builtin_fmaf(-lr_r, u, wi);
+                } else {
+                    // step_size taken into the denominator
+                    const float denom =
+                        __builtin_fmaf(__builtin_amdgcn_sqrtf(vi), sc.sdiv_c, sc.sdiv_eps);
+                    wi = __builtin_fmaf(-mi, __builtin_amdgcn_rcpf(denom), wi);
+                }
                 v[i] = ok ? vi : 0.0f;
                 mx2[c] = fmaxf(mx2[c], fabsf(v[i]));
             }
@@ -485,11 +497,124 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
     D.a1 = dp->a1;
     D.a2 = dp->a2;
     D.numel = dp->numel;
+    float lr_r = 0.0f;
+    if constexpr (has_trust_ratio(OPT))
+        lr_r = G(a.lr_ratio)[dp->tile_begin];  // tile_begin holds the tensor index
     const int64_t t0 = 0;
     if (t0 + K::TILE <= D.numel)
-        K::template tile<true>(a, D, t0, lds, gran);
+        K::template tile<true>(a, D, t0, lds, gran, lr_r);
     else
-        K::template tile<false>(a, D, t0, lds, gran);
+        K::template tile<false>(a, D, t0, lds, gran, lr_r);
+}
+
+// ---------------------------------------------------------------------------
+// LAMB / LARS: per-tile partial squared norms, then per-tensor lr * ratio
+// ---------------------------------------------------------------------------
+
+// One workgroup per tile, the step kernel's tile shape.  Sums (in double) of
+// w^2 and of u^2 (LAMB: u = mhat / (sqrt(vhat) + eps) + wd w from the states
+// the step will compute) or g^2 (LARS, g before weight decay).
+template <int OPT, int GRAD, int B>
+__global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
+{
+    using K = StepOS<OPT, GRAD, B>;
+    __shared__ float q1[256], q2[256];
+    __shared__ double red[kOSWaves][2];
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const gptr<const TensorDesc> dp = G(a.tiles) + blockIdx.x;
+    float *const param = dp->param;
+    const void *const grad = dp->grad;
+    const uint8_t *const s1 = dp->s1;
+    const uint8_t *const s2 = dp->s2;
+    const float *const a1 = dp->a1;
+    const float *const a2 = dp->a2;
+    const int64_t numel = dp->numel;
+    if constexpr (OPT == kLamb) {
+        if (tid < 256) {
+            q1[tid] = G(reinterpret_cast<const float *>(a.tables + kPreparedOffQ))[tid];
+            q2[tid] = G(reinterpret_cast<const float *>(a.tables + kPreparedBytes +
+                                                        kPreparedOffQ))[tid];
+        }
+        __syncthreads();
+    }
+    const StepScalars &sc = a.sc;
+    double sw = 0.0, sx = 0.0;
+#pragma unroll
+    for (int c = 0; c < K::C; ++c) {
+        const int b = (8 * c + wave) / K::kSPB;  // tile-local block of this chunk
+        const int64_t e0 = c * (kOS * 4) + tid * 4;
+        const bool live = e0 < numel;
+        const float n1 = (OPT == kLamb && live) ? G(a1)[b] : 0.0f;
+        const float n2 = (OPT == kLamb && live) ? G(a2)[b] : 0.0f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t e = e0 + r;
+            if (e < numel) {
+                const float w = G(param)[e];
+                float g;
+                if constexpr (GRAD == kF16)
+                    g = (float)G(static_cast<const _Float16 *>(grad))[e];
+                else
+                    g = G(static_cast<const float *>(grad))[e];
+                sw += (double)w * (double)w;
+                if constexpr (OPT == kLamb) {
+                    const float m = q1[G(s1)[e]] * n1;
+                    const float v = q2[G(s2)[e]] * n2;
+                    const float mn = sc.b1 * m + sc.omb1 * g;
+                    const float vn = sc.b2 * v + sc.omb2 * (g * g);
+                    const float denom =
+                        __builtin_fmaf(__builtin_amdgcn_sqrtf(vn), sc.inv_sqrt_bc2, sc.eps);
+                    const float u =
+                        __builtin_fmaf(mn * sc.bc1_inv, __builtin_amdgcn_rcpf(denom), sc.wd * w);
+                    sx += (double)u * (double)u;
+                } else {
+                    sx += (double)g * (double)g;
+                }
+            }
+        }
+    }
+    // wave sums, then the 8 wave sums in order
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        sw += __shfl_xor(sw, off);
+        sx += __shfl_xor(sx, off);
+    }
+    if ((tid & 63) == 0) {
+        red[wave][0] = sw;
+        red[wave][1] = sx;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double tw = 0.0, tx = 0.0;
+        for (int k = 0; k < kOSWaves; ++k) {
+            tw += red[k][0];
+            tx += red[k][1];
+        }
+        G(a.partials)[2 * (int64_t)blockIdx.x] = tw;
+        G(a.partials)[2 * (int64_t)blockIdx.x + 1] = tx;
+    }
+}
+
+// One thread per tensor: its tiles' partial sums in tile order, then
+// lr * ratio, ratio = |w| / |u| (LAMB) or trust |w| / (|g| + wd |w|) (LARS),
+// 1 when either norm is zero.
+__global__ __launch_bounds__(256) void trust_ratio_kernel(const PlanArgs a, int lamb)
+{
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    if (t >= a.ntensors)
+        return;
+    const int64_t k0 = G(a.first_tile)[t], k1 = G(a.first_tile)[t + 1];
+    double sw = 0.0, sx = 0.0;
+    for (int64_t k = k0; k < k1; ++k) {
+        sw += G(a.partials)[2 * k];
+        sx += G(a.partials)[2 * k + 1];
+    }
+    const double nw = sqrt(sw), nx = sqrt(sx);
+    double ratio = 1.0;
+    if (nw > 0.0 && nx > 0.0)
+        ratio = lamb ? nw / nx : (double)a.sc.trust * nw / (nx + (double)a.sc.wd * nw);
+    G(a.lr_ratio)[t] = (float)((double)a.sc.lr * ratio);
 }
 
 // ---------------------------------------------------------------------------
@@ -643,10 +768,50 @@ hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *table
     return hipGetLastError();
 }
 
+template <int OPT, int GRAD>
+hipError_t launch_norms_b(int blocksize, const PlanArgs &a, hipStream_t stream)
+{
+    const dim3 grid((unsigned)a.total_tiles), block(kOS);
+    switch (blocksize) {
+    case 256: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 256>), grid, block, 0, stream, a); break;
+    case 512: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 512>), grid, block, 0, stream, a); break;
+    case 1024: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 1024>), grid, block, 0, stream, a); break;
+    case 2048: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 2048>), grid, block, 0, stream, a); break;
+    case 4096: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 4096>), grid, block, 0, stream, a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int OPT>
+hipError_t launch_norms_g(int grad_dtype, int blocksize, const PlanArgs &a, hipStream_t stream)
+{
+    return grad_dtype == kF16 ? launch_norms_b<OPT, kF16>(blocksize, a, stream)
+                              : launch_norms_b<OPT, kF32>(blocksize, a, stream);
+}
+
+hipError_t launch_trust_ratios(int opt, int grad_dtype, int blocksize, const PlanArgs &a,
+                               hipStream_t stream)
+{
+    hipError_t e;
+    switch (opt) {
+    case kLamb: e = launch_norms_g<kLamb>(grad_dtype, blocksize, a, stream); break;
+    case kLars: e = launch_norms_g<kLars>(grad_dtype, blocksize, a, stream); break;
+    default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(trust_ratio_kernel, dim3((unsigned)((a.ntensors + 255) / 256)), dim3(256),
+                       0, stream, a, opt == kLamb ? 1 : 0);
+    return hipGetLastError();
+}
+
 hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const PlanArgs &a,
                                hipStream_t stream)
 {
     switch (opt) {
+    case kLamb: return launch_os_g<kLamb>(grad_dtype, blocksize, a, stream);
+    case kLars: return launch_os_g<kLars>(grad_dtype, blocksize, a, stream);
     case kAdam: return launch_os_g<kAdam>(grad_dtype, blocksize, a, stream);
     case kAdamW: return launch_os_g<kAdamW>(grad_dtype, blocksize, a, stream);
     case kMomentum: return launch_os_g<kMomentum>(grad_dtype, blocksize, a, stream);

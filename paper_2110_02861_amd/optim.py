@@ -2,7 +2,9 @@
 
 The paper's 8-bit optimizers replace their 32-bit counterparts without
 hyperparameter changes (Section 1, Section 4): Adam (Eq. 2 with bias
-correction), AdamW, SGD with momentum (Eq. 1), and AdaGrad (App. H).  Each state is stored as one
+correction), AdamW, SGD with momentum (Eq. 1), and AdaGrad (App. H); LAMB and
+LARS, whose 8-bit versions App. E times, in their textbook forms (per-tensor
+trust ratios, which need a norm pass and therefore step plans).  Each state is stored as one
 uint8 code per element plus one fp32 absmax per block of ``blocksize`` elements
 (Section 3.1); the signed dynamic map holds the first state and the unsigned
 dynamic map the second (Section 3.2); AdaGrad's single, non-negative state
@@ -79,7 +81,7 @@ class Optimizer8bit(torch.optim.Optimizer):
 
     @property
     def _two_states(self) -> bool:
-        return self.OPT in (bq.BQ_ADAM, bq.BQ_ADAMW)
+        return self.OPT in (bq.BQ_ADAM, bq.BQ_ADAMW, bq.BQ_LAMB)
 
     @property
     def _state1_unsigned(self) -> bool:
@@ -96,6 +98,8 @@ class Optimizer8bit(torch.optim.Optimizer):
 
     def _init_state(self, p: torch.Tensor, state: dict) -> None:
         state["step"] = 0
+        if self.OPT in (bq.BQ_LAMB, bq.BQ_LARS) and not self._is_8bit(p):
+            raise NotImplementedError("LAMB / LARS keep 8-bit states only (no 32-bit override)")
         if self._is_8bit(p):
             _, _, z1, z2 = self._maps(p.device)
             nb = (p.numel() + self.blocksize - 1) // self.blocksize
@@ -163,7 +167,7 @@ class Optimizer8bit(torch.optim.Optimizer):
         for p in ps:
             s = self.state[p]
             rows.append((p, p.grad, s["state1"], s.get("state2"), s["absmax1"], s.get("absmax2")))
-        if not self.use_plans:
+        if not self.use_plans and self.OPT not in (bq.BQ_LAMB, bq.BQ_LARS):
             bq.bq_optimizer8bit_step(self.OPT, self.blocksize, gdt, rows, hp, q1, q2)
             return
         # a plan holds device pointers: reuse it while every storage stays put
@@ -257,6 +261,48 @@ class Adagrad8bit(Optimizer8bit):
     def _hparams(self, group, step):
         return dict(lr=group["lr"], beta1=0.0, beta2=0.0, eps=group["eps"],
                     wd=group["weight_decay"], step=step)
+
+
+class Lamb8bit(Optimizer8bit):
+    """LAMB with 8-bit states: the Adam direction u = mhat / (sqrt(vhat) + eps)
+    + weight_decay w, scaled per tensor by |w| / |u| (1 if either is zero):
+    w -= lr |w| / |u| u.  Runs through step plans (a norm pass, then the step)."""
+
+    OPT = bq.BQ_LAMB
+
+    def __init__(self, params, lr=1e-3, betas=(0.9, 0.999), eps=1e-6, weight_decay=0.0, **kw):
+        _check_hparams(lr, betas, eps, weight_decay)
+        super().__init__(params, dict(lr=lr, betas=tuple(betas), eps=eps,
+                                      weight_decay=weight_decay), **kw)
+
+    def _hparams(self, group, step):
+        b1, b2 = group["betas"]
+        return dict(lr=group["lr"], beta1=b1, beta2=b2, eps=group["eps"],
+                    wd=group["weight_decay"], step=step)
+
+
+class Lars8bit(Optimizer8bit):
+    """LARS with an 8-bit momentum buffer: per tensor the local rate
+    trust_coefficient |w| / (|g| + weight_decay |w|) (1 if a norm is zero);
+    m = momentum m + lr rate (g + weight_decay w); w -= m.  Runs through step
+    plans (a norm pass, then the step)."""
+
+    OPT = bq.BQ_LARS
+
+    def __init__(self, params, lr=0.1, momentum=0.9, weight_decay=0.0, trust_coefficient=1e-3,
+                 **kw):
+        if lr < 0.0:
+            raise ValueError(f"invalid learning rate {lr}")
+        if not 0.0 <= momentum < 1.0:
+            raise ValueError(f"invalid momentum {momentum}")
+        if weight_decay < 0.0 or trust_coefficient <= 0.0:
+            raise ValueError("invalid weight_decay or trust_coefficient")
+        super().__init__(params, dict(lr=lr, momentum=momentum, weight_decay=weight_decay,
+                                      trust_coefficient=trust_coefficient), **kw)
+
+    def _hparams(self, group, step):
+        return dict(lr=group["lr"], beta1=group["momentum"], beta2=0.0, eps=0.0,
+                    wd=group["weight_decay"], step=step, trust=group["trust_coefficient"])
 
 
 def _check_hparams(lr, betas, eps, weight_decay):

@@ -13,7 +13,7 @@ from paper_2110_02861_amd import bq
 needs_gpu = pytest.mark.skipif(not torch.cuda.is_available(), reason="no GPU visible")
 
 OPT_ID = {"adam": oracle.ADAM, "adamw": oracle.ADAMW, "momentum": oracle.MOMENTUM,
-          "adagrad": oracle.ADAGRAD}
+          "adagrad": oracle.ADAGRAD, "lamb": oracle.LAMB, "lars": oracle.LARS}
 
 
 def say(*a):
@@ -84,7 +84,7 @@ class HostState:
         prev = self.w.astype(np.float64)
         oracle.step8(OPT_ID[opt], B, self.w, g, self.c1, self.a1, q1, self.c2, self.a2, q2,
                      hp["lr"], hp["beta1"], hp.get("beta2", 0.0), hp.get("eps", 0.0),
-                     hp.get("wd", 0.0), t)
+                     hp.get("wd", 0.0), t, trust=hp.get("trust", 0.0))
         upd = np.abs(prev - self.w.astype(np.float64))
         self.step_tol = 1e-6 * upd
         self.tol += 1e-6 * upd + 2.0 ** -23 * np.abs(self.w.astype(np.float64))

@@ -171,7 +171,7 @@ def test_step_plan_argument_checks(L):
     h = ctypes.c_void_p(123)
     good = _tensors(_good_row())
     assert c(0, 2048, 1, good, 1, None) == bq.BQ_ERR_NULL
-    assert c(5, 2048, 1, good, 1, ctypes.byref(h)) == bq.BQ_ERR_ENUM
+    assert c(6, 2048, 1, good, 1, ctypes.byref(h)) == bq.BQ_ERR_ENUM
     assert h.value is None  # the handle is cleared on every error
     assert c(0, 2048, 9, good, 1, ctypes.byref(h)) == bq.BQ_ERR_DTYPE
     assert c(0, 100, 1, good, 1, ctypes.byref(h)) == bq.BQ_ERR_BLOCKSIZE

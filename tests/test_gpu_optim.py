@@ -32,10 +32,17 @@ CASES = {
               oracle.ADAMW),
     "sgd": (optim.SGD8bit, dict(lr=0.1, momentum=0.9, weight_decay=1e-4), oracle.MOMENTUM),
     "adagrad": (optim.Adagrad8bit, dict(lr=1e-2, eps=1e-10, weight_decay=0.0), oracle.ADAGRAD),
+    "lamb": (optim.Lamb8bit, dict(lr=1e-3, betas=(0.9, 0.999), eps=1e-6, weight_decay=0.01),
+             oracle.LAMB),
+    "lars": (optim.Lars8bit, dict(lr=0.5, momentum=0.9, weight_decay=1e-4,
+                                  trust_coefficient=1e-3), oracle.LARS),
 }
 
 
 def oracle_hp(kw):
+    if "trust_coefficient" in kw:  # LARS
+        return dict(lr=kw["lr"], beta1=kw["momentum"], beta2=0.0, eps=0.0,
+                    wd=kw["weight_decay"], trust=kw["trust_coefficient"])
     if "betas" not in kw and "momentum" not in kw:  # AdaGrad
         return dict(lr=kw["lr"], beta1=0.0, beta2=0.0, eps=kw["eps"], wd=kw["weight_decay"])
     if "momentum" in kw:
@@ -95,7 +102,7 @@ def oracle_step8(kind, hp, w, g, snap, n, two, t):
         a2 = snap["absmax2"].copy() if two else None
     w = w.copy()
     oracle.step8(kind, B, w, g, c1, a1, q1, c2, a2, q2 if two else None, hp["lr"], hp["beta1"],
-                 hp["beta2"], hp["eps"], hp["wd"], t)
+                 hp["beta2"], hp["eps"], hp["wd"], t, trust=hp.get("trust", 0.0))
     return w, c1, a1, c2, a2
 
 
@@ -105,7 +112,7 @@ def oracle_step8(kind, hp, w, g, snap, n, two, t):
 def test_optimizer_matches_oracle(case, gdt, use_plans):
     cls, kw, kind = CASES[case]
     hp = oracle_hp(kw)
-    two = kind in (oracle.ADAM, oracle.ADAMW)
+    two = kind in (oracle.ADAM, oracle.ADAMW, oracle.LAMB)
     params = init_params(7)
     opt = cls(params, blocksize=B, use_plans=use_plans, **kw)
     for t in range(1, 4):

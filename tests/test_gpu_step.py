@@ -24,6 +24,8 @@ HPS = {
     "adamw": dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.01),
     "momentum": dict(lr=0.1, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4),
     "adagrad": dict(lr=1e-2, beta1=0.0, beta2=0.0, eps=1e-10, wd=0.0),
+    "lamb": dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-6, wd=0.01),
+    "lars": dict(lr=0.5, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4, trust=1e-3),
 }
 
 
@@ -35,7 +37,7 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
     if maps is not None:  # (state-1 map, state-2 map), host fp32
         qs, qu = maps
         qs_d, qu_d = torch.from_numpy(qs).cuda(), torch.from_numpy(qu).cuda()
-    two = opt in ("adam", "adamw")
+    two = opt in ("adam", "adamw", "lamb")
     hp = dict(HPS[opt] if hp is None else hp)
     tdt = torch.float16 if grad_dtype == bq.BQ_F16 else torch.float32
     ndt = np.float16 if grad_dtype == bq.BQ_F16 else np.float32
@@ -227,3 +229,12 @@ def test_other_codebooks_step(opt, family, path):
     q1, q2 = _map_families()[family]
     run_lists(opt, 2048, bq.BQ_F16, [1, 2047, 4097, 3 * 4096 + 77], 3, seed=5, path=path,
               maps=(q1, q2))
+
+
+@pytest.mark.parametrize("B", [256, 2048, 4096])
+@pytest.mark.parametrize("grad_dtype", [bq.BQ_F16, bq.BQ_F32])
+@pytest.mark.parametrize("opt", ["lamb", "lars"])
+def test_trust_ratio_optimizers(opt, grad_dtype, B):
+    """LAMB and LARS through plans (norm pass, per-tensor rates, step), over a
+    ragged list of tensors, 4 steps free-running."""
+    run_lists(opt, B, grad_dtype, RAGGED, steps=4, path="plan")

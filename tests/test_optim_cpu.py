@@ -32,6 +32,14 @@ def test_defaults_follow_torch():
     s = optim.SGD8bit(p, lr=0.1)
     assert s.defaults == dict(lr=0.1, momentum=0.9, weight_decay=0.0)
     assert a.blocksize == 2048 and a.min_8bit_size == 0 and a.use_plans
+    lamb = optim.Lamb8bit(p, weight_decay=0.01)
+    assert lamb._hparams(lamb.param_groups[0], 1) == dict(lr=1e-3, beta1=0.9, beta2=0.999,
+                                                          eps=1e-6, wd=0.01, step=1)
+    lars = optim.Lars8bit(p, lr=0.2)
+    assert lars._hparams(lars.param_groups[0], 4) == dict(lr=0.2, beta1=0.9, beta2=0.0, eps=0.0,
+                                                          wd=0.0, step=4, trust=1e-3)
+    with pytest.raises(ValueError):
+        optim.Lars8bit(p, trust_coefficient=0.0)
     g = optim.Adagrad8bit(p)
     assert g.defaults == dict(lr=1e-2, eps=1e-10, weight_decay=0.0)
     assert g._hparams(g.param_groups[0], 2) == dict(lr=1e-2, beta1=0.0, beta2=0.0, eps=1e-10,
