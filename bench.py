@@ -41,8 +41,8 @@ BLOCKSIZE = 2048
 # the bench reports traffic null.
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "4e884610fe02e03e9dff23a9c59a907babaeb7e7178cc25f54c685f5b7f6c3c0",
-    "fetch_kib": 6132440.0, "write_kib": 9150410.0, "fetch_scale": 2.0, "write_scale": 1.0,
+    "sources_sha256": "83c016a5516dcfb38bec291f30062715ae7f0aea0c8f1cfe57774de4ae422fcf",
+    "fetch_kib": 6132450.0, "write_kib": 9150410.0, "fetch_scale": 2.0, "write_scale": 1.0,
 }
 
 
