@@ -28,14 +28,12 @@ constexpr int kThreads = 512;
 constexpr int kTableWords = 4096;  // 16 KiB
 
 template <int CHUNKS, bool EARLY_ABSMAX, bool TABLE>
-__global__ __launch_bounds__(kThreads) void stream_kernel(float *__restrict__ w,
-                                                          const uint16_t *__restrict__ g,
-                                                          uint8_t *__restrict__ c1,
-                                                          uint8_t *__restrict__ c2,
-                                                          float *__restrict__ a1,
-                                                          float *__restrict__ a2, int lg_block,
-                                                          uint32_t key,
-                                                          const uint32_t *__restrict__ table)
+// (no __restrict__ on the buffers: with it the compiler dropped the
+// non-temporal hint from the stores of the one-chunk variants)
+__global__ __launch_bounds__(kThreads) void stream_kernel(float *w, const uint16_t *g,
+                                                          uint8_t *c1, uint8_t *c2, float *a1,
+                                                          float *a2, int lg_block, uint32_t key,
+                                                          const uint32_t *table)
 {
     __shared__ uint32_t lds[TABLE ? kTableWords : 1];
     if (TABLE) {
