@@ -8,9 +8,15 @@ states already resident in HBM.  By default the step goes through a step plan
 bq_optimizer8bit_step.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+                    [--workload lm1p5b-adam|gpt2m-adamw|resnet50-momentum|
+                                quantize|dequantize] [--blocksize B]
 
 Prints one JSON line.  The CPU baseline is the oracle (plain C, OpenMP over
 blocks) timed on a bounded sample of the same workload on the host cores.
+The other workloads are secondary measurements of the same kernels: the
+8-bit AdamW step on the GPT-2-medium list (fp16 grads), the 8-bit Momentum
+step on the ResNet-50 list (fp32 grads), and standalone block-wise quantize /
+dequantize of 67,108,864 Student-t values over four rotating buffers.
 """
 from __future__ import annotations
 
@@ -32,17 +38,20 @@ METRIC = "8-bit Adam step params/sec and achieved HBM GB/s (% of peak), 1.5B-par
 HBM_PEAK_GBS = 8000.0
 BLOCKSIZE = 2048
 
-# HBM traffic of one step-kernel launch on this workload, from two rocprofv3
-# --pmc runs of `bench.py --steps 3 --warmup 1 --no-cpu-baseline` (FETCH_SIZE,
-# then WRITE_SIZE, KiB per dispatch), FETCH_SIZE scaled by 2.0 and WRITE_SIZE by
-# 1.0: the factors that make the counters of a plain fp32->fp16 copy of known
-# size read its true bytes on MI355X (profiles/step_kernel_adam_f16_b2048_lm1p5b_pmc.md).
-# Valid only for the kernel sources it was taken on (sha256 below); otherwise
-# the bench reports traffic null.
+# HBM traffic of one launch of the dominant kernel, from two rocprofv3 --pmc
+# runs of the bench command (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch),
+# FETCH_SIZE scaled by 2.0 and WRITE_SIZE by 1.0: the factors that make the
+# counters of kernels of known traffic (a plain fp32->fp16 copy, the
+# same-byte-mix stream) read their true bytes on MI355X.  Valid only for the
+# kernel sources the counters were taken on (sha256 below); otherwise the
+# bench reports traffic null.  Keys: (workload, blocksize, path).
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h"]
+TRAFFIC_SOURCES_SHA256 = "2b6fb4e267479793f1513686ce5844880d0a9b1d9a6e67159323bd28348511df"
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    "sources_sha256": "83c016a5516dcfb38bec291f30062715ae7f0aea0c8f1cfe57774de4ae422fcf",
-    "fetch_kib": 6132450.0, "write_kib": 9150410.0, "fetch_scale": 2.0, "write_scale": 1.0,
+    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132440.0, "write_kib": 9150410.0},
+    ("quantize", 2048, "plan"): {"fetch_kib": 131151.0, "write_kib": 65792.0},
+    ("dequantize", 2048, "call"): {"fetch_kib": 33815.7, "write_kib": 262165.0},
 }
 
 
@@ -63,13 +72,14 @@ def kernel_sources_sha256():
     return h.hexdigest()
 
 
-def measured_traffic():
-    """Counter-measured HBM bytes per step-kernel launch, or None when the
-    kernel sources differ from the ones the counters were taken on."""
-    m = MEASURED_TRAFFIC
-    if m["sources_sha256"] is None or m["sources_sha256"] != kernel_sources_sha256():
+def measured_traffic(workload, blocksize, path):
+    """Counter-measured HBM bytes per launch of the workload's dominant kernel,
+    or None when none were taken for it or the kernel sources differ from the
+    ones the counters were taken on."""
+    m = MEASURED_TRAFFIC.get((workload, blocksize, path))
+    if m is None or TRAFFIC_SOURCES_SHA256 != kernel_sources_sha256():
         return None
-    return m["fetch_kib"] * 1024 * m["fetch_scale"] + m["write_kib"] * 1024 * m["write_scale"]
+    return m["fetch_kib"] * 1024 * FETCH_SCALE + m["write_kib"] * 1024 * WRITE_SCALE
 
 
 def stream_ceiling(torch, nparams, steps=20):
@@ -125,32 +135,44 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def setup_c5(torch, bq, workloads, seed=0):
-    specs = workloads.lm_1p5b_specs()
+def setup_list(torch, bq, workloads, config, nstates, blocksize=BLOCKSIZE, seed=0):
+    """Params, a ring of two grad buffers and zero 8-bit states for one of the
+    parameter lists, generated on the GPU.  Returns (specs, params, grads,
+    states, rows) with rows[r] the bq_tensor tuples that use grad buffer r."""
+    specs = workloads.SPECS[config]()
+    gdt = torch.float16 if workloads.GRADS[config][0] == "float16" else torch.float32
     dev = torch.device("cuda:0")
-    B = BLOCKSIZE
+    B = blocksize
     params, grads, states = [], [[], []], []
     for i, s in enumerate(specs):
         n = s.numel
         nb = (n + B - 1) // B
         w = torch.empty(n, dtype=torch.float32, device=dev)
-        workloads.init_param_device(s, w, seed, "c5", i)
+        workloads.init_param_device(s, w, seed, config, i)
         params.append(w)
         for r in range(2):
-            g = torch.empty(n, dtype=torch.float16, device=dev)
-            workloads.grad_device("c5", s, g, seed, i, r)
+            g = torch.empty(n, dtype=gdt, device=dev)
+            workloads.grad_device(config, s, g, seed, i, r)
             grads[r].append(g)
-        states.append((torch.full((n,), 127, dtype=torch.uint8, device=dev),
-                       torch.zeros(n, dtype=torch.uint8, device=dev),
-                       torch.zeros(nb, dtype=torch.float32, device=dev),
-                       torch.zeros(nb, dtype=torch.float32, device=dev)))
+        if nstates == 2:
+            states.append((torch.full((n,), 127, dtype=torch.uint8, device=dev),
+                           torch.zeros(n, dtype=torch.uint8, device=dev),
+                           torch.zeros(nb, dtype=torch.float32, device=dev),
+                           torch.zeros(nb, dtype=torch.float32, device=dev)))
+        else:
+            states.append((torch.full((n,), 127, dtype=torch.uint8, device=dev), None,
+                           torch.zeros(nb, dtype=torch.float32, device=dev), None))
     torch.cuda.synchronize()
     rows = [[(params[i], grads[r][i], states[i][0], states[i][1], states[i][2], states[i][3])
              for i in range(len(specs))] for r in range(2)]
     return specs, params, grads, states, rows
 
 
-def cpu_baseline(specs, params, grads, layers, steps=4):
+def setup_c5(torch, bq, workloads, seed=0):
+    return setup_list(torch, bq, workloads, "c5", 2, BLOCKSIZE, seed)
+
+
+def cpu_baseline(specs, params, grads, layers, steps=6):
     """Time the oracle on the first `layers` transformer layers of the list
     (initial params, the first grad buffer, zero state): one warm-up step and
     `steps` timed steps on all host cores."""
@@ -192,109 +214,129 @@ def cpu_baseline(specs, params, grads, layers, steps=4):
     }
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-stream-ceiling", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=16)
-    ap.add_argument("--path", choices=["plan", "call"], default="plan",
-                    help="plan: bq_step_plan_run (one launch over all 580 tensors); "
-                         "call: bq_optimizer8bit_step (descriptor chunks of 56 tensors)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py measures one GPU only: the 8-bit step has no cross-GPU exchange, and "
-              "this build runs on a single MI355X (use --gpus 1)", file=sys.stderr)
-        sys.exit(2)
+LIST_WORKLOADS = {
+    # name: (config, optimizer, states, description)
+    "lm1p5b-adam": ("c5", "adam", 2,
+                    "8-bit Adam, 1.5B-param LM-shaped list: 48 layers, d=1600, ffn 6400, "
+                    "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4) "
+                    "with 0.01% outliers x1000"),
+    "gpt2m-adamw": ("c4", "adamw", 2,
+                    "8-bit AdamW, GPT-2-medium-shaped list: 24 layers, d=1024, ffn 4096, "
+                    "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4), "
+                    "heavy-tailed embedding rows"),
+    "resnet50-momentum": ("c3", "momentum", 1,
+                          "8-bit Momentum, ResNet-50 v1.5 parameter list (161 tensors); conv/fc "
+                          "N(0, sqrt(2/fan_in)), BN 1/0, fp32 grads N(0,1e-3)"),
+}
+QUANT_N = 67_108_864
+QUANT_BUFFERS = 4
 
-    import torch
-    from paper_2110_02861_amd import bq, workloads
 
+def timed(torch, stream, fn, steps, warmup, per_event):
+    """Run fn(i) warmup times, then `steps` times with a HIP event on `stream`
+    every `per_event` calls.  Returns (ms per call over the whole timed region,
+    sorted per-call ms of each event segment)."""
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True)]
+    evs[0].record(stream)
+    for i in range(steps):
+        fn(warmup + i)
+        if (i + 1) % per_event == 0 or i + 1 == steps:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            evs.append(e)
+    torch.cuda.synchronize()
+    total = evs[0].elapsed_time(evs[-1]) / steps
+    seg = []
+    done = 0
+    for a, b in zip(evs[:-1], evs[1:]):
+        k = min(per_event, steps - done)
+        done += k
+        seg.append(a.elapsed_time(b) / k)
+    return total, sorted(seg)
+
+
+def base_record(args, metric, value, unit, ms, seg, dtype, data, config):
+    return {
+        "metric": metric, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dtype, "data": data, "config": config,
+        "ms_per_step_median": seg[len(seg) // 2], "ms_per_step_min": seg[0],
+    }
+
+
+def run_list(args, torch, bq, workloads):
+    config, opt_name, nstates, desc = LIST_WORKLOADS[args.workload]
+    headline = args.workload == "lm1p5b-adam"
+    B = args.blocksize
+    opt = bq.OPTIMIZERS[opt_name]
+    gdt_name = workloads.GRADS[config][0]
+    gdt = bq.BQ_F16 if gdt_name == "float16" else bq.BQ_F32
     torch.cuda.set_device(0)
     qs_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)).cuda()
     qu_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)).cuda()
-    log("allocating the 1.5B-parameter list")
-    specs, params, grads, states, rows = setup_c5(torch, bq, workloads)
+    log(f"allocating the {args.workload} list")
+    specs, params, grads, states, rows = setup_list(torch, bq, workloads, config, nstates, B)
     numels = [s.numel for s in specs]
     nparams = sum(numels)
-    bytes_step = step_bytes(numels, BLOCKSIZE, 2, 2)
-    hp = {k: workloads.C5[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
+    bytes_step = step_bytes(numels, B, 2 if gdt == bq.BQ_F16 else 4, nstates)
+    C = getattr(workloads, config.upper())
+    hp = {k: C[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if headline and not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         cpu = cpu_baseline(specs, params, grads, args.cpu_layers)
         log(f"cpu baseline {cpu['value'] / 1e6:.1f} Mparam/s on {cpu['cores']} threads")
 
     ceiling = None
-    if not args.no_stream_ceiling:
+    if headline and not args.no_stream_ceiling:
         log("measuring the same-byte-mix streaming ceiling")
         ceiling, ceiling_per = stream_ceiling(torch, nparams)
         log(f"stream ceiling {ceiling:.0f} GB/s (variants {ceiling_per})")
 
     stream = torch.cuda.current_stream()
+    q2 = qu_d if nstates == 2 else None
 
     # a ring of two gradient buffers, one plan (or descriptor array) for each
     if args.path == "plan":
-        plans = [bq.StepPlan(bq.BQ_ADAM, BLOCKSIZE, bq.BQ_F16, r) for r in rows]
+        plans = [bq.StepPlan(opt, B, gdt, r) for r in rows]
 
-        def step(t):
-            plans[t % 2].run(dict(hp, step=t), qs_d, qu_d, stream=stream)
+        def step(i):
+            plans[i % 2].run(dict(hp, step=i + 1), qs_d, q2, stream=stream)
     else:
         arrays = [(bq.make_tensor_array(r), len(r)) for r in rows]
 
-        def step(t):
-            bq.bq_optimizer8bit_step(bq.BQ_ADAM, BLOCKSIZE, bq.BQ_F16, arrays[t % 2],
-                                     dict(hp, step=t), qs_d, qu_d, stream=stream)
+        def step(i):
+            bq.bq_optimizer8bit_step(opt, B, gdt, arrays[i % 2], dict(hp, step=i + 1), qs_d,
+                                     q2, stream=stream)
 
-    log(f"warmup {args.warmup} steps")
-    t = 1
-    for _ in range(args.warmup):
-        step(t)
-        t += 1
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    log(f"timing {args.steps} steps")
-    start.record(stream)
-    for _ in range(args.steps):
-        step(t)
-        t += 1
-    stop.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
-    sec = ms / 1e3
-    gbs = bytes_step / sec / 1e9
-    res = {
-        "metric": METRIC,
-        "value": nparams / sec,
-        "unit": "params/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic (seeded torch Philox on the GPU; shapes of a 48-layer GPT-2-style LM)",
-        "config": {
-            "workload": "8-bit Adam, 1.5B-param LM-shaped list: 48 layers, d=1600, ffn 6400, "
-                        "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4) "
-                        "with 0.01% outliers x1000, blocksize 2048",
-            "tensors": len(specs), "params": nparams, "blocksize": BLOCKSIZE,
-            "grad_dtype": "fp16", "state_dtype": "u8", "path": args.path,
-        },
+    log(f"warmup {args.warmup} steps, timing {args.steps} steps")
+    ms, seg = timed(torch, stream, step, args.steps, args.warmup, 1)
+    gbs = bytes_step / (ms / 1e3) / 1e9
+    tag = {"adam": "Adam", "adamw": "AdamW", "momentum": "Momentum"}[opt_name]
+    metric = METRIC if headline else (
+        f"8-bit {tag} step params/sec and achieved HBM GB/s (% of peak), {args.workload} list")
+    res = base_record(
+        args, metric, nparams / (ms / 1e3), "params/s", ms, seg, "f32",
+        f"synthetic (seeded torch Philox on the GPU; shapes of the {args.workload} list)",
+        {"workload": f"{desc}, blocksize {B}", "tensors": len(specs), "params": nparams,
+         "blocksize": B, "grad_dtype": "fp16" if gdt == bq.BQ_F16 else "fp32",
+         "state_dtype": "u8", "path": args.path})
+    kname = (f"step_oneshot_kernel<{tag}, {'fp16' if gdt == bq.BQ_F16 else 'fp32'} grad, {B}>"
+             if args.path == "plan" else f"step_kernel<{tag}> (persistent, call path)")
+    res.update({
         "gbs": gbs,
         "hbm_frac": gbs / HBM_PEAK_GBS,
         "roofline": {
             "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
+            "frac": gbs / HBM_PEAK_GBS,
+            "traffic": measured_traffic(args.workload, B, args.path),
             "bytes_per_step": bytes_step,
-            "kernel": "step_oneshot_kernel<Adam, fp16 grad, 2048> (+ prepare_kernel, ~10 us, "
-                      "inside the timed launch pair)",
+            "kernel": kname + (" (+ prepare_kernel, ~10 us, inside the timed launch pair)"
+                               if args.path == "plan" else ""),
         },
         "stream_ceiling": None if ceiling is None else {
             "gbs": ceiling, "frac_of_peak": ceiling / HBM_PEAK_GBS,
@@ -304,7 +346,116 @@ def main():
                     "shapes in libbq_stream.so",
         },
         "cpu_baseline": cpu,
-    }
+    })
+    return res
+
+
+def run_quant(args, torch, bq, workloads):
+    """Standalone quantize or dequantize of 67,108,864 Student-t(3) x 1e-2
+    values; four input / output buffer sets rotate so that no call finds its
+    operands in the 256 MB last-level cache."""
+    B = args.blocksize
+    n = QUANT_N
+    nb = (n + B - 1) // B
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    qs_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)).cuda()
+    prepared = bq.bq_prepare_codebook(qs_d)
+    log("generating the Student-t input on the host")
+    x_h = torch.from_numpy(workloads.student_t_host(n, seed=0))
+    xs = [x_h.to(dev) for _ in range(QUANT_BUFFERS)]
+    codes = [torch.empty(n, dtype=torch.uint8, device=dev) for _ in range(QUANT_BUFFERS)]
+    absmax = [torch.empty(nb, dtype=torch.float32, device=dev) for _ in range(QUANT_BUFFERS)]
+    outs = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(QUANT_BUFFERS)]
+    stream = torch.cuda.current_stream()
+    for k in range(QUANT_BUFFERS):
+        bq.bq_quantize_blockwise_prepared(prepared, xs[k], B, codes[k], absmax[k], stream=stream)
+    torch.cuda.synchronize()
+    L = bq.lib()
+    path = args.path if args.workload == "quantize" else "call"
+    if args.workload == "quantize":
+        if args.path == "plan":
+            pp = prepared.data_ptr()
+            args_k = [(pp, xs[k].data_ptr(), n, B, codes[k].data_ptr(), absmax[k].data_ptr(),
+                       stream.cuda_stream) for k in range(QUANT_BUFFERS)]
+
+            def call(i):
+                if L.bq_quantize_blockwise_prepared(*args_k[i % QUANT_BUFFERS]) != 0:
+                    raise RuntimeError("bq_quantize_blockwise_prepared failed")
+            kname = f"quantize_oneshot_kernel<{B}> (prepared codebook)"
+        else:
+            qp = qs_d.data_ptr()
+            args_k = [(qp, xs[k].data_ptr(), n, B, codes[k].data_ptr(), absmax[k].data_ptr(),
+                       stream.cuda_stream) for k in range(QUANT_BUFFERS)]
+
+            def call(i):
+                if L.bq_quantize_blockwise(*args_k[i % QUANT_BUFFERS]) != 0:
+                    raise RuntimeError("bq_quantize_blockwise failed")
+            kname = f"quantize_kernel<{B}> (persistent, raw codebook)"
+        what = "block-wise quantize"
+    else:
+        qp = qs_d.data_ptr()
+        args_k = [(qp, codes[k].data_ptr(), absmax[k].data_ptr(), n, B, outs[k].data_ptr(),
+                   stream.cuda_stream) for k in range(QUANT_BUFFERS)]
+
+        def call(i):
+            if L.bq_dequantize_blockwise(*args_k[i % QUANT_BUFFERS]) != 0:
+                raise RuntimeError("bq_dequantize_blockwise failed")
+        kname = "dequantize_kernel"
+        what = "block-wise dequantize"
+    steps = args.steps * 20
+    warmup = args.warmup * 4
+    log(f"warmup {warmup} calls, timing {steps} calls")
+    ms, seg = timed(torch, stream, call, steps, warmup, 20)
+    nbytes = n * 5 + nb * 4
+    gbs = nbytes / (ms / 1e3) / 1e9
+    res = base_record(
+        args, f"{what} elements/sec and achieved HBM GB/s (% of peak), 67M Student-t values",
+        n / (ms / 1e3), "elements/s", ms, seg, "f32",
+        "synthetic (numpy PCG64 Student-t(3) x 1e-2, seed 0; four rotating buffer sets)",
+        {"workload": f"{what}, signed dynamic map, n = {n}, blocksize {B}", "elements": n,
+         "blocksize": B, "path": path})
+    res["steps"] = steps
+    res["warmup"] = warmup
+    res.update({
+        "gbs": gbs, "hbm_frac": gbs / HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(args.workload, B, path), "bytes_per_step": nbytes,
+                     "kernel": kname},
+        "stream_ceiling": None, "cpu_baseline": None,
+    })
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="lm1p5b-adam",
+                    choices=list(LIST_WORKLOADS) + ["quantize", "dequantize"])
+    ap.add_argument("--blocksize", type=int, default=BLOCKSIZE)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stream-ceiling", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=16)
+    ap.add_argument("--path", choices=["plan", "call"], default="plan",
+                    help="plan: bq_step_plan_run (one launch over the whole list) or, for "
+                         "quantize, the prepared codebook; call: bq_optimizer8bit_step "
+                         "(descriptor chunks of 56 tensors) or bq_quantize_blockwise")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the 8-bit step has no cross-GPU exchange, and "
+              "this build runs on a single MI355X (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2110_02861_amd import bq, workloads
+
+    if args.workload in LIST_WORKLOADS:
+        res = run_list(args, torch, bq, workloads)
+    else:
+        res = run_quant(args, torch, bq, workloads)
     print(json.dumps(res), flush=True)
 
 

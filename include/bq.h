@@ -167,7 +167,9 @@ bq_status bq_quantize_blockwise(const float *qmap, const float *x, int64_t n,
  *   codes  device, n uint8 (read)
  *   absmax device, ceil(n / blocksize) fp32 (read)
  *   out    device, n fp32 (written)
- * Errors: BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_BLOCKSIZE, BQ_ERR_ALIGN, BQ_ERR_HIP.
+ * One workgroup per tile of 4096 elements.
+ * Errors: BQ_ERR_NULL, BQ_ERR_SIZE (n < 0, or more than 8,388,607 tiles),
+ * BQ_ERR_BLOCKSIZE, BQ_ERR_ALIGN, BQ_ERR_HIP.
  */
 bq_status bq_dequantize_blockwise(const float *qmap, const uint8_t *codes,
                                   const float *absmax, int64_t n, int32_t blocksize,
@@ -257,7 +259,7 @@ bq_status bq_optimizer32bit_step(bq_optimizer opt, bq_dtype grad_dtype,
  * The calls above build a codebook's decision tables inside every persistent
  * workgroup, because they receive nothing but the raw map.  The calls below
  * keep those tables in caller-visible device memory, so that every tile can
- * run as its own short-lived workgroup (512 threads; 2048 elements for the
+ * run as its own short-lived workgroup (512 threads; 8192 elements for the
  * quantize call, 4096 for the step), which streams HBM markedly faster on
  * MI355X.  Codes and absmax are identical to the calls above, bit for bit.
  * ------------------------------------------------------------------------ */
@@ -277,7 +279,7 @@ bq_status bq_prepare_codebook(const float *qmap, void *prepared, hipStream_t str
 
 /*
  * bq_quantize_blockwise with a prepared codebook (Section 3.1, Eq. 4); same
- * arguments and results, one workgroup per tile.
+ * arguments and results, one workgroup per tile of 8192 elements.
  * Errors: BQ_ERR_NULL, BQ_ERR_SIZE (n < 0, or more than 8,388,607 tiles),
  * BQ_ERR_BLOCKSIZE, BQ_ERR_ALIGN, BQ_ERR_HIP.
  */

@@ -230,7 +230,7 @@ bq_status bq_dequantize_blockwise(const float *qmap, const uint8_t *codes, const
         return BQ_ERR_NULL;
     if (!aligned(codes, 16) || !aligned(out, 16) || !aligned(absmax, 4) || !aligned(qmap, 4))
         return BQ_ERR_ALIGN;
-    if ((n + 2047) / 2048 > kMaxOneShotTiles)
+    if ((n + bq::dequant_tile() - 1) / bq::dequant_tile() > kMaxOneShotTiles)
         return BQ_ERR_SIZE;
     return from_hip(bq::launch_dequantize(qmap, codes, absmax, n, blocksize, out, stream));
 }
@@ -389,7 +389,7 @@ bq_status bq_quantize_blockwise_prepared(const void *prepared, const float *x, i
         return BQ_ERR_NULL;
     if (!aligned(prepared, 16) || !aligned(x, 16) || !aligned(codes, 16) || !aligned(absmax, 4))
         return BQ_ERR_ALIGN;
-    const int64_t tile = bq::tile_elems(blocksize);
+    const int64_t tile = bq::quant_tile(blocksize);
     if ((n + tile - 1) / tile > kMaxOneShotTiles)
         return BQ_ERR_SIZE;
     return from_hip(bq::launch_quantize_prepared(static_cast<const uint8_t *>(prepared), x, n,

@@ -58,6 +58,19 @@ static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must stay below 4
 // persistent kernels and the one-shot quantize kernel.
 constexpr int tile_elems(int blocksize) { return blocksize >= 2048 ? blocksize : 2048; }
 
+// Elements per tile of the prepared-codebook quantize kernel: kQuantChunks
+// chunks of 2048 (512 threads x 4 elements), or one block when the block is
+// larger; of the dequantize kernel: kDequantChunks chunks of 2048.  (Measured
+// on MI355X at 67M elements: quantize streams best with 4 chunks, dequantize,
+// whose traffic is mostly writes, with 2.)
+constexpr int kQuantChunks = 4;
+constexpr int kDequantChunks = 2;
+constexpr int quant_tile(int blocksize)
+{
+    return 2048 * (blocksize > 2048 * kQuantChunks ? blocksize / 2048 : kQuantChunks);
+}
+constexpr int dequant_tile() { return 2048 * kDequantChunks; }
+
 // Elements per tile of the one-shot step kernel: 512 threads x 4 elements per
 // chunk, kStepChunks chunks (two for 4096 blocks, which must fit one tile).
 constexpr int kStepChunks = 2;

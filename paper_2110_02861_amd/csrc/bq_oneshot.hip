@@ -1,6 +1,7 @@
-// One-shot kernels for gfx950: one workgroup of 512 threads per tile of 2048
-// elements (or per 4096 block), 4 contiguous elements per thread and chunk,
-// wave-contiguous non-temporal loads and stores.  The decision tables of each
+// One-shot kernels for gfx950: one workgroup of 512 threads per tile, chunks
+// of 2048 elements with 4 contiguous elements per thread, wave-contiguous
+// non-temporal loads and stores (4096-element tiles for the step, 8192 for
+// quantize, 4096 for dequantize).  The decision tables of each
 // codebook are built once per call by prepare_kernel into a prepared-codebook
 // buffer and copied from there (L2) into LDS by every workgroup.
 //
@@ -17,56 +18,36 @@ using namespace dev;
 constexpr int kOS = 512;  // threads per workgroup
 constexpr int kOSWaves = kOS / 64;
 
-template <int B>
-struct OSShape {
-    static constexpr int CHUNKS = B == 4096 ? 2 : 1;        // chunks of 4 per thread
-    static constexpr int EPT = 4 * CHUNKS;                   // elements per thread
-    static constexpr int TILE = kOS * EPT;                   // elements per workgroup
-    static constexpr int GROUP = B >= 2048 ? kOS : B / 4;    // threads per block
-    static_assert(TILE == tile_elems(B), "tile size");
-};
-
 // ---------------------------------------------------------------------------
 // Prepare: decision tables of 1 or 2 maps (one workgroup each)
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(256) void prepare_kernel(const float *__restrict__ q1,
-                                                      const float *__restrict__ q2,
-                                                      uint8_t *__restrict__ out)
+// kPrepThreads threads per map: each walks ceil(3328 / kPrepThreads) buckets
+// of each sign, a chain of dependent LDS reads that sets the kernel's length.
+constexpr int kPrepThreads = 1024;
+
+__global__ __launch_bounds__(kPrepThreads) void prepare_kernel(const float *__restrict__ q1,
+                                                               const float *__restrict__ q2,
+                                                               uint8_t *__restrict__ out)
 {
     __shared__ float q[256];
     __shared__ float t[256];
     __shared__ __attribute__((aligned(16))) uint8_t base[2 * kBuckets];
     __shared__ int kmax;
     const float *qm = blockIdx.x == 0 ? q1 : q2;
-    build_tables<256>(qm, q, t, base, &kmax);
+    build_tables<kPrepThreads>(qm, q, t, base, &kmax);
     uint8_t *dst = out + (size_t)blockIdx.x * kPreparedBytes;
     const int j = threadIdx.x;
-    reinterpret_cast<float *>(dst + kPreparedOffQ)[j] = q[j];
-    reinterpret_cast<float *>(dst + kPreparedOffT)[j] = t[j];
+    if (j < 256) {
+        reinterpret_cast<float *>(dst + kPreparedOffQ)[j] = q[j];
+        reinterpret_cast<float *>(dst + kPreparedOffT)[j] = t[j];
+    }
     const uint32_t *bs = reinterpret_cast<const uint32_t *>(base);
     uint32_t *bd = reinterpret_cast<uint32_t *>(dst + kPreparedOffBase);
-    for (int i = j; i < (int)(2 * kBuckets / 4); i += 256)
+    for (int i = j; i < (int)(2 * kBuckets / 4); i += kPrepThreads)
         bd[i] = bs[i];
     if (j == 0)
         *reinterpret_cast<int *>(dst + kPreparedOffKmax) = kmax;
-}
-
-// Copy `bytes` (a multiple of 16) of a prepared map into LDS.
-__device__ inline void copy_granules(uint8_t *lds, const uint8_t *__restrict__ src, int bytes)
-{
-    for (int i = threadIdx.x; i < bytes / 16; i += blockDim.x)
-        reinterpret_cast<vu4 *>(lds)[i] = reinterpret_cast<const vu4 *>(src)[i];
-}
-
-__device__ inline Tables tables_at(const uint8_t *lds, int kmax)
-{
-    Tables M;
-    M.q = reinterpret_cast<const float *>(lds + kPreparedOffQ);
-    M.t = reinterpret_cast<const float *>(lds + kPreparedOffT);
-    M.base = lds + kPreparedOffBase;
-    M.kmax = kmax;
-    return M;
 }
 
 __device__ inline int prepared_kmax(const uint8_t *tables)
@@ -621,6 +602,31 @@ __global__ __launch_bounds__(256) void trust_ratio_kernel(const PlanArgs a, int 
 // Block-wise quantize with a prepared map, one tile per workgroup
 // ---------------------------------------------------------------------------
 
+// Tile of quant_tile(B) elements: C chunks of 2048, chunk c of thread t at
+// tile element 2048 c + 4 t, so that segment s = 8 c + wave covers tile
+// elements [256 s, 256 s + 256) and block b of the tile is made of segments
+// [b B / 256, (b + 1) B / 256), as in the step.
+template <int B>
+struct QuantOS {
+    static constexpr int TILE = quant_tile(B);
+    static constexpr int C = TILE / 2048;      // chunks per thread
+    static constexpr int N = 4 * C;            // elements per thread
+    static constexpr int kBPT = TILE / B;      // blocks per tile
+    static constexpr int kSPB = B / 256;       // segments per block
+    static_assert(kBPT <= 64, "one lane of wave 0 per block");
+};
+
+// Only the thresholds and both bucket halves are copied (the map values
+// themselves are not needed to find a code), placed so that the bucket
+// table starts at LDS byte kBucketLo, as in the step.
+// In front of them: one max slot and one BlockNorm per block of the tile.
+constexpr int kQuantGran = (kPreparedSignedBytes - kPreparedOffT) / 16;   // 480
+constexpr int kLdsQSlots = 0;                                             // uint32 [64]
+constexpr int kLdsQNorms = 64 * 4;                                        // BlockNorm [64]
+constexpr int kLdsQuantBytes = kLdsMap1 + kPreparedSignedBytes;
+static_assert(kQuantGran <= kOS, "one granule per thread");
+static_assert(kLdsQNorms + 64 * (int)sizeof(BlockNorm) <= kLdsMap1, "LDS layout");
+
 template <int B>
 __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__restrict__ tables,
                                                                const float *__restrict__ x,
@@ -628,15 +634,21 @@ __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__
                                                                uint8_t *__restrict__ codes,
                                                                float *__restrict__ absmax)
 {
-    using S = OSShape<B>;
-    constexpr int C = S::CHUNKS;
-    constexpr int N = S::EPT;
-    __shared__ __attribute__((aligned(16))) uint8_t lds[kPreparedSignedBytes];
-    __shared__ float2 slots[kOSWaves];
-
+    using S = QuantOS<B>;
+    constexpr int C = S::C;
+    constexpr int N = S::N;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsQuantBytes];
+    uint32_t *slots = reinterpret_cast<uint32_t *>(lds + kLdsQSlots);
+    BlockNorm *norms = reinterpret_cast<BlockNorm *>(lds + kLdsQNorms);
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
     const int64_t t0 = (int64_t)blockIdx.x * S::TILE;
     const bool full = t0 + S::TILE <= n;
-    const int tid = threadIdx.x;
+
+    // this thread's table granule (L2) first, then the tile's HBM loads
+    vu4 gran = {0u, 0u, 0u, 0u};
+    if (tid < kQuantGran)
+        gran = G(reinterpret_cast<const vu4 *>(tables + kPreparedOffT))[tid];
     float v[N];
     int valid[C];
 #pragma unroll
@@ -653,69 +665,138 @@ __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__
         } else {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                v[4 * c + r] = r < valid[c] ? x[e + r] : 0.0f;
+                v[4 * c + r] = r < valid[c] ? G(x)[e + r] : 0.0f;
         }
     }
-    copy_granules(lds, tables, kPreparedSignedBytes);
-    const Tables T = tables_at(lds, prepared_kmax(tables));
+    const int km = prepared_kmax(tables);
+    if (tid < kQuantGran)
+        reinterpret_cast<vu4 *>(lds + kLdsMap1 + kPreparedOffT)[tid] = gran;
+    if (tid < S::kBPT)
+        slots[tid] = 0u;
     __syncthreads();
 
-    float mx = 0.0f;
+    // block absmax: row max by DPP, one LDS max per row into the block's slot
 #pragma unroll
-    for (int i = 0; i < N; ++i)
-        mx = fmaxf(mx, fabsf(v[i]));
-    const float A = group_max<S::GROUP>(make_float2(mx, 0.0f), slots).x;
-    uint32_t c[N];
-    requantize<N, S::GROUP, false>(T, A, v, c);
+    for (int c = 0; c < C; ++c) {
+        float mx = 0.0f;
 #pragma unroll
-    for (int k = 0; k < C; ++k) {
-        const int64_t e = t0 + k * (kOS * 4) + tid * 4;
+        for (int r = 0; r < 4; ++r)
+            mx = fmaxf(mx, fabsf(v[4 * c + r]));
+        const uint32_t u = row_umax(__float_as_uint(mx));
+        if ((tid & 15) == 0)
+            atomicMax(&slots[(8 * c + wave) / S::kSPB], u);
+    }
+    __syncthreads();
+    if (tid < S::kBPT) {
+        const float A = __uint_as_float(slots[tid]);
+        norms[tid] = block_norm(A);
+        if (full || t0 + (int64_t)tid * B < n)
+            G(absmax)[t0 / B + tid] = A;
+    }
+    __syncthreads();
+
+    Tables T;
+    T.q = nullptr;  // not copied: finding a code reads only t and base
+    T.t = reinterpret_cast<const float *>(lds + kLdsMap1 + kPreparedOffT);
+    T.base = lds + kLdsMap1 + kPreparedOffBase;
+    T.kmax = km;
+    BlockNorm nb[C];
+    bool plain = km == 1;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        nb[c] = norms[(8 * c + wave) / S::kSPB];
+        plain = plain &&
+                __builtin_amdgcn_readfirstlane(__float_as_int(nb[c].s)) == __float_as_int(1.0f);
+    }
+    uint32_t q[N];
+    if (plain) {
+        float y[N];
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            y[i] = normalize_plain(nb[i / 4], v[i]);
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            q[i] = T.base[bucket_of<false>(y[i])];
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            q[i] += (y[i] >= T.t[q[i]]) ? 1u : 0u;
+    } else {
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const float vc[4] = {v[4 * c], v[4 * c + 1], v[4 * c + 2], v[4 * c + 3]};
+            uint32_t qc[4];
+            requantize_norm<4, false>(T, nb[c], vc, qc);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                q[4 * c + r] = qc[r];
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int64_t e = t0 + c * (kOS * 4) + tid * 4;
         if (full) {
             st_nt(reinterpret_cast<uint32_t *>(codes + e),
-                  c[4 * k] | (c[4 * k + 1] << 8) | (c[4 * k + 2] << 16) | (c[4 * k + 3] << 24));
+                  q[4 * c] | (q[4 * c + 1] << 8) | (q[4 * c + 2] << 16) | (q[4 * c + 3] << 24));
         } else {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                if (r < valid[k])
-                    codes[e + r] = (uint8_t)c[4 * k + r];
+                if (r < valid[c])
+                    G(codes)[e + r] = (uint8_t)q[4 * c + r];
         }
     }
-    const int64_t first = t0 + tid * 4;
-    if (first < n && (tid % S::GROUP) == 0)
-        absmax[first / B] = A;
 }
 
 // ---------------------------------------------------------------------------
 // Block-wise dequantize: out = q[code] * absmax, one tile per workgroup
 // ---------------------------------------------------------------------------
 
+// Tile of kDequantChunks chunks of 2048 elements laid out as in quantize; the 256
+// elements of one wave and chunk lie in one block (B >= 256), so the wave reads
+// that block's absmax once.
 __global__ __launch_bounds__(kOS) void dequantize_kernel(const float *__restrict__ qmap,
                                                          const uint8_t *__restrict__ codes,
                                                          const float *__restrict__ absmax,
                                                          int64_t n, int log2_blocksize,
                                                          float *__restrict__ out)
 {
+    constexpr int C = kDequantChunks;
+    constexpr int TILE = dequant_tile();
+    static_assert(TILE == kOS * 4 * C, "tile size");
     __shared__ float q[256];
     const int tid = threadIdx.x;
-    const int64_t e = (int64_t)blockIdx.x * (kOS * 4) + tid * 4;
-    uint32_t k = 0;
-    float A = 0.0f;
-    const bool full = e + 4 <= n;
+    const int wave = tid >> 6;
+    const int64_t t0 = (int64_t)blockIdx.x * TILE;
+    const bool full = t0 + TILE <= n;
+    uint32_t k[C];
+    float A[C];
     if (full) {
-        k = ld_nt(reinterpret_cast<const uint32_t *>(codes + e));
-        A = absmax[e >> log2_blocksize];   // blocksize >= 256: 4 elements, one block
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            k[c] = ld_nt(reinterpret_cast<const uint32_t *>(codes + e));
+            const int seg = __builtin_amdgcn_readfirstlane(8 * c + wave);
+            A[c] = G(absmax)[(t0 + (int64_t)seg * 256) >> log2_blocksize];
+        }
     }
     if (tid < 256)
-        q[tid] = qmap[tid];
+        q[tid] = G(qmap)[tid];
     __syncthreads();
     if (full) {
-        const vf4 y = {q[k & 0xffu] * A, q[(k >> 8) & 0xffu] * A, q[(k >> 16) & 0xffu] * A,
-                       q[k >> 24] * A};
-        st_nt(reinterpret_cast<vf4 *>(out + e), y);
-    } else if (e < n) {
-        const float Ap = absmax[e >> log2_blocksize];
-        for (int64_t i = e; i < n; ++i)
-            out[i] = q[codes[i]] * Ap;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            const vf4 y = {q[k[c] & 0xffu] * A[c], q[(k[c] >> 8) & 0xffu] * A[c],
+                           q[(k[c] >> 16) & 0xffu] * A[c], q[k[c] >> 24] * A[c]};
+            st_nt(reinterpret_cast<vf4 *>(out + e), y);
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            for (int r = 0; r < 4; ++r)
+                if (e + r < n)
+                    G(out)[e + r] = q[G(codes)[e + r]] * G(absmax)[(e + r) >> log2_blocksize];
+        }
     }
 }
 
@@ -751,7 +832,7 @@ template <int B>
 hipError_t launch_qp_t(const uint8_t *tables, const float *x, int64_t n, uint8_t *codes,
                        float *absmax, hipStream_t s)
 {
-    const int64_t tiles = (n + OSShape<B>::TILE - 1) / OSShape<B>::TILE;
+    const int64_t tiles = (n + quant_tile(B) - 1) / quant_tile(B);
     hipLaunchKernelGGL((quantize_oneshot_kernel<B>), dim3((unsigned)tiles), dim3(kOS), 0, s,
                        tables, x, n, codes, absmax);
     return hipGetLastError();
@@ -763,7 +844,7 @@ hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *table
                           hipStream_t stream)
 {
     const unsigned maps = qmap2 ? 2u : 1u;
-    hipLaunchKernelGGL(prepare_kernel, dim3(maps), dim3(256), 0, stream, qmap1,
+    hipLaunchKernelGGL(prepare_kernel, dim3(maps), dim3(kPrepThreads), 0, stream, qmap1,
                        qmap2 ? qmap2 : qmap1, tables);
     return hipGetLastError();
 }
@@ -823,7 +904,7 @@ hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const Pla
 hipError_t launch_dequantize(const float *qmap, const uint8_t *codes, const float *absmax,
                              int64_t n, int blocksize, float *out, hipStream_t stream)
 {
-    const int64_t tiles = (n + kOS * 4 - 1) / (kOS * 4);
+    const int64_t tiles = (n + dequant_tile() - 1) / dequant_tile();
     int lg = 0;
     while ((1 << lg) < blocksize)
         ++lg;

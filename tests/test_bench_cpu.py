@@ -1,0 +1,45 @@
+"""Host logic of bench.py: the algorithmic byte model and the one-GPU guard."""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+import bench
+from paper_2110_02861_amd import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_byte_model_of_the_lists():
+    # 1.5B list, Adam, fp16 grads, B = 2048: 14 B per param + 16 B per block
+    c5 = [s.numel for s in workloads.lm_1p5b_specs()]
+    assert sum(c5) == 1_557_611_200
+    assert bench.step_bytes(c5, 2048, 2, 2) == 21_818_727_840
+    # ResNet-50 list, Momentum, fp32 grads: 4 + 4 + 4 + 2 B per param + 8 B per block
+    c3 = [s.numel for s in workloads.resnet50_specs()]
+    nb = sum((k + 2047) // 2048 for k in c3)
+    assert nb == 12_560
+    assert bench.step_bytes(c3, 2048, 4, 1) == 14 * sum(c3) + 8 * nb
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_recorded_counter_traffic_matches_the_byte_model():
+    """The FETCH / WRITE counters recorded for each dominant kernel read within
+    2 % of its algorithmic bytes (every byte moved once)."""
+    c5 = [s.numel for s in workloads.lm_1p5b_specs()]
+    algorithmic = {
+        ("lm1p5b-adam", 2048, "plan"): bench.step_bytes(c5, 2048, 2, 2),
+        ("quantize", 2048, "plan"): bench.QUANT_N * 5 + bench.QUANT_N // 2048 * 4,
+        ("dequantize", 2048, "call"): bench.QUANT_N * 5 + bench.QUANT_N // 2048 * 4,
+    }
+    assert set(algorithmic) == set(bench.MEASURED_TRAFFIC)
+    for key, m in bench.MEASURED_TRAFFIC.items():
+        t = m["fetch_kib"] * 1024 * bench.FETCH_SCALE + m["write_kib"] * 1024 * bench.WRITE_SCALE
+        assert 0.99 < t / algorithmic[key] < 1.02, key

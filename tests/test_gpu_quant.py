@@ -37,14 +37,16 @@ def run_pair(qmap_h, qmap_d, x, B):
 @pytest.mark.parametrize("B", BLOCKSIZES)
 def test_ragged_multi_tile(B):
     qs, qu, qs_d, qu_d = codebooks_on_device()
-    tile = max(B, 2048)
-    n = 7 * tile + 1234          # several tiles and a ragged tail
-    x = workloads.student_t_host(n, seed=B)
-    run_pair(qs, qs_d, x, B)
-    run_pair(qu, qu_d, np.abs(x), B)
+    # several tiles of every kernel (2048 / 4096 / 8192 elements) and a
+    # ragged tail ending in the first, second and last chunk of a tile
+    for n in (7 * max(B, 2048) + 1234, 5 * 8192 + 2048 + 777, 3 * 8192 + 6144 + 3):
+        x = workloads.student_t_host(n, seed=B + n)
+        run_pair(qs, qs_d, x, B)
+        run_pair(qu, qu_d, np.abs(x), B)
 
 
-@pytest.mark.parametrize("n", [1, 7, 255, 256, 257, 2047, 2048, 2049, 4095, 4097, 10000])
+@pytest.mark.parametrize("n", [1, 7, 255, 256, 257, 2047, 2048, 2049, 4095, 4097, 8191, 8192,
+                               8193, 10000, 16383, 16385])
 def test_edge_lengths(n):
     qs, _, qs_d, _ = codebooks_on_device()
     x = workloads.student_t_host(n, seed=n)
