@@ -5,7 +5,7 @@ list (prepare both codebooks' decision tables, then dequantize states, fp32
 Adam update, block absmax, requantize), with the params, fp16 grads and 8-bit
 states already resident in HBM.  By default the step goes through a step plan
 (bq_step_plan_run: one launch over all 580 tensors); --path call uses
-bq_optimizer8bit_step.
+bq_optimizer8bit_step, --path optim the drop-in torch optimizer.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
                     [--workload lm1p5b-adam|gpt2m-adamw|resnet50-momentum|
@@ -301,7 +301,26 @@ def run_list(args, torch, bq, workloads):
     q2 = qu_d if nstates == 2 else None
 
     # a ring of two gradient buffers, one plan (or descriptor array) for each
-    if args.path == "plan":
+    if args.path == "optim":
+        from paper_2110_02861_amd import optim
+        del states, rows
+        torch.cuda.empty_cache()
+        ps = [torch.nn.Parameter(w) for w in params]
+        for p in ps:
+            p.grad_dtype = None  # fp16 grads on fp32 params
+        if opt_name == "momentum":
+            opt_obj = optim.SGD8bit(ps, lr=hp["lr"], momentum=hp["beta1"],
+                                    weight_decay=hp["wd"], blocksize=B)
+        else:
+            cls = optim.Adam8bit if opt_name == "adam" else optim.AdamW8bit
+            opt_obj = cls(ps, lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
+                          weight_decay=hp["wd"], blocksize=B)
+
+        def step(i):
+            for p, g in zip(ps, grads[i % 2]):
+                p.grad = g
+            opt_obj.step()
+    elif args.path == "plan":
         plans = [bq.StepPlan(opt, B, gdt, r) for r in rows]
 
         def step(i):
@@ -326,7 +345,9 @@ def run_list(args, torch, bq, workloads):
          "blocksize": B, "grad_dtype": "fp16" if gdt == bq.BQ_F16 else "fp32",
          "state_dtype": "u8", "path": args.path})
     kname = (f"step_oneshot_kernel<{tag}, {'fp16' if gdt == bq.BQ_F16 else 'fp32'} grad, {B}>"
-             if args.path == "plan" else f"step_kernel<{tag}> (persistent, call path)")
+             if args.path != "call" else f"step_kernel<{tag}> (persistent, call path)")
+    if args.path == "optim":
+        kname += f" via optim.{type(opt_obj).__name__}.step()"
     res.update({
         "gbs": gbs,
         "hbm_frac": gbs / HBM_PEAK_GBS,
@@ -335,8 +356,8 @@ def run_list(args, torch, bq, workloads):
             "frac": gbs / HBM_PEAK_GBS,
             "traffic": measured_traffic(args.workload, B, args.path),
             "bytes_per_step": bytes_step,
-            "kernel": kname + (" (+ prepare_kernel, ~10 us, inside the timed launch pair)"
-                               if args.path == "plan" else ""),
+            "kernel": kname + (" (+ prepare_kernel, ~7 us, inside the timed launch pair)"
+                               if args.path != "call" else ""),
         },
         "stream_ceiling": None if ceiling is None else {
             "gbs": ceiling, "frac_of_peak": ceiling / HBM_PEAK_GBS,
@@ -354,6 +375,9 @@ def run_quant(args, torch, bq, workloads):
     """Standalone quantize or dequantize of 67,108,864 Student-t(3) x 1e-2
     values; four input / output buffer sets rotate so that no call finds its
     operands in the 256 MB last-level cache."""
+    if args.path == "optim":
+        print("--path optim applies to the optimizer-step workloads", file=sys.stderr)
+        sys.exit(2)
     B = args.blocksize
     n = QUANT_N
     nb = (n + B - 1) // B
@@ -439,10 +463,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=16)
-    ap.add_argument("--path", choices=["plan", "call"], default="plan",
+    ap.add_argument("--path", choices=["plan", "call", "optim"], default="plan",
                     help="plan: bq_step_plan_run (one launch over the whole list) or, for "
                          "quantize, the prepared codebook; call: bq_optimizer8bit_step "
-                         "(descriptor chunks of 56 tensors) or bq_quantize_blockwise")
+                         "(descriptor chunks of 56 tensors) or bq_quantize_blockwise; optim: "
+                         "the drop-in torch optimizer (Adam8bit / AdamW8bit / SGD8bit) with "
+                         "the grads of the ring assigned to .grad before each step")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the 8-bit step has no cross-GPU exchange, and "

@@ -311,13 +311,16 @@ def bq_quantize_blockwise_prepared(prepared, x, blocksize: int, codes=None, absm
 class StepPlan:
     """bq_step_plan_create / bq_step_plan_run / bq_step_plan_destroy.
 
-    The plan holds device pointers to the given tensors; keep them alive (this
-    object keeps references) while the plan is used."""
+    The plan holds device pointers to the given tensors.  By default this
+    object keeps references to them, so they stay allocated while the plan
+    lives.  keep=False drops those references: the caller must then check,
+    before every run, that the same storages (pointers and sizes) are still
+    the live tensors (the drop-in optimizers do)."""
 
-    def __init__(self, opt, blocksize: int, grad_dtype: int, tensors):
+    def __init__(self, opt, blocksize: int, grad_dtype: int, tensors, keep: bool = True):
         if isinstance(opt, str):
             opt = OPTIMIZERS[opt]
-        self._keep = [t for row in tensors for t in row if t is not None]
+        self._keep = [t for row in tensors for t in row if t is not None] if keep else []
         arr = make_tensor_array(tensors)
         h = ctypes.c_void_p()
         _check(lib().bq_step_plan_create(int(opt), int(blocksize), int(grad_dtype), arr,

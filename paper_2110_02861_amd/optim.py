@@ -170,23 +170,26 @@ class Optimizer8bit(torch.optim.Optimizer):
         if not self.use_plans and self.OPT not in (bq.BQ_LAMB, bq.BQ_LARS):
             bq.bq_optimizer8bit_step(self.OPT, self.blocksize, gdt, rows, hp, q1, q2)
             return
-        # a plan holds device pointers: reuse it while every storage stays put
-        key = tuple(0 if t is None else t.data_ptr() for row in rows for t in row)
+        # A plan holds device pointers and is a function of them and the sizes
+        # alone: look it up by every storage pointer and size, so a plan runs
+        # only on the storages it was built for.  Plans keep no references to
+        # the tensors, so grads freed by zero_grad(set_to_none=True) can be
+        # reallocated at the same addresses (and the plan reused); several
+        # plans per param set serve alternating grad buffers.
+        key = (gdt, device.index)
+        key += tuple(0 if t is None else t.data_ptr() for row in rows for t in row)
         key += tuple(p.numel() for p in ps)
-        slot = (gi, gdt, device.index, tuple(id(p) for p in ps))
-        cached = self._plans.pop(slot, None)
-        if cached is None or cached[0] != key:
-            if cached is not None:
-                cached[1].close()
-            cached = (key, bq.StepPlan(self.OPT, self.blocksize, gdt, rows))
-        self._plans[slot] = cached  # most recently used last
+        plan = self._plans.pop(key, None)
+        if plan is None:
+            plan = bq.StepPlan(self.OPT, self.blocksize, gdt, rows, keep=False)
+        self._plans[key] = plan  # most recently used last
         while len(self._plans) > self.MAX_PLANS:
             oldest = next(iter(self._plans))
-            self._plans.pop(oldest)[1].close()
-        cached[1].run(hp, q1, q2)
+            self._plans.pop(oldest).close()
+        plan.run(hp, q1, q2)
 
     def load_state_dict(self, state_dict):
-        for _, plan in self._plans.values():
+        for plan in self._plans.values():
             plan.close()
         self._plans = {}
         super().load_state_dict(state_dict)

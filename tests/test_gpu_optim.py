@@ -250,6 +250,36 @@ def test_plans_follow_reallocated_grads():
         assert torch.all((pa - pb).abs() <= 1e-6 * pa.abs() + 1e-6 * upd)
 
 
+def test_alternating_grad_buffers_reuse_plans():
+    """Two grad buffer sets used in turn: one plan each, built once and reused,
+    and codes equal to the plan-free path at every step."""
+    params_a = init_params(5)
+    params_b = [torch.nn.Parameter(p.detach().clone()) for p in params_a]
+    opt_a = optim.Adam8bit(params_a, use_plans=True)
+    opt_b = optim.Adam8bit(params_b, use_plans=False)
+    ring = [[torch.from_numpy(g).cuda() for g in grads(5, r + 1, np.float16)] for r in range(2)]
+    for p in params_a + params_b:
+        p.grad_dtype = None
+    seen = {}
+    for t in range(1, 7):
+        for pa, pb, g in zip(params_a, params_b, ring[t % 2]):
+            pa.grad = g
+            pb.grad = g
+        say(f"optim alternating grads step {t}")
+        opt_a.step()
+        opt_b.step()
+        assert len(opt_a._plans) == min(t, 2)
+        for key, plan in opt_a._plans.items():
+            assert seen.setdefault(key, plan) is plan  # never rebuilt
+    torch.cuda.synchronize()
+    for pa, pb in zip(params_a, params_b):
+        sa, sb = opt_a.state[pa], opt_b.state[pb]
+        for k in ("state1", "absmax1", "state2", "absmax2"):
+            assert torch.equal(sa[k], sb[k]), k
+        upd = 1e-3 * torch.ones_like(pa)
+        assert torch.all((pa - pb).abs() <= 1e-6 * pa.abs() + 1e-6 * upd)
+
+
 def test_training_loop_reduces_loss():
     """A least-squares fit with 8-bit Adam: the loss falls by orders of magnitude."""
     torch.manual_seed(0)
