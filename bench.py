@@ -135,10 +135,11 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def setup_list(torch, bq, workloads, config, nstates, blocksize=BLOCKSIZE, seed=0):
+def setup_list(torch, bq, workloads, config, nstates, blocksize=BLOCKSIZE, seed=0, zero1=127):
     """Params, a ring of two grad buffers and zero 8-bit states for one of the
-    parameter lists, generated on the GPU.  Returns (specs, params, grads,
-    states, rows) with rows[r] the bq_tensor tuples that use grad buffer r."""
+    parameter lists, generated on the GPU (zero1: the code of 0 in state 1's
+    map).  Returns (specs, params, grads, states, rows) with rows[r] the
+    bq_tensor tuples that use grad buffer r."""
     specs = workloads.SPECS[config]()
     gdt = torch.float16 if workloads.GRADS[config][0] == "float16" else torch.float32
     dev = torch.device("cuda:0")
@@ -155,12 +156,12 @@ def setup_list(torch, bq, workloads, config, nstates, blocksize=BLOCKSIZE, seed=
             workloads.grad_device(config, s, g, seed, i, r)
             grads[r].append(g)
         if nstates == 2:
-            states.append((torch.full((n,), 127, dtype=torch.uint8, device=dev),
+            states.append((torch.full((n,), zero1, dtype=torch.uint8, device=dev),
                            torch.zeros(n, dtype=torch.uint8, device=dev),
                            torch.zeros(nb, dtype=torch.float32, device=dev),
                            torch.zeros(nb, dtype=torch.float32, device=dev)))
         else:
-            states.append((torch.full((n,), 127, dtype=torch.uint8, device=dev), None,
+            states.append((torch.full((n,), zero1, dtype=torch.uint8, device=dev), None,
                            torch.zeros(nb, dtype=torch.float32, device=dev), None))
     torch.cuda.synchronize()
     rows = [[(params[i], grads[r][i], states[i][0], states[i][1], states[i][2], states[i][3])
@@ -214,20 +215,44 @@ def cpu_baseline(specs, params, grads, layers, steps=6):
     }
 
 
+_LM = ("1.5B-param LM-shaped list: 48 layers, d=1600, ffn 6400, vocab 50257, ctx 1024; fp32 params "
+       "N(0,0.02), fp16 grads N(0,1e-4) with 0.01% outliers x1000")
 LIST_WORKLOADS = {
-    # name: (config, optimizer, states, description)
-    "lm1p5b-adam": ("c5", "adam", 2,
-                    "8-bit Adam, 1.5B-param LM-shaped list: 48 layers, d=1600, ffn 6400, "
-                    "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4) "
-                    "with 0.01% outliers x1000"),
-    "gpt2m-adamw": ("c4", "adamw", 2,
-                    "8-bit AdamW, GPT-2-medium-shaped list: 24 layers, d=1024, ffn 4096, "
-                    "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4), "
-                    "heavy-tailed embedding rows"),
-    "resnet50-momentum": ("c3", "momentum", 1,
-                          "8-bit Momentum, ResNet-50 v1.5 parameter list (161 tensors); conv/fc "
-                          "N(0, sqrt(2/fan_in)), BN 1/0, fp32 grads N(0,1e-3)"),
+    # name: config, optimizer, description, hyperparameters (None: the config's own),
+    # extra bytes of the per-tensor norm pass (per param, per block and state)
+    "lm1p5b-adam": dict(config="c5", opt="adam", desc="8-bit Adam, " + _LM, hp=None,
+                        norms=(0, 0)),
+    "gpt2m-adamw": dict(config="c4", opt="adamw", hp=None, norms=(0, 0),
+                        desc="8-bit AdamW, GPT-2-medium-shaped list: 24 layers, d=1024, ffn 4096, "
+                             "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4), "
+                             "heavy-tailed embedding rows"),
+    "resnet50-momentum": dict(config="c3", opt="momentum", hp=None, norms=(0, 0),
+                              desc="8-bit Momentum, ResNet-50 v1.5 parameter list (161 tensors); "
+                                   "conv/fc N(0, sqrt(2/fan_in)), BN 1/0, fp32 grads N(0,1e-3)"),
+    "lm1p5b-adagrad": dict(config="c5", opt="adagrad", desc="8-bit AdaGrad, " + _LM,
+                           hp=dict(lr=1e-2, beta1=0.0, beta2=0.0, eps=1e-10, wd=0.0),
+                           norms=(0, 0)),
+    # LAMB reads w, g and both states again for the norms of w and of the update
+    "lm1p5b-lamb": dict(config="c5", opt="lamb", desc="8-bit LAMB, " + _LM,
+                        hp=dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-6, wd=0.01),
+                        norms=(8, 4)),
+    # LARS reads w and g again for their norms
+    "lm1p5b-lars": dict(config="c5", opt="lars", desc="8-bit LARS, " + _LM,
+                        hp=dict(lr=0.1, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4, trust=1e-3),
+                        norms=(6, 0)),
 }
+
+
+def workload_bytes(name, numels, blocksize, grad_bytes):
+    """Algorithmic HBM bytes of one step of a list workload: the fused step's
+    bytes plus, for LAMB and LARS, the norm pass's reads."""
+    W = LIST_WORKLOADS[name]
+    nstates = 2 if W["opt"] in ("adam", "adamw", "lamb") else 1
+    nblocks = sum((k + blocksize - 1) // blocksize for k in numels)
+    return (step_bytes(numels, blocksize, grad_bytes, nstates) + sum(numels) * W["norms"][0]
+            + nblocks * W["norms"][1] * nstates)
+
+
 QUANT_N = 67_108_864
 QUANT_BUFFERS = 4
 
@@ -268,22 +293,28 @@ def base_record(args, metric, value, unit, ms, seg, dtype, data, config):
 
 
 def run_list(args, torch, bq, workloads):
-    config, opt_name, nstates, desc = LIST_WORKLOADS[args.workload]
+    W = LIST_WORKLOADS[args.workload]
+    config, opt_name, desc = W["config"], W["opt"], W["desc"]
     headline = args.workload == "lm1p5b-adam"
     B = args.blocksize
     opt = bq.OPTIMIZERS[opt_name]
+    nstates = 2 if opt_name in ("adam", "adamw", "lamb") else 1
     gdt_name = workloads.GRADS[config][0]
     gdt = bq.BQ_F16 if gdt_name == "float16" else bq.BQ_F32
     torch.cuda.set_device(0)
     qs_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)).cuda()
     qu_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)).cuda()
+    # AdaGrad's one state (a sum of squares) lives on the unsigned map
+    q1 = qu_d if opt_name == "adagrad" else qs_d
+    zero1 = 0 if opt_name == "adagrad" else 127
     log(f"allocating the {args.workload} list")
-    specs, params, grads, states, rows = setup_list(torch, bq, workloads, config, nstates, B)
+    specs, params, grads, states, rows = setup_list(torch, bq, workloads, config, nstates, B,
+                                                    zero1=zero1)
     numels = [s.numel for s in specs]
     nparams = sum(numels)
-    bytes_step = step_bytes(numels, B, 2 if gdt == bq.BQ_F16 else 4, nstates)
+    bytes_step = workload_bytes(args.workload, numels, B, 2 if gdt == bq.BQ_F16 else 4)
     C = getattr(workloads, config.upper())
-    hp = {k: C[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
+    hp = dict(W["hp"]) if W["hp"] else {k: C[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
 
     cpu = None
     if headline and not args.no_cpu_baseline:
@@ -299,6 +330,10 @@ def run_list(args, torch, bq, workloads):
 
     stream = torch.cuda.current_stream()
     q2 = qu_d if nstates == 2 else None
+    if args.path == "call" and opt_name in ("lamb", "lars"):
+        print("LAMB and LARS run through step plans only (--path plan or optim)",
+              file=sys.stderr)
+        sys.exit(2)
 
     # a ring of two gradient buffers, one plan (or descriptor array) for each
     if args.path == "optim":
@@ -311,8 +346,16 @@ def run_list(args, torch, bq, workloads):
         if opt_name == "momentum":
             opt_obj = optim.SGD8bit(ps, lr=hp["lr"], momentum=hp["beta1"],
                                     weight_decay=hp["wd"], blocksize=B)
+        elif opt_name == "adagrad":
+            opt_obj = optim.Adagrad8bit(ps, lr=hp["lr"], eps=hp["eps"], weight_decay=hp["wd"],
+                                        blocksize=B)
+        elif opt_name == "lars":
+            opt_obj = optim.Lars8bit(ps, lr=hp["lr"], momentum=hp["beta1"],
+                                     weight_decay=hp["wd"], trust_coefficient=hp["trust"],
+                                     blocksize=B)
         else:
-            cls = optim.Adam8bit if opt_name == "adam" else optim.AdamW8bit
+            cls = {"adam": optim.Adam8bit, "adamw": optim.AdamW8bit,
+                   "lamb": optim.Lamb8bit}[opt_name]
             opt_obj = cls(ps, lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
                           weight_decay=hp["wd"], blocksize=B)
 
@@ -324,18 +367,19 @@ def run_list(args, torch, bq, workloads):
         plans = [bq.StepPlan(opt, B, gdt, r) for r in rows]
 
         def step(i):
-            plans[i % 2].run(dict(hp, step=i + 1), qs_d, q2, stream=stream)
+            plans[i % 2].run(dict(hp, step=i + 1), q1, q2, stream=stream)
     else:
         arrays = [(bq.make_tensor_array(r), len(r)) for r in rows]
 
         def step(i):
-            bq.bq_optimizer8bit_step(opt, B, gdt, arrays[i % 2], dict(hp, step=i + 1), qs_d,
+            bq.bq_optimizer8bit_step(opt, B, gdt, arrays[i % 2], dict(hp, step=i + 1), q1,
                                      q2, stream=stream)
 
     log(f"warmup {args.warmup} steps, timing {args.steps} steps")
     ms, seg = timed(torch, stream, step, args.steps, args.warmup, 1)
     gbs = bytes_step / (ms / 1e3) / 1e9
-    tag = {"adam": "Adam", "adamw": "AdamW", "momentum": "Momentum"}[opt_name]
+    tag = {"adam": "Adam", "adamw": "AdamW", "momentum": "Momentum", "adagrad": "AdaGrad",
+           "lamb": "LAMB", "lars": "LARS"}[opt_name]
     metric = METRIC if headline else (
         f"8-bit {tag} step params/sec and achieved HBM GB/s (% of peak), {args.workload} list")
     res = base_record(
@@ -346,6 +390,8 @@ def run_list(args, torch, bq, workloads):
          "state_dtype": "u8", "path": args.path})
     kname = (f"step_oneshot_kernel<{tag}, {'fp16' if gdt == bq.BQ_F16 else 'fp32'} grad, {B}>"
              if args.path != "call" else f"step_kernel<{tag}> (persistent, call path)")
+    if opt_name in ("lamb", "lars"):
+        kname += " (+ norms_kernel and trust_ratio_kernel: the per-tensor norm pass)"
     if args.path == "optim":
         kname += f" via optim.{type(opt_obj).__name__}.step()"
     res.update({

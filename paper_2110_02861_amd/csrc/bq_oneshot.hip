@@ -492,13 +492,18 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
 // LAMB / LARS: per-tile partial squared norms, then per-tensor lr * ratio
 // ---------------------------------------------------------------------------
 
-// One workgroup per tile, the step kernel's tile shape.  Sums (in double) of
-// w^2 and of u^2 (LAMB: u = mhat / (sqrt(vhat) + eps) + wd w from the states
-// the step will compute) or g^2 (LARS, g before weight decay).
+// One workgroup per tile, the step kernel's tile shape and access pattern
+// (wave-contiguous 4-element chunks, non-temporal vector loads, all issued
+// before any arithmetic).  Sums (in double) of w^2 and of u^2 (LAMB: u =
+// mhat / (sqrt(vhat) + eps) + wd w from the states the step will compute) or
+// g^2 (LARS, g before weight decay); each thread sums its elements in order,
+// the waves by a fixed butterfly, the 8 wave sums in order.
 template <int OPT, int GRAD, int B>
 __global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
 {
     using K = StepOS<OPT, GRAD, B>;
+    constexpr int C = K::C;
+    constexpr bool kIsLamb = OPT == kLamb;
     __shared__ float q1[256], q2[256];
     __shared__ double red[kOSWaves][2];
     const int tid = threadIdx.x;
@@ -511,7 +516,69 @@ __global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
     const float *const a1 = dp->a1;
     const float *const a2 = dp->a2;
     const int64_t numel = dp->numel;
-    if constexpr (OPT == kLamb) {
+    const bool full = numel >= K::TILE;
+
+    float w[4 * C], g[4 * C];
+    uint32_t k1[C], k2[C];
+    int valid[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int64_t e0 = c * (kOS * 4) + tid * 4;
+        const int64_t rem = numel - e0;
+        valid[c] = rem <= 0 ? 0 : (rem >= 4 ? 4 : (int)rem);
+        if (full) {
+            const vf4 wv = ld_nt(reinterpret_cast<const vf4 *>(param + e0));
+            w[4 * c] = wv.x;
+            w[4 * c + 1] = wv.y;
+            w[4 * c + 2] = wv.z;
+            w[4 * c + 3] = wv.w;
+            if constexpr (GRAD == kF16) {
+                const vu2 gv =
+                    ld_nt(reinterpret_cast<const vu2 *>(static_cast<const _Float16 *>(grad) + e0));
+                g[4 * c] = half_lo(gv.x);
+                g[4 * c + 1] = half_hi(gv.x);
+                g[4 * c + 2] = half_lo(gv.y);
+                g[4 * c + 3] = half_hi(gv.y);
+            } else {
+                const vf4 gv =
+                    ld_nt(reinterpret_cast<const vf4 *>(static_cast<const float *>(grad) + e0));
+                g[4 * c] = gv.x;
+                g[4 * c + 1] = gv.y;
+                g[4 * c + 2] = gv.z;
+                g[4 * c + 3] = gv.w;
+            }
+            k1[c] = kIsLamb ? ld_nt(reinterpret_cast<const uint32_t *>(s1 + e0)) : 0u;
+            k2[c] = kIsLamb ? ld_nt(reinterpret_cast<const uint32_t *>(s2 + e0)) : 0u;
+        } else {
+            uint32_t b1 = 0, b2 = 0;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool ok = r < valid[c];
+                const int64_t e = e0 + r;
+                w[4 * c + r] = ok ? G(param)[e] : 0.0f;
+                if constexpr (GRAD == kF16)
+                    g[4 * c + r] = ok ? (float)G(static_cast<const _Float16 *>(grad))[e] : 0.0f;
+                else
+                    g[4 * c + r] = ok ? G(static_cast<const float *>(grad))[e] : 0.0f;
+                if constexpr (kIsLamb) {
+                    b1 |= (ok ? (uint32_t)G(s1)[e] : 0u) << (8 * r);
+                    b2 |= (ok ? (uint32_t)G(s2)[e] : 0u) << (8 * r);
+                }
+            }
+            k1[c] = b1;
+            k2[c] = b2;
+        }
+    }
+    // old absmax of the block of each chunk (wave-uniform, as in the step)
+    float n1[C], n2[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int b = (8 * c + wave) / K::kSPB;
+        const bool live = full || (int64_t)b * B < numel;
+        n1[c] = (kIsLamb && live) ? G(a1)[b] : 0.0f;
+        n2[c] = (kIsLamb && live) ? G(a2)[b] : 0.0f;
+    }
+    if constexpr (kIsLamb) {
         if (tid < 256) {
             q1[tid] = G(reinterpret_cast<const float *>(a.tables + kPreparedOffQ))[tid];
             q2[tid] = G(reinterpret_cast<const float *>(a.tables + kPreparedBytes +
@@ -522,37 +589,24 @@ __global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
     const StepScalars &sc = a.sc;
     double sw = 0.0, sx = 0.0;
 #pragma unroll
-    for (int c = 0; c < K::C; ++c) {
-        const int b = (8 * c + wave) / K::kSPB;  // tile-local block of this chunk
-        const int64_t e0 = c * (kOS * 4) + tid * 4;
-        const bool live = e0 < numel;
-        const float n1 = (OPT == kLamb && live) ? G(a1)[b] : 0.0f;
-        const float n2 = (OPT == kLamb && live) ? G(a2)[b] : 0.0f;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t e = e0 + r;
-            if (e < numel) {
-                const float w = G(param)[e];
-                float g;
-                if constexpr (GRAD == kF16)
-                    g = (float)G(static_cast<const _Float16 *>(grad))[e];
-                else
-                    g = G(static_cast<const float *>(grad))[e];
-                sw += (double)w * (double)w;
-                if constexpr (OPT == kLamb) {
-                    const float m = q1[G(s1)[e]] * n1;
-                    const float v = q2[G(s2)[e]] * n2;
-                    const float mn = sc.b1 * m + sc.omb1 * g;
-                    const float vn = sc.b2 * v + sc.omb2 * (g * g);
-                    const float denom =
-                        __builtin_fmaf(__builtin_amdgcn_sqrtf(vn), sc.inv_sqrt_bc2, sc.eps);
-                    const float u =
-                        __builtin_fmaf(mn * sc.bc1_inv, __builtin_amdgcn_rcpf(denom), sc.wd * w);
-                    sx += (double)u * (double)u;
-                } else {
-                    sx += (double)g * (double)g;
-                }
-            }
+    for (int i = 0; i < 4 * C; ++i) {
+        const int c = i / 4;
+        if (!full && (i & 3) >= valid[c])
+            continue;
+        const float wi = w[i], gi = g[i];
+        sw += (double)wi * (double)wi;
+        if constexpr (kIsLamb) {
+            const float m = q1[(k1[c] >> (8 * (i & 3))) & 0xffu] * n1[c];
+            const float v = q2[(k2[c] >> (8 * (i & 3))) & 0xffu] * n2[c];
+            const float mn = sc.b1 * m + sc.omb1 * gi;
+            const float vn = sc.b2 * v + sc.omb2 * (gi * gi);
+            const float denom =
+                __builtin_fmaf(__builtin_amdgcn_sqrtf(vn), sc.inv_sqrt_bc2, sc.eps);
+            const float u =
+                __builtin_fmaf(mn * sc.bc1_inv, __builtin_amdgcn_rcpf(denom), sc.wd * wi);
+            sx += (double)u * (double)u;
+        } else {
+            sx += (double)gi * (double)gi;
         }
     }
     // wave sums, then the 8 wave sums in order
@@ -577,25 +631,41 @@ __global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
     }
 }
 
-// One thread per tensor: its tiles' partial sums in tile order, then
-// lr * ratio, ratio = |w| / |u| (LAMB) or trust |w| / (|g| + wd |w|) (LARS),
-// 1 when either norm is zero.
-__global__ __launch_bounds__(256) void trust_ratio_kernel(const PlanArgs a, int lamb)
+// One workgroup per tensor: thread t sums the partials of the tensor's tiles
+// t, t + 256, ... in order, the 256 thread sums are combined by a fixed tree,
+// then lr * ratio, ratio = |w| / |u| (LAMB) or trust |w| / (|g| + wd |w|)
+// (LARS), 1 when either norm is zero.  The order depends on the tile count
+// only, so the result is deterministic.
+constexpr int kTrustThreads = 256;
+
+__global__ __launch_bounds__(kTrustThreads) void trust_ratio_kernel(const PlanArgs a, int lamb)
 {
-    const int t = blockIdx.x * 256 + threadIdx.x;
-    if (t >= a.ntensors)
-        return;
+    __shared__ double rw[kTrustThreads], rx[kTrustThreads];
+    const int t = blockIdx.x;
+    const int tid = threadIdx.x;
     const int64_t k0 = G(a.first_tile)[t], k1 = G(a.first_tile)[t + 1];
     double sw = 0.0, sx = 0.0;
-    for (int64_t k = k0; k < k1; ++k) {
+    for (int64_t k = k0 + tid; k < k1; k += kTrustThreads) {
         sw += G(a.partials)[2 * k];
         sx += G(a.partials)[2 * k + 1];
     }
-    const double nw = sqrt(sw), nx = sqrt(sx);
-    double ratio = 1.0;
-    if (nw > 0.0 && nx > 0.0)
-        ratio = lamb ? nw / nx : (double)a.sc.trust * nw / (nx + (double)a.sc.wd * nw);
-    G(a.lr_ratio)[t] = (float)((double)a.sc.lr * ratio);
+    rw[tid] = sw;
+    rx[tid] = sx;
+    __syncthreads();
+    for (int h = kTrustThreads / 2; h > 0; h >>= 1) {
+        if (tid < h) {
+            rw[tid] += rw[tid + h];
+            rx[tid] += rx[tid + h];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        const double nw = sqrt(rw[0]), nx = sqrt(rx[0]);
+        double ratio = 1.0;
+        if (nw > 0.0 && nx > 0.0)
+            ratio = lamb ? nw / nx : (double)a.sc.trust * nw / (nx + (double)a.sc.wd * nw);
+        G(a.lr_ratio)[t] = (float)((double)a.sc.lr * ratio);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -882,8 +952,8 @@ hipError_t launch_trust_ratios(int opt, int grad_dtype, int blocksize, const Pla
     }
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(trust_ratio_kernel, dim3((unsigned)((a.ntensors + 255) / 256)), dim3(256),
-                       0, stream, a, opt == kLamb ? 1 : 0);
+    hipLaunchKernelGGL(trust_ratio_kernel, dim3((unsigned)a.ntensors), dim3(kTrustThreads), 0,
+                       stream, a, opt == kLamb ? 1 : 0);
     return hipGetLastError();
 }
 

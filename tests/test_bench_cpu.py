@@ -43,3 +43,15 @@ def test_recorded_counter_traffic_matches_the_byte_model():
     for key, m in bench.MEASURED_TRAFFIC.items():
         t = m["fetch_kib"] * 1024 * bench.FETCH_SCALE + m["write_kib"] * 1024 * bench.WRITE_SCALE
         assert 0.99 < t / algorithmic[key] < 1.02, key
+
+
+def test_byte_model_of_the_norm_pass():
+    c5 = [s.numel for s in workloads.lm_1p5b_specs()]
+    n = sum(c5)
+    nb = sum((k + 2047) // 2048 for k in c5)
+    # LAMB: Adam's step plus a read of w, g, both codes and both absmax
+    assert bench.workload_bytes("lm1p5b-lamb", c5, 2048, 2) == 22 * n + 24 * nb
+    # LARS: a one-state step (4+4+2+1+1 B, 8 B per block) plus a read of w and g
+    assert bench.workload_bytes("lm1p5b-lars", c5, 2048, 2) == 18 * n + 8 * nb
+    assert bench.workload_bytes("lm1p5b-adagrad", c5, 2048, 2) == 12 * n + 8 * nb
+    assert bench.workload_bytes("lm1p5b-adam", c5, 2048, 2) == bench.step_bytes(c5, 2048, 2, 2)
