@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libbq.so")
-SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_kernels.hip", "bq_oneshot.hip", "bq_state32.hip",
+SOURCES = ["bq_api.cpp", "bq_codebook.cpp", "bq_oneshot.hip", "bq_state32.hip",
            "bq_quantiles.hip"]
 # the benchmark's streaming-ceiling kernel, a library of its own
 STREAM_LIB = os.path.join(PKG, "libbq_stream.so")
@@ -59,7 +59,7 @@ def build(verbose: bool = False) -> str:
 def build_asm(out_dir: str) -> None:
     """Write the device assembly of the kernels (for inspection only)."""
     os.makedirs(out_dir, exist_ok=True)
-    for name in ("bq_kernels.hip", "bq_oneshot.hip"):
+    for name in ("bq_oneshot.hip", "bq_state32.hip", "bq_quantiles.hip"):
         cmd = [hipcc(), *FLAGS, "--cuda-device-only", "-S", "-o",
                os.path.join(out_dir, name.replace(".hip", ".s")), os.path.join(CSRC, name)]
         subprocess.run(cmd, check=True)
@@ -68,4 +68,4 @@ def build_asm(out_dir: str) -> None:
 if __name__ == "__main__":
     build(verbose=True)
     if "--asm" in sys.argv:
-        build_asm(os.path.join(ROOT, "_work", "asm"))
+        build_asm(os.path.join(PKG, "_build", "asm"))

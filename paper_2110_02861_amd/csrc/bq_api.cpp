@@ -272,7 +272,7 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
 
     // Pack non-empty tensors into launches of at most kMaxDescPerLaunch
     // descriptors, or fewer when a launch's tile count would overflow int32.
-    const int64_t tile = bq::tile_elems(blocksize);
+    const int64_t tile = bq::step_tile(blocksize);
     int32_t i = 0;
     while (i < ntensors) {
         int32_t k = 0;
@@ -291,8 +291,8 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
             continue;
         args.ntensors = k;
         args.total_tiles = static_cast<int32_t>(tiles);
-        const hipError_t e = bq::launch_step(static_cast<int>(opt), static_cast<int>(grad_dtype),
-                                             blocksize, args, stream);
+        const hipError_t e = bq::launch_step_persistent(
+            static_cast<int>(opt), static_cast<int>(grad_dtype), blocksize, args, stream);
         if (e != hipSuccess)
             return BQ_ERR_HIP;
     }

@@ -1,5 +1,6 @@
 // Internal declarations shared by the C-ABI layer (bq_api.cpp) and the HIP
-// kernels (bq_kernels.hip).  Not part of the public interface.
+// kernels (bq_oneshot.hip, bq_state32.hip, bq_quantiles.hip).  Not part of the
+// public interface.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -177,8 +178,10 @@ constexpr bool has_two_states(int opt) { return opt == kAdam || opt == kAdamW ||
 constexpr bool has_trust_ratio(int opt) { return opt == kLamb || opt == kLars; }
 enum { kF32 = 0, kF16 = 1 };
 
-hipError_t launch_step(int opt, int grad_dtype, int blocksize, const StepArgs &args,
-                       hipStream_t stream);
+// the fused step from raw maps: the one-shot tile code in persistent
+// workgroups (tile_begin in units of step_tile(blocksize))
+hipError_t launch_step_persistent(int opt, int grad_dtype, int blocksize, const StepArgs &args,
+                                  hipStream_t stream);
 hipError_t launch_quantize(const float *qmap, const float *x, int64_t n, int blocksize,
                            uint8_t *codes, float *absmax, hipStream_t stream);
 hipError_t launch_dequantize(const float *qmap, const uint8_t *codes, const float *absmax,

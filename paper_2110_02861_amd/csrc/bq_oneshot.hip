@@ -145,11 +145,16 @@ struct StepOS {
     static constexpr int kGran = kGran1 + (kTwo ? kPreparedNonnegBytes / 16 : 0);
     static constexpr int kGPT = (kGran + kOS - 1) / kOS;          // granules per thread
 
-    // One tile.  gran: this thread's decision-table granules, loaded by the
-    // caller before anything else so their L2 latency overlaps the HBM loads.
-    template <bool FULL>
-    __device__ static void tile(const PlanArgs &a, const TensorDesc &D, int64_t t0, uint8_t *lds,
-                                const vu4 (&gran)[kGPT], float lr_r)
+    // One tile.  STAGE (one-shot workgroups): gran holds this thread's
+    // decision-table granules, loaded by the caller before anything else so
+    // their L2 latency overlaps the HBM loads, and the tile writes them into
+    // LDS; kmax comes from a.tables.  Without STAGE (persistent workgroups)
+    // the tables are already in LDS and kmax is passed in.  Args: PlanArgs or
+    // StepArgs (sc and use_wd are read).
+    template <bool FULL, bool STAGE = true, class Args = PlanArgs>
+    __device__ static void tile(const Args &a, const TensorDesc &D, int64_t t0, uint8_t *lds,
+                                const vu4 (&gran)[kGPT], float lr_r, int km1_in = 0,
+                                int km2_in = 0)
     {
         uint32_t *slots = reinterpret_cast<uint32_t *>(lds + kLdsSlots);
         BlockNorm *norms = reinterpret_cast<BlockNorm *>(lds + kLdsNorms);
@@ -215,15 +220,17 @@ struct StepOS {
         // priority, so tiles that hold loaded data finish (and free their
         // slot for a new tile's loads) ahead of tiles still waiting
         __builtin_amdgcn_s_setprio(2);
-        const int km1 = prepared_kmax(a.tables);
-        const int km2 = kTwo ? prepared_kmax(a.tables + kPreparedBytes) : 0;
-
-        // tables into LDS (threads past the last granule rewrite it, same bytes);
-        // block max slots cleared
+        int km1 = km1_in, km2 = km2_in;
+        if constexpr (STAGE) {
+            km1 = prepared_kmax(a.tables);
+            km2 = kTwo ? prepared_kmax(a.tables + kPreparedBytes) : 0;
+            // tables into LDS (threads past the last granule rewrite it, same bytes)
 #pragma unroll
-        for (int k = 0; k < kGPT; ++k)
-            reinterpret_cast<vu4 *>(lds + kLdsMap1)[min((int)threadIdx.x + k * kOS, kGran - 1)] =
-                gran[k];
+            for (int k = 0; k < kGPT; ++k)
+                reinterpret_cast<vu4 *>(lds + kLdsMap1)[min((int)threadIdx.x + k * kOS,
+                                                             kGran - 1)] = gran[k];
+        }
+        // block max slots cleared
         if (tid < 2 * kBPT)
             slots[tid] = 0u;
         __syncthreads();
@@ -489,6 +496,57 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Fused 8-bit optimizer step from raw maps, persistent workgroups
+// ---------------------------------------------------------------------------
+
+// The allocation-free call receives only the raw maps: every workgroup builds
+// both maps' decision tables in its own LDS once (in the layout the one-shot
+// kernel stages, plus map 2's unused negative half), then runs the one-shot
+// tile code over tiles blockIdx.x, blockIdx.x + gridDim.x, ... of the launch,
+// whose tensors travel in the kernel arguments (tile_begin in units of
+// step_tile(B)).
+constexpr int kLdsPersistBytes = kLdsMap2 + kPreparedSignedBytes;
+
+template <int OPT, int GRAD, int B>
+__global__ __launch_bounds__(kOS) void step_persistent_kernel(const StepArgs a)
+{
+    using K = StepOS<OPT, GRAD, B>;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsPersistBytes];
+    __shared__ int kmax[2];
+    build_tables<kOS>(a.q1, reinterpret_cast<float *>(lds + kLdsMap1 + kPreparedOffQ),
+                      reinterpret_cast<float *>(lds + kLdsMap1 + kPreparedOffT),
+                      lds + kLdsMap1 + kPreparedOffBase, &kmax[0]);
+    if constexpr (K::kTwo)
+        build_tables<kOS>(a.q2, reinterpret_cast<float *>(lds + kLdsMap2 + kPreparedOffQ),
+                          reinterpret_cast<float *>(lds + kLdsMap2 + kPreparedOffT),
+                          lds + kLdsMap2 + kPreparedOffBase, &kmax[1]);
+    const int km1 = __builtin_amdgcn_readfirstlane(kmax[0]);
+    const int km2 = K::kTwo ? __builtin_amdgcn_readfirstlane(kmax[1]) : 0;
+    const vu4 none[K::kGPT] = {};
+    int t = 0;
+    for (int tile = blockIdx.x; tile < a.total_tiles; tile += gridDim.x) {
+        while (t + 1 < a.ntensors && tile >= a.d[t + 1].tile_begin)
+            ++t;
+        const TensorDesc &S = a.d[t];
+        const int64_t t0 = (int64_t)(tile - S.tile_begin) * K::TILE;
+        TensorDesc D;
+        D.param = S.param + t0;
+        D.grad = static_cast<const char *>(S.grad) + t0 * (GRAD == kF16 ? 2 : 4);
+        D.s1 = S.s1 + t0;
+        D.s2 = K::kTwo ? S.s2 + t0 : nullptr;
+        D.a1 = S.a1 + t0 / B;
+        D.a2 = K::kTwo ? S.a2 + t0 / B : nullptr;
+        D.numel = S.numel - t0;
+        // loads of this tile at normal priority, the rest raised (as one-shot)
+        __builtin_amdgcn_s_setprio(0);
+        if (K::TILE <= D.numel)
+            K::template tile<true, false>(a, D, 0, lds, none, 0.0f, km1, km2);
+        else
+            K::template tile<false, false>(a, D, 0, lds, none, 0.0f, km1, km2);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // LAMB / LARS: per-tile partial squared norms, then per-tensor lr * ratio
 // ---------------------------------------------------------------------------
 
@@ -684,6 +742,15 @@ struct QuantOS {
     static constexpr int kBPT = TILE / B;      // blocks per tile
     static constexpr int kSPB = B / 256;       // segments per block
     static_assert(kBPT <= 64, "one lane of wave 0 per block");
+
+    // One tile starting at element t0.  STAGE (one-shot workgroups): gran is
+    // this thread's table granule, loaded by the caller before the tile's HBM
+    // loads, written into LDS here; kmax comes from tables.  Without STAGE
+    // (persistent workgroups) the tables are already in LDS and km is passed.
+    template <bool FULL, bool STAGE>
+    __device__ static void tile(const uint8_t *tables, const float *x, int64_t n, int64_t t0,
+                                uint8_t *codes, float *absmax, uint8_t *lds, const vu4 &gran,
+                                int km_in);
 };
 
 // Only the thresholds and both bucket halves are copied (the map values
@@ -698,35 +765,24 @@ static_assert(kQuantGran <= kOS, "one granule per thread");
 static_assert(kLdsQNorms + 64 * (int)sizeof(BlockNorm) <= kLdsMap1, "LDS layout");
 
 template <int B>
-__global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__restrict__ tables,
-                                                               const float *__restrict__ x,
-                                                               int64_t n,
-                                                               uint8_t *__restrict__ codes,
-                                                               float *__restrict__ absmax)
+template <bool FULL, bool STAGE>
+__device__ void QuantOS<B>::tile(const uint8_t *tables, const float *x, int64_t n, int64_t t0,
+                                 uint8_t *codes, float *absmax, uint8_t *lds, const vu4 &gran,
+                                 int km_in)
 {
-    using S = QuantOS<B>;
-    constexpr int C = S::C;
-    constexpr int N = S::N;
-    __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsQuantBytes];
     uint32_t *slots = reinterpret_cast<uint32_t *>(lds + kLdsQSlots);
     BlockNorm *norms = reinterpret_cast<BlockNorm *>(lds + kLdsQNorms);
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
-    const int64_t t0 = (int64_t)blockIdx.x * S::TILE;
-    const bool full = t0 + S::TILE <= n;
 
-    // this thread's table granule (L2) first, then the tile's HBM loads
-    vu4 gran = {0u, 0u, 0u, 0u};
-    if (tid < kQuantGran)
-        gran = G(reinterpret_cast<const vu4 *>(tables + kPreparedOffT))[tid];
     float v[N];
     int valid[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         const int64_t e = t0 + c * (kOS * 4) + tid * 4;
         const int64_t rem = n - e;
-        valid[c] = rem <= 0 ? 0 : (rem >= 4 ? 4 : (int)rem);
-        if (full) {
+        valid[c] = FULL ? 4 : (rem <= 0 ? 0 : (rem >= 4 ? 4 : (int)rem));
+        if (FULL) {
             const vf4 y = ld_nt(reinterpret_cast<const vf4 *>(x + e));
             v[4 * c] = y.x;
             v[4 * c + 1] = y.y;
@@ -738,10 +794,13 @@ __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__
                 v[4 * c + r] = r < valid[c] ? G(x)[e + r] : 0.0f;
         }
     }
-    const int km = prepared_kmax(tables);
-    if (tid < kQuantGran)
-        reinterpret_cast<vu4 *>(lds + kLdsMap1 + kPreparedOffT)[tid] = gran;
-    if (tid < S::kBPT)
+    int km = km_in;
+    if constexpr (STAGE) {
+        km = prepared_kmax(tables);
+        if (tid < kQuantGran)
+            reinterpret_cast<vu4 *>(lds + kLdsMap1 + kPreparedOffT)[tid] = gran;
+    }
+    if (tid < kBPT)
         slots[tid] = 0u;
     __syncthreads();
 
@@ -754,13 +813,13 @@ __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__
             mx = fmaxf(mx, fabsf(v[4 * c + r]));
         const uint32_t u = row_umax(__float_as_uint(mx));
         if ((tid & 15) == 0)
-            atomicMax(&slots[(8 * c + wave) / S::kSPB], u);
+            atomicMax(&slots[(8 * c + wave) / kSPB], u);
     }
     __syncthreads();
-    if (tid < S::kBPT) {
+    if (tid < kBPT) {
         const float A = __uint_as_float(slots[tid]);
         norms[tid] = block_norm(A);
-        if (full || t0 + (int64_t)tid * B < n)
+        if (FULL || t0 + (int64_t)tid * B < n)
             G(absmax)[t0 / B + tid] = A;
     }
     __syncthreads();
@@ -774,7 +833,7 @@ __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__
     bool plain = km == 1;
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        nb[c] = norms[(8 * c + wave) / S::kSPB];
+        nb[c] = norms[(8 * c + wave) / kSPB];
         plain = plain &&
                 __builtin_amdgcn_readfirstlane(__float_as_int(nb[c].s)) == __float_as_int(1.0f);
     }
@@ -804,7 +863,7 @@ __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         const int64_t e = t0 + c * (kOS * 4) + tid * 4;
-        if (full) {
+        if (FULL) {
             st_nt(reinterpret_cast<uint32_t *>(codes + e),
                   q[4 * c] | (q[4 * c + 1] << 8) | (q[4 * c + 2] << 16) | (q[4 * c + 3] << 24));
         } else {
@@ -813,6 +872,55 @@ __global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__
                 if (r < valid[c])
                     G(codes)[e + r] = (uint8_t)q[4 * c + r];
         }
+    }
+}
+
+// Prepared map: one workgroup per tile; this thread's table granule (L2) is
+// loaded first, then the tile's HBM loads.
+template <int B>
+__global__ __launch_bounds__(kOS) void quantize_oneshot_kernel(const uint8_t *__restrict__ tables,
+                                                               const float *__restrict__ x,
+                                                               int64_t n,
+                                                               uint8_t *__restrict__ codes,
+                                                               float *__restrict__ absmax)
+{
+    using S = QuantOS<B>;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsQuantBytes];
+    const int64_t t0 = (int64_t)blockIdx.x * S::TILE;
+    vu4 gran = {0u, 0u, 0u, 0u};
+    if (threadIdx.x < kQuantGran)
+        gran = G(reinterpret_cast<const vu4 *>(tables + kPreparedOffT))[threadIdx.x];
+    if (t0 + S::TILE <= n)
+        S::template tile<true, true>(tables, x, n, t0, codes, absmax, lds, gran, 0);
+    else
+        S::template tile<false, true>(tables, x, n, t0, codes, absmax, lds, gran, 0);
+}
+
+// Raw map (the allocation-free call): every workgroup builds the decision
+// tables in its own LDS once, then walks tiles blockIdx.x, blockIdx.x +
+// gridDim.x, ...
+template <int B>
+__global__ __launch_bounds__(kOS) void quantize_persistent_kernel(const float *__restrict__ qmap,
+                                                                  const float *__restrict__ x,
+                                                                  int64_t n,
+                                                                  uint8_t *__restrict__ codes,
+                                                                  float *__restrict__ absmax)
+{
+    using S = QuantOS<B>;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsQuantBytes];
+    __shared__ int kmax;
+    build_tables<kOS>(qmap, reinterpret_cast<float *>(lds + kLdsMap1 + kPreparedOffQ),
+                      reinterpret_cast<float *>(lds + kLdsMap1 + kPreparedOffT),
+                      lds + kLdsMap1 + kPreparedOffBase, &kmax);
+    const int km = __builtin_amdgcn_readfirstlane(kmax);
+    const vu4 none = {0u, 0u, 0u, 0u};
+    const int64_t tiles = (n + S::TILE - 1) / S::TILE;
+    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        const int64_t t0 = tile * S::TILE;
+        if (t0 + S::TILE <= n)
+            S::template tile<true, false>(nullptr, x, n, t0, codes, absmax, lds, none, km);
+        else
+            S::template tile<false, false>(nullptr, x, n, t0, codes, absmax, lds, none, km);
     }
 }
 
@@ -871,6 +979,44 @@ __global__ __launch_bounds__(kOS) void dequantize_kernel(const float *__restrict
 }
 
 template <int OPT, int GRAD, int B>
+hipError_t launch_persist_t(const StepArgs &a, hipStream_t s)
+{
+    auto k = step_persistent_kernel<OPT, GRAD, B>;
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kOS, 0) != hipSuccess ||
+        per_cu <= 0)
+        per_cu = 1;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        cus = 256;
+    const int64_t cap = (int64_t)per_cu * cus;
+    const int64_t grid = a.total_tiles < cap ? a.total_tiles : cap;
+    hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kOS), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int OPT, int GRAD>
+hipError_t launch_persist_b(int blocksize, const StepArgs &a, hipStream_t s)
+{
+    switch (blocksize) {
+    case 256: return launch_persist_t<OPT, GRAD, 256>(a, s);
+    case 512: return launch_persist_t<OPT, GRAD, 512>(a, s);
+    case 1024: return launch_persist_t<OPT, GRAD, 1024>(a, s);
+    case 2048: return launch_persist_t<OPT, GRAD, 2048>(a, s);
+    case 4096: return launch_persist_t<OPT, GRAD, 4096>(a, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int OPT>
+hipError_t launch_persist_g(int grad_dtype, int blocksize, const StepArgs &a, hipStream_t s)
+{
+    return grad_dtype == kF16 ? launch_persist_b<OPT, kF16>(blocksize, a, s)
+                              : launch_persist_b<OPT, kF32>(blocksize, a, s);
+}
+
+template <int OPT, int GRAD, int B>
 hipError_t launch_os_t(const PlanArgs &a, hipStream_t s)
 {
     hipLaunchKernelGGL((step_oneshot_kernel<OPT, GRAD, B>), dim3((unsigned)a.total_tiles),
@@ -896,6 +1042,26 @@ hipError_t launch_os_g(int grad_dtype, int blocksize, const PlanArgs &a, hipStre
 {
     return grad_dtype == kF16 ? launch_os_b<OPT, kF16>(blocksize, a, s)
                               : launch_os_b<OPT, kF32>(blocksize, a, s);
+}
+
+template <int B>
+hipError_t launch_qr_t(const float *qmap, const float *x, int64_t n, uint8_t *codes,
+                       float *absmax, hipStream_t s)
+{
+    auto k = quantize_persistent_kernel<B>;
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kOS, 0) != hipSuccess ||
+        per_cu <= 0)
+        per_cu = 1;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        cus = 256;
+    const int64_t tiles = (n + quant_tile(B) - 1) / quant_tile(B);
+    const int64_t cap = (int64_t)per_cu * cus;
+    hipLaunchKernelGGL(k, dim3((unsigned)(tiles < cap ? tiles : cap)), dim3(kOS), 0, s, qmap, x,
+                       n, codes, absmax);
+    return hipGetLastError();
 }
 
 template <int B>
@@ -957,6 +1123,18 @@ hipError_t launch_trust_ratios(int opt, int grad_dtype, int blocksize, const Pla
     return hipGetLastError();
 }
 
+hipError_t launch_step_persistent(int opt, int grad_dtype, int blocksize, const StepArgs &a,
+                                 hipStream_t stream)
+{
+    switch (opt) {
+    case kAdam: return launch_persist_g<kAdam>(grad_dtype, blocksize, a, stream);
+    case kAdamW: return launch_persist_g<kAdamW>(grad_dtype, blocksize, a, stream);
+    case kMomentum: return launch_persist_g<kMomentum>(grad_dtype, blocksize, a, stream);
+    case kAdaGrad: return launch_persist_g<kAdaGrad>(grad_dtype, blocksize, a, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const PlanArgs &a,
                                hipStream_t stream)
 {
@@ -981,6 +1159,19 @@ hipError_t launch_dequantize(const float *qmap, const uint8_t *codes, const floa
     hipLaunchKernelGGL(dequantize_kernel, dim3((unsigned)tiles), dim3(kOS), 0, stream, qmap,
                        codes, absmax, n, lg, out);
     return hipGetLastError();
+}
+
+hipError_t launch_quantize(const float *qmap, const float *x, int64_t n, int blocksize,
+                           uint8_t *codes, float *absmax, hipStream_t stream)
+{
+    switch (blocksize) {
+    case 256: return launch_qr_t<256>(qmap, x, n, codes, absmax, stream);
+    case 512: return launch_qr_t<512>(qmap, x, n, codes, absmax, stream);
+    case 1024: return launch_qr_t<1024>(qmap, x, n, codes, absmax, stream);
+    case 2048: return launch_qr_t<2048>(qmap, x, n, codes, absmax, stream);
+    case 4096: return launch_qr_t<4096>(qmap, x, n, codes, absmax, stream);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_quantize_prepared(const uint8_t *tables, const float *x, int64_t n,
