@@ -37,21 +37,21 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
 
     float w[4], g[4], m[4], v[4];
     if (nv == 4) {
-        const vf4 wv = *G(reinterpret_cast<const vf4 *>(D.param + e0));
-        const vf4 mv = *G(reinterpret_cast<const vf4 *>(D.m + e0));
+        const vf4 wv = ld_nt(reinterpret_cast<const vf4 *>(D.param + e0));
+        const vf4 mv = ld_nt(reinterpret_cast<const vf4 *>(D.m + e0));
         w[0] = wv.x; w[1] = wv.y; w[2] = wv.z; w[3] = wv.w;
         m[0] = mv.x; m[1] = mv.y; m[2] = mv.z; m[3] = mv.w;
         if constexpr (kTwo) {
-            const vf4 vv = *G(reinterpret_cast<const vf4 *>(D.v + e0));
+            const vf4 vv = ld_nt(reinterpret_cast<const vf4 *>(D.v + e0));
             v[0] = vv.x; v[1] = vv.y; v[2] = vv.z; v[3] = vv.w;
         }
         if constexpr (GRAD == kF16) {
-            const vu2 gv = *G(reinterpret_cast<const vu2 *>(
+            const vu2 gv = ld_nt(reinterpret_cast<const vu2 *>(
                 static_cast<const _Float16 *>(D.grad) + e0));
             g[0] = half_lo(gv.x); g[1] = half_hi(gv.x);
             g[2] = half_lo(gv.y); g[3] = half_hi(gv.y);
         } else {
-            const vf4 gv = *G(reinterpret_cast<const vf4 *>(static_cast<const float *>(D.grad) + e0));
+            const vf4 gv = ld_nt(reinterpret_cast<const vf4 *>(static_cast<const float *>(D.grad) + e0));
             g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
         }
     } else {
@@ -93,10 +93,10 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
     }
 
     if (nv == 4) {
-        *G(reinterpret_cast<vf4 *>(D.param + e0)) = vf4{w[0], w[1], w[2], w[3]};
-        *G(reinterpret_cast<vf4 *>(D.m + e0)) = vf4{m[0], m[1], m[2], m[3]};
+        st_nt(reinterpret_cast<vf4 *>(D.param + e0), vf4{w[0], w[1], w[2], w[3]});
+        st_nt(reinterpret_cast<vf4 *>(D.m + e0), vf4{m[0], m[1], m[2], m[3]});
         if constexpr (kTwo)
-            *G(reinterpret_cast<vf4 *>(D.v + e0)) = vf4{v[0], v[1], v[2], v[3]};
+            st_nt(reinterpret_cast<vf4 *>(D.v + e0), vf4{v[0], v[1], v[2], v[3]});
     } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
