@@ -15,8 +15,10 @@ namespace {
 
 using namespace dev;
 
-constexpr int kOS = 512;  // threads per workgroup
+constexpr int kOS = 512;  // threads per workgroup (quantize, dequantize)
 constexpr int kOSWaves = kOS / 64;
+constexpr int kST = 512;  // threads per workgroup of the step and its norm pass
+constexpr int kSTWaves = kST / 64;
 
 // ---------------------------------------------------------------------------
 // Prepare: decision tables of 1 or 2 maps (one workgroup each)
@@ -127,23 +129,23 @@ static_assert(kLdsMap1 % 16 == 0 && kLdsMap2 % 16 == 0, "16 B granules");
 // Fused 8-bit optimizer step, one tile per workgroup
 // ---------------------------------------------------------------------------
 
-// One tile of the step: 4096 elements, 512 threads, two chunks of 4 contiguous
-// elements per thread (chunk c of thread t starts at element c*2048 + 4t).
-// Element groups of 256 (one wave and chunk) are "segments"; segment s = 8c + w
-// covers tile elements [256 s, 256 s + 256), so block b of the tile is made of
-// segments [b B/256, (b+1) B/256).
+// One tile of the step: 4096 elements, kST threads, chunks of 4 contiguous
+// elements per thread (chunk c of thread t starts at element 4 kST c + 4t).
+// Element groups of 256 (one wave and chunk) are "segments"; segment
+// s = kSTWaves c + w covers tile elements [256 s, 256 s + 256), so block b of
+// the tile is made of segments [b B/256, (b+1) B/256).
 template <int OPT, int GRAD, int B>
 struct StepOS {
-    static constexpr int C = step_tile(B) / 2048;       // chunks per thread
+    static constexpr int C = step_tile(B) / (kST * 4);  // chunks per thread
     static constexpr int N = 4 * C;                     // elements per thread
     static constexpr int TILE = step_tile(B);
-    static_assert(TILE == kOS * N, "tile size");
+    static_assert(TILE == kST * N, "tile size");
     static constexpr bool kTwo = has_two_states(OPT);
     static constexpr int kBPT = TILE / B;               // blocks per tile
     static constexpr int kSPB = B / 256;                // segments per block
     static constexpr int kGran1 = kPreparedSignedBytes / 16;      // map 1 granules
     static constexpr int kGran = kGran1 + (kTwo ? kPreparedNonnegBytes / 16 : 0);
-    static constexpr int kGPT = (kGran + kOS - 1) / kOS;          // granules per thread
+    static constexpr int kGPT = (kGran + kST - 1) / kST;          // granules per thread
 
     // One tile.  STAGE (one-shot workgroups): gran holds this thread's
     // decision-table granules, loaded by the caller before anything else so
@@ -168,7 +170,7 @@ struct StepOS {
         int valid[C];
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            const int64_t e = t0 + c * (kST * 4) + tid * 4;
             if (FULL) {
                 valid[c] = 4;
                 wr[c] = ld_nt(reinterpret_cast<const vf4 *>(D.param + e));
@@ -210,7 +212,7 @@ struct StepOS {
         float n1[C], n2[C];
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            const int seg = 8 * c + wave;
+            const int seg = kSTWaves * c + wave;
             const int b = seg / kSPB;
             const bool live = FULL || t0 + (int64_t)b * B < D.numel;
             n1[c] = live ? G(D.a1)[blk0 + b] : 0.0f;
@@ -227,7 +229,7 @@ struct StepOS {
             // tables into LDS (threads past the last granule rewrite it, same bytes)
 #pragma unroll
             for (int k = 0; k < kGPT; ++k)
-                reinterpret_cast<vu4 *>(lds + kLdsMap1)[min((int)threadIdx.x + k * kOS,
+                reinterpret_cast<vu4 *>(lds + kLdsMap1)[min((int)threadIdx.x + k * kST,
                                                              kGran - 1)] = gran[k];
         }
         // block max slots cleared
@@ -333,7 +335,7 @@ struct StepOS {
         // block reduction
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            const int64_t e = t0 + c * (kST * 4) + tid * 4;
             if (FULL) {
                 st_nt(reinterpret_cast<vf4 *>(D.param + e),
                       vf4{w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]});
@@ -351,7 +353,7 @@ struct StepOS {
         // block's normalizers once and stores the new absmax
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            const int b = (8 * c + wave) / kSPB;
+            const int b = (kSTWaves * c + wave) / kSPB;
             const uint32_t u1 = row_umax(__float_as_uint(mx1[c]));
             const uint32_t u2 = kTwo ? row_umax(__float_as_uint(mx2[c])) : 0u;
             if ((tid & 15) == 0) {
@@ -382,7 +384,7 @@ struct StepOS {
         bool plain = (km1 == 1) && (!kTwo || km2 == 1);
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            const int b = (8 * c + wave) / kSPB;
+            const int b = (kSTWaves * c + wave) / kSPB;
             nb1[c] = norms[2 * b];
             nb2[c] = kTwo ? norms[2 * b + 1] : nb1[c];
             plain = plain && __builtin_amdgcn_readfirstlane(__float_as_int(nb1[c].s)) ==
@@ -435,7 +437,7 @@ struct StepOS {
         // store the codes
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            const int64_t e = t0 + c * (kOS * 4) + tid * 4;
+            const int64_t e = t0 + c * (kST * 4) + tid * 4;
             if (FULL) {
                 st_nt(reinterpret_cast<uint32_t *>(D.s1 + e),
                       c1[4 * c] | (c1[4 * c + 1] << 8) | (c1[4 * c + 2] << 16) |
@@ -459,7 +461,7 @@ struct StepOS {
 };
 
 template <int OPT, int GRAD, int B>
-__global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
+__global__ __launch_bounds__(kST) void step_oneshot_kernel(const PlanArgs a)
 {
     using K = StepOS<OPT, GRAD, B>;
     __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
@@ -471,7 +473,7 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
     vu4 gran[K::kGPT];
 #pragma unroll
     for (int k = 0; k < K::kGPT; ++k) {
-        const int gi = min(tid + k * kOS, K::kGran - 1);
+        const int gi = min(tid + k * kST, K::kGran - 1);
         const int src = 16 * gi + (gi >= K::kGran1 ? kPreparedBytes - kPreparedSignedBytes : 0);
         gran[k] = *G(reinterpret_cast<const vu4 *>(a.tables + src));
     }
@@ -508,16 +510,16 @@ __global__ __launch_bounds__(kOS) void step_oneshot_kernel(const PlanArgs a)
 constexpr int kLdsPersistBytes = kLdsMap2 + kPreparedSignedBytes;
 
 template <int OPT, int GRAD, int B>
-__global__ __launch_bounds__(kOS) void step_persistent_kernel(const StepArgs a)
+__global__ __launch_bounds__(kST) void step_persistent_kernel(const StepArgs a)
 {
     using K = StepOS<OPT, GRAD, B>;
     __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsPersistBytes];
     __shared__ int kmax[2];
-    build_tables<kOS>(a.q1, reinterpret_cast<float *>(lds + kLdsMap1 + kPreparedOffQ),
+    build_tables<kST>(a.q1, reinterpret_cast<float *>(lds + kLdsMap1 + kPreparedOffQ),
                       reinterpret_cast<float *>(lds + kLdsMap1 + kPreparedOffT),
                       lds + kLdsMap1 + kPreparedOffBase, &kmax[0]);
     if constexpr (K::kTwo)
-        build_tables<kOS>(a.q2, reinterpret_cast<float *>(lds + kLdsMap2 + kPreparedOffQ),
+        build_tables<kST>(a.q2, reinterpret_cast<float *>(lds + kLdsMap2 + kPreparedOffQ),
                           reinterpret_cast<float *>(lds + kLdsMap2 + kPreparedOffT),
                           lds + kLdsMap2 + kPreparedOffBase, &kmax[1]);
     const int km1 = __builtin_amdgcn_readfirstlane(kmax[0]);
@@ -557,13 +559,13 @@ __global__ __launch_bounds__(kOS) void step_persistent_kernel(const StepArgs a)
 // g^2 (LARS, g before weight decay); each thread sums its elements in order,
 // the waves by a fixed butterfly, the 8 wave sums in order.
 template <int OPT, int GRAD, int B>
-__global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
+__global__ __launch_bounds__(kST) void norms_kernel(const PlanArgs a)
 {
     using K = StepOS<OPT, GRAD, B>;
     constexpr int C = K::C;
     constexpr bool kIsLamb = OPT == kLamb;
     __shared__ float q1[256], q2[256];
-    __shared__ double red[kOSWaves][2];
+    __shared__ double red[kSTWaves][2];
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const gptr<const TensorDesc> dp = G(a.tiles) + blockIdx.x;
@@ -581,7 +583,7 @@ __global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
     int valid[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        const int64_t e0 = c * (kOS * 4) + tid * 4;
+        const int64_t e0 = c * (kST * 4) + tid * 4;
         const int64_t rem = numel - e0;
         valid[c] = rem <= 0 ? 0 : (rem >= 4 ? 4 : (int)rem);
         if (full) {
@@ -631,7 +633,7 @@ __global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
     float n1[C], n2[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        const int b = (8 * c + wave) / K::kSPB;
+        const int b = (kSTWaves * c + wave) / K::kSPB;
         const bool live = full || (int64_t)b * B < numel;
         n1[c] = (kIsLamb && live) ? G(a1)[b] : 0.0f;
         n2[c] = (kIsLamb && live) ? G(a2)[b] : 0.0f;
@@ -680,7 +682,7 @@ __global__ __launch_bounds__(kOS) void norms_kernel(const PlanArgs a)
     __syncthreads();
     if (tid == 0) {
         double tw = 0.0, tx = 0.0;
-        for (int k = 0; k < kOSWaves; ++k) {
+        for (int k = 0; k < kSTWaves; ++k) {
             tw += red[k][0];
             tx += red[k][1];
         }
@@ -813,7 +815,7 @@ __device__ void QuantOS<B>::tile(const uint8_t *tables, const float *x, int64_t 
             mx = fmaxf(mx, fabsf(v[4 * c + r]));
         const uint32_t u = row_umax(__float_as_uint(mx));
         if ((tid & 15) == 0)
-            atomicMax(&slots[(8 * c + wave) / kSPB], u);
+            atomicMax(&slots[(kOSWaves * c + wave) / kSPB], u);
     }
     __syncthreads();
     if (tid < kBPT) {
@@ -833,7 +835,7 @@ __device__ void QuantOS<B>::tile(const uint8_t *tables, const float *x, int64_t 
     bool plain = km == 1;
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        nb[c] = norms[(8 * c + wave) / kSPB];
+        nb[c] = norms[(kOSWaves * c + wave) / kSPB];
         plain = plain &&
                 __builtin_amdgcn_readfirstlane(__float_as_int(nb[c].s)) == __float_as_int(1.0f);
     }
@@ -952,7 +954,7 @@ __global__ __launch_bounds__(kOS) void dequantize_kernel(const float *__restrict
         for (int c = 0; c < C; ++c) {
             const int64_t e = t0 + c * (kOS * 4) + tid * 4;
             k[c] = ld_nt(reinterpret_cast<const uint32_t *>(codes + e));
-            const int seg = __builtin_amdgcn_readfirstlane(8 * c + wave);
+            const int seg = __builtin_amdgcn_readfirstlane(kOSWaves * c + wave);
             A[c] = G(absmax)[(t0 + (int64_t)seg * 256) >> log2_blocksize];
         }
     }
@@ -983,7 +985,7 @@ hipError_t launch_persist_t(const StepArgs &a, hipStream_t s)
 {
     auto k = step_persistent_kernel<OPT, GRAD, B>;
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kOS, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kST, 0) != hipSuccess ||
         per_cu <= 0)
         per_cu = 1;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -992,7 +994,7 @@ hipError_t launch_persist_t(const StepArgs &a, hipStream_t s)
         cus = 256;
     const int64_t cap = (int64_t)per_cu * cus;
     const int64_t grid = a.total_tiles < cap ? a.total_tiles : cap;
-    hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kOS), 0, s, a);
+    hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kST), 0, s, a);
     return hipGetLastError();
 }
 
@@ -1020,7 +1022,7 @@ template <int OPT, int GRAD, int B>
 hipError_t launch_os_t(const PlanArgs &a, hipStream_t s)
 {
     hipLaunchKernelGGL((step_oneshot_kernel<OPT, GRAD, B>), dim3((unsigned)a.total_tiles),
-                       dim3(kOS), 0, s, a);
+                       dim3(kST), 0, s, a);
     return hipGetLastError();
 }
 
@@ -1088,7 +1090,7 @@ hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *table
 template <int OPT, int GRAD>
 hipError_t launch_norms_b(int blocksize, const PlanArgs &a, hipStream_t stream)
 {
-    const dim3 grid((unsigned)a.total_tiles), block(kOS);
+    const dim3 grid((unsigned)a.total_tiles), block(kST);
     switch (blocksize) {
     case 256: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 256>), grid, block, 0, stream, a); break;
     case 512: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 512>), grid, block, 0, stream, a); break;
