@@ -220,6 +220,10 @@ typedef struct bq_hparams {
  * Arithmetic of the states is fp32 in a fixed order without contraction, so
  * codes and absmax are reproducible; the param update uses the hardware square
  * root and reciprocal (relative error a few ulp of the update).
+ * Allocates nothing: the descriptors of up to 56 non-empty tensors travel in
+ * each kernel launch's arguments (so a list takes ceil(count / 56) launches,
+ * in list order), and every workgroup builds the maps' decision tables in its
+ * own on-chip memory.  A step plan (below) runs the same step in one launch.
  * Errors: BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_BLOCKSIZE, BQ_ERR_ENUM, BQ_ERR_DTYPE,
  * BQ_ERR_ALIGN, BQ_ERR_ARG (hp->step < 1), BQ_ERR_HIP.
  */

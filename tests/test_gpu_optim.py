@@ -298,3 +298,25 @@ def test_training_loop_reduces_loss():
         first = first if first is not None else float(loss)
     final = float(loss)
     assert final < 1e-3 * first, (first, final)
+
+
+@pytest.mark.parametrize("case", ["adam", "sgd"])
+def test_state_memory(case):
+    """8-bit state bytes: 1 B per param and state plus 4 B per block and state
+    (2 + 8/B for Adam, 1 + 4/B for Momentum), against 8 and 4 for fp32 states."""
+    B = 2048
+    params = init_params(3)
+    for p in params:
+        p.grad = torch.zeros_like(p)
+    opt = (optim.Adam8bit(params, blocksize=B) if case == "adam"
+           else optim.SGD8bit(params, lr=0.1, blocksize=B))
+    say(f"optim state memory {case}")
+    opt.step()
+    torch.cuda.synchronize()
+    nstates = 2 if case == "adam" else 1
+    for p in params:
+        st = opt.state[p]
+        nbytes = sum(t.numel() * t.element_size() for t in st.values()
+                     if isinstance(t, torch.Tensor))
+        n = p.numel()
+        assert nbytes == nstates * (n + 4 * ((n + B - 1) // B)), (case, n, nbytes)

@@ -233,3 +233,35 @@ def test_exact_thresholds_for_uneven_maps():
             blk[-1] = 1.0
             blocks.append(blk)
         run_pair(qm, dev(qm), np.concatenate(blocks), B)
+
+
+@pytest.mark.parametrize("B", [256, 2048])
+def test_block_isolation_on_gpu(B):
+    """Changing one block's values changes only that block's codes and absmax
+    (each block is normalized by its own absmax, Section 3.1)."""
+    qs, _, qs_d, _ = codebooks_on_device()
+    n = 9 * 8192 + 333
+    x = workloads.student_t_host(n, seed=77)
+    prep = bq.bq_prepare_codebook(qs_d)
+    say(f"block isolation B={B}")
+    c0, a0 = bq.bq_quantize_blockwise_prepared(prep, dev(x), B)
+    r0, s0 = bq.bq_quantize_blockwise(qs_d, dev(x), B)
+    nb = (n + B - 1) // B
+    for b in (0, nb // 2, nb - 1):
+        y = x.copy()
+        s = slice(b * B, min((b + 1) * B, n))
+        y[s] = y[s] * np.float32(-3.0) + np.float32(1e-3)
+        c1, a1 = bq.bq_quantize_blockwise_prepared(prep, dev(y), B)
+        r1, s1 = bq.bq_quantize_blockwise(qs_d, dev(y), B)
+        torch.cuda.synchronize()
+        for (ca, aa), (cb, ab) in (((c0, a0), (c1, a1)), ((r0, s0), (r1, s1))):
+            ca, cb, aa, ab = host(ca), host(cb), host(aa), host(ab)
+            keep = np.ones(n, bool)
+            keep[s] = False
+            np.testing.assert_array_equal(ca[keep], cb[keep])
+            others = np.arange(nb) != b
+            np.testing.assert_array_equal(aa[others], ab[others])
+            assert aa[b] != ab[b]
+            ref_c, ref_a = oracle.quantize_blockwise(qs, np.ascontiguousarray(y[s]), B)
+            np.testing.assert_array_equal(cb[s], ref_c)
+            assert ab[b] == ref_a[0]
