@@ -238,3 +238,55 @@ def test_trust_ratio_optimizers(opt, grad_dtype, B):
     """LAMB and LARS through plans (norm pass, per-tensor rates, step), over a
     ragged list of tensors, 4 steps free-running."""
     run_lists(opt, B, grad_dtype, RAGGED, steps=4, path="plan")
+
+
+@pytest.mark.parametrize("path,opt", [("plan", "adam"), ("call", "adam"), ("plan", "lamb"),
+                                      ("call", "momentum")])
+def test_steps_follow_the_callers_stream(path, opt):
+    """Every launch of a step goes to the stream the caller passes.  The side
+    stream is held back by a spin kernel before each step, and the step's
+    grads are written on it just before the step: a launch on any other
+    stream would run first and read stale grads."""
+    if not hasattr(torch.cuda, "_sleep"):
+        pytest.skip("torch.cuda._sleep not available")
+    B = 2048
+    sizes = [5000, 3 * 2048 + 1]
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    two = opt in ("adam", "adamw", "lamb")
+    hp = dict(HPS[opt])
+    hs, ds = [], []
+    for i, n in enumerate(sizes):
+        w = np.random.default_rng([31, i]).uniform(-0.05, 0.05, n).astype(np.float32)
+        hs.append(HostState(w, B, two))
+        ds.append(DevState(w, B, two, torch.float16))
+        ds[-1].g.zero_()
+    gh = {(t, i): (np.random.default_rng([31, i, t]).standard_normal(n) * 1e-3).astype(np.float16)
+          for t in (1, 2, 3) for i, n in enumerate(sizes)}
+    gd = {k: torch.from_numpy(v).cuda() for k, v in gh.items()}
+    rows = [d.row() for d in ds]
+    plan = bq.StepPlan(opt, B, bq.BQ_F16, rows) if path == "plan" else None
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        for t in (1, 2, 3):
+            torch.cuda._sleep(20_000_000)
+            for i in range(len(sizes)):
+                ds[i].g.copy_(gd[(t, i)])
+            say(f"step on a side stream: {path} {opt} t={t}")
+            if plan is not None:
+                plan.run(dict(hp, step=t), qs_d, qu_d if two else None, stream=s)
+            else:
+                bq.bq_optimizer8bit_step(opt, B, bq.BQ_F16, rows, dict(hp, step=t), qs_d,
+                                         qu_d if two else None, stream=s)
+    s.synchronize()
+    for t in (1, 2, 3):
+        for i in range(len(sizes)):
+            hs[i].step(opt, B, gh[(t, i)], qs, qu if two else None, hp, t)
+    for i in range(len(sizes)):
+        ok, worst = param_close(host(ds[i].w), hs[i].w, hs[i].tol)
+        assert ok, (path, opt, i, worst)
+        np.testing.assert_array_equal(host(ds[i].c1), hs[i].c1)
+        np.testing.assert_array_equal(host(ds[i].a1).view(np.uint32), hs[i].a1.view(np.uint32))
+        if two:
+            np.testing.assert_array_equal(host(ds[i].c2), hs[i].c2)
+            np.testing.assert_array_equal(host(ds[i].a2).view(np.uint32), hs[i].a2.view(np.uint32))
