@@ -300,7 +300,8 @@ typedef struct bq_step_plan_s *bq_step_plan;
  * per tile (4096 elements; pointers at the tile's first element and block) to
  * device memory of the current device -- 16 bytes per 1,024 params -- and
  * reserves space for two prepared codebooks (and, for LAMB and LARS, 16 bytes
- * of partial norms per tile and one rate per tensor).
+ * of partial norms per tile, 32 bytes per segment of up to 2048 tiles of one
+ * tensor, and 12 bytes per tensor).
  * Besides the optimizers of bq_optimizer8bit_step, plans run (App. E lists
  * 8-bit versions of both; textbook forms, one trust ratio per tensor, from
  * the norms before the update, 1 when a norm is zero):
@@ -309,7 +310,8 @@ typedef struct bq_step_plan_s *bq_step_plan;
  *         w' = w - lr (|w| / |u|) u   (states: signed and unsigned maps)
  *   LARS: g' = g + wd w;  m' = b1 m + lr (trust |w| / (|g| + wd |w|)) g';
  *         w' = w - m'   (one state; trust = hp->trust_coeff)
- * Each run first takes the norms in an extra pass over the tensors.
+ * Each run first takes the norms in an extra pass over the tensors; the sums
+ * are formed in a fixed order, so a run is deterministic.
  * Synchronous.  The tensors' buffers must stay valid while the plan is used.
  *   tensors  host array of ntensors descriptors (as bq_optimizer8bit_step)
  *   plan     receives the handle (NULL on error)

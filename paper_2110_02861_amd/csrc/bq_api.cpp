@@ -2,6 +2,7 @@
 // per-step scalar precomputation, packing of tensor descriptors (kernel-argument
 // chunks, or a device-resident plan), and launches.  Every check runs before
 // the first HIP call, so an error return means nothing was enqueued.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -131,10 +132,14 @@ struct bq_step_plan_s {
     int64_t total_tiles;
     bq::TensorDesc *tiles;  // device, one record per tile
     uint8_t *tables;        // device, two prepared maps
-    // LAMB / LARS: per-tile partial norms, per-tensor lr * ratio, tile ranges
+    // LAMB / LARS: per-tile partial norms, segment tile ranges and partial
+    // sums, each tensor's first segment, per-tensor lr * ratio
     double *partials;
+    int64_t *seg_range;
+    double *seg_partials;
+    int64_t *first_seg;
     float *lr_ratio;
-    int64_t *first_tile;
+    int64_t nsegments;
 };
 
 extern "C" {
@@ -452,6 +457,18 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
         }
     }
     first_tile.push_back((int64_t)recs.size());
+    // segments of at most kTrustSegTiles tiles, never across tensors
+    std::vector<int64_t> seg_range, first_seg;
+    if (trust) {
+        for (size_t t = 0; t + 1 < first_tile.size(); ++t) {
+            first_seg.push_back((int64_t)seg_range.size() / 2);
+            for (int64_t k = first_tile[t]; k < first_tile[t + 1]; k += bq::kTrustSegTiles) {
+                seg_range.push_back(k);
+                seg_range.push_back(std::min(k + bq::kTrustSegTiles, first_tile[t + 1]));
+            }
+        }
+        first_seg.push_back((int64_t)seg_range.size() / 2);
+    }
 
     bq_step_plan_s *p = new (std::nothrow) bq_step_plan_s();
     if (!p)
@@ -461,6 +478,7 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
     p->grad_dtype = grad_dtype;
     p->ntensors = nonempty;
     p->total_tiles = (int64_t)recs.size();
+    p->nsegments = (int64_t)seg_range.size() / 2;
     hipError_t e = hipGetDevice(&p->device);
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&p->tables), 2 * bq::kPreparedBytes);
@@ -475,10 +493,19 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
                 e = hipMalloc(reinterpret_cast<void **>(&p->lr_ratio),
                               (size_t)nonempty * sizeof(float));
             if (e == hipSuccess)
-                e = hipMalloc(reinterpret_cast<void **>(&p->first_tile),
-                              first_tile.size() * sizeof(int64_t));
+                e = hipMalloc(reinterpret_cast<void **>(&p->seg_partials),
+                              (size_t)p->nsegments * 2 * sizeof(double));
             if (e == hipSuccess)
-                e = hipMemcpy(p->first_tile, first_tile.data(), first_tile.size() * sizeof(int64_t),
+                e = hipMalloc(reinterpret_cast<void **>(&p->seg_range),
+                              seg_range.size() * sizeof(int64_t));
+            if (e == hipSuccess)
+                e = hipMemcpy(p->seg_range, seg_range.data(), seg_range.size() * sizeof(int64_t),
+                              hipMemcpyHostToDevice);
+            if (e == hipSuccess)
+                e = hipMalloc(reinterpret_cast<void **>(&p->first_seg),
+                              first_seg.size() * sizeof(int64_t));
+            if (e == hipSuccess)
+                e = hipMemcpy(p->first_seg, first_seg.data(), first_seg.size() * sizeof(int64_t),
                               hipMemcpyHostToDevice);
         }
     }
@@ -515,9 +542,12 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
     a.tables = plan->tables;
     a.tiles = plan->tiles;
     a.partials = plan->partials;
+    a.seg_range = plan->seg_range;
+    a.seg_partials = plan->seg_partials;
+    a.first_seg = plan->first_seg;
     a.lr_ratio = plan->lr_ratio;
-    a.first_tile = plan->first_tile;
     a.ntensors = plan->ntensors;
+    a.nsegments = (int32_t)plan->nsegments;
     a.sc = make_scalars(*hp, plan->opt);
     // decoupled decay for AdamW, inside the update direction for LAMB, an L2
     // term on the gradient otherwise
@@ -541,7 +571,8 @@ bq_status bq_step_plan_destroy(bq_step_plan plan)
     hipError_t e = hipSuccess;
     for (void *ptr : {static_cast<void *>(plan->tiles), static_cast<void *>(plan->tables),
                       static_cast<void *>(plan->partials), static_cast<void *>(plan->lr_ratio),
-                      static_cast<void *>(plan->first_tile)}) {
+                      static_cast<void *>(plan->seg_range), static_cast<void *>(plan->seg_partials),
+                      static_cast<void *>(plan->first_seg)}) {
         if (ptr && hipFree(ptr) != hipSuccess)
             e = hipErrorUnknown;
     }

@@ -108,14 +108,19 @@ struct PlanArgs {
     StepScalars sc;
     int32_t use_wd;
     int32_t total_tiles;
-    // LAMB / LARS only: per-tile partial squared norms (2 doubles per tile),
-    // per-tensor lr * trust ratio, first tile of each tensor (ntensors + 1)
+    // LAMB / LARS only: per-tile partial squared norms (2 doubles per tile);
+    // each tensor's tiles cut into segments of at most kTrustSegTiles tiles:
+    // per segment its tile range [begin, end) and its 2 partial sums; first
+    // segment of each tensor (ntensors + 1); per-tensor lr * trust ratio
     double *partials;
+    const int64_t *seg_range;
+    double *seg_partials;
+    const int64_t *first_seg;
     float *lr_ratio;
-    const int64_t *first_tile;
     int32_t ntensors;
-    int32_t pad;
+    int32_t nsegments;
 };
+constexpr int64_t kTrustSegTiles = 2048;
 
 // One tensor of a 32-bit-state launch (states are fp32 arrays).
 struct Desc32 {

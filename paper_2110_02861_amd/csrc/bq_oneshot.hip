@@ -691,19 +691,20 @@ __global__ __launch_bounds__(kST) void norms_kernel(const PlanArgs a)
     }
 }
 
-// One workgroup per tensor: thread t sums the partials of the tensor's tiles
-// t, t + 256, ... in order, the 256 thread sums are combined by a fixed tree,
-// then lr * ratio, ratio = |w| / |u| (LAMB) or trust |w| / (|g| + wd |w|)
-// (LARS), 1 when either norm is zero.  The order depends on the tile count
-// only, so the result is deterministic.
+// Per-tensor rates from the per-tile partial sums in two steps, each in a
+// fixed order (so the result is deterministic): one workgroup per segment of at
+// most kTrustSegTiles tiles of one tensor sums them (thread t takes tiles t,
+// t + 256, ... in order, then a fixed tree); one thread per tensor sums its
+// segments in order and forms lr * ratio, ratio = |w| / |u| (LAMB) or
+// trust |w| / (|g| + wd |w|) (LARS), 1 when either norm is zero.
 constexpr int kTrustThreads = 256;
 
-__global__ __launch_bounds__(kTrustThreads) void trust_ratio_kernel(const PlanArgs a, int lamb)
+__global__ __launch_bounds__(kTrustThreads) void segment_sums_kernel(const PlanArgs a)
 {
     __shared__ double rw[kTrustThreads], rx[kTrustThreads];
-    const int t = blockIdx.x;
+    const int64_t sg = blockIdx.x;
     const int tid = threadIdx.x;
-    const int64_t k0 = G(a.first_tile)[t], k1 = G(a.first_tile)[t + 1];
+    const int64_t k0 = G(a.seg_range)[2 * sg], k1 = G(a.seg_range)[2 * sg + 1];
     double sw = 0.0, sx = 0.0;
     for (int64_t k = k0 + tid; k < k1; k += kTrustThreads) {
         sw += G(a.partials)[2 * k];
@@ -720,12 +721,27 @@ __global__ __launch_bounds__(kTrustThreads) void trust_ratio_kernel(const PlanAr
         __syncthreads();
     }
     if (tid == 0) {
-        const double nw = sqrt(rw[0]), nx = sqrt(rx[0]);
-        double ratio = 1.0;
-        if (nw > 0.0 && nx > 0.0)
-            ratio = lamb ? nw / nx : (double)a.sc.trust * nw / (nx + (double)a.sc.wd * nw);
-        G(a.lr_ratio)[t] = (float)((double)a.sc.lr * ratio);
+        G(a.seg_partials)[2 * sg] = rw[0];
+        G(a.seg_partials)[2 * sg + 1] = rx[0];
     }
+}
+
+__global__ __launch_bounds__(kTrustThreads) void trust_ratio_kernel(const PlanArgs a, int lamb)
+{
+    const int t = blockIdx.x * kTrustThreads + threadIdx.x;
+    if (t >= a.ntensors)
+        return;
+    const int64_t s0 = G(a.first_seg)[t], s1 = G(a.first_seg)[t + 1];
+    double sw = 0.0, sx = 0.0;
+    for (int64_t sg = s0; sg < s1; ++sg) {
+        sw += G(a.seg_partials)[2 * sg];
+        sx += G(a.seg_partials)[2 * sg + 1];
+    }
+    const double nw = sqrt(sw), nx = sqrt(sx);
+    double ratio = 1.0;
+    if (nw > 0.0 && nx > 0.0)
+        ratio = lamb ? nw / nx : (double)a.sc.trust * nw / (nx + (double)a.sc.wd * nw);
+    G(a.lr_ratio)[t] = (float)((double)a.sc.lr * ratio);
 }
 
 // ---------------------------------------------------------------------------
@@ -1120,8 +1136,11 @@ hipError_t launch_trust_ratios(int opt, int grad_dtype, int blocksize, const Pla
     }
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(trust_ratio_kernel, dim3((unsigned)a.ntensors), dim3(kTrustThreads), 0,
-                       stream, a, opt == kLamb ? 1 : 0);
+    hipLaunchKernelGGL(segment_sums_kernel, dim3((unsigned)a.nsegments), dim3(kTrustThreads), 0,
+                       stream, a);
+    hipLaunchKernelGGL(trust_ratio_kernel,
+                       dim3((unsigned)((a.ntensors + kTrustThreads - 1) / kTrustThreads)),
+                       dim3(kTrustThreads), 0, stream, a, opt == kLamb ? 1 : 0);
     return hipGetLastError();
 }
 

@@ -26,7 +26,7 @@ C3 = dict(opt="momentum", lr=0.1, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4, blocks
 C4 = dict(opt="adamw", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.01, blocksize=2048)
 C5 = dict(opt="adam", lr=1e-3, beta1=0.9, beta2=0.995, eps=1e-8, wd=0.0, blocksize=2048)
 
-CONFIG_IDS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
+CONFIG_IDS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5, "p1b": 6}
 
 
 @dataclass(frozen=True)
@@ -116,7 +116,14 @@ def c1_specs():
     return [TensorSpec("w", (1_048_576,), "uniform", 0.05)]
 
 
-SPECS = {"c1": c1_specs, "c3": resnet50_specs, "c4": gpt2_medium_specs, "c5": lm_1p5b_specs}
+def paper_1b_specs():
+    """The setup of the paper's isolated optimizer timing (App. E): one large
+    sample of a normal distribution, here 10^9 values, with fp32 gradients."""
+    return [TensorSpec("w", (1_000_000_000,), "normal", 1.0)]
+
+
+SPECS = {"c1": c1_specs, "c3": resnet50_specs, "c4": gpt2_medium_specs, "c5": lm_1p5b_specs,
+         "p1b": paper_1b_specs}
 
 # Gradient distributions per configuration: (dtype, std, outlier prob, outlier factor).
 GRADS = {
@@ -124,6 +131,7 @@ GRADS = {
     "c3": ("float32", 1e-3, 0.0, 1.0),
     "c4": ("float16", 1e-4, 0.0, 1.0),
     "c5": ("float16", 1e-4, 1e-4, 1000.0),
+    "p1b": ("float32", 1.0, 0.0, 1.0),
 }
 
 

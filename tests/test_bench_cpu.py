@@ -55,3 +55,16 @@ def test_byte_model_of_the_norm_pass():
     assert bench.workload_bytes("lm1p5b-lars", c5, 2048, 2) == 18 * n + 8 * nb
     assert bench.workload_bytes("lm1p5b-adagrad", c5, 2048, 2) == 12 * n + 8 * nb
     assert bench.workload_bytes("lm1p5b-adam", c5, 2048, 2) == bench.step_bytes(c5, 2048, 2, 2)
+
+
+def test_byte_model_of_the_paper_setup():
+    """One tensor of 10^9 params with fp32 grads: Adam 16 B/param (the paper's
+    setup), LAMB's norm pass reads w, the fp32 grad and both codes again."""
+    p = [s.numel for s in workloads.paper_1b_specs()]
+    n = 10 ** 9
+    nb = (n + 2047) // 2048
+    assert p == [n]
+    assert bench.workload_bytes("paper1b-adam", p, 2048, 4) == 16 * n + 16 * nb
+    assert bench.workload_bytes("paper1b-momentum", p, 2048, 4) == 14 * n + 8 * nb
+    assert bench.workload_bytes("paper1b-lamb", p, 2048, 4) == (16 + 10) * n + 24 * nb
+    assert bench.workload_bytes("paper1b-lars", p, 2048, 4) == (14 + 8) * n + 8 * nb

@@ -290,3 +290,12 @@ def test_steps_follow_the_callers_stream(path, opt):
         if two:
             np.testing.assert_array_equal(host(ds[i].c2), hs[i].c2)
             np.testing.assert_array_equal(host(ds[i].a2).view(np.uint32), hs[i].a2.view(np.uint32))
+
+
+@pytest.mark.parametrize("opt", ["lamb", "lars"])
+def test_trust_ratio_over_several_segments(opt):
+    """A tensor of more than 2 x 2048 tiles: its norm sums run over three
+    segments (each tensor's tiles are summed in segments of at most 2048
+    tiles, then the segments in order), next to a small tensor."""
+    n_big = 2 * 2048 * 4096 + 12345
+    run_lists(opt, 2048, bq.BQ_F16, [n_big, 777], steps=2, path="plan")
