@@ -733,7 +733,21 @@ __global__ __launch_bounds__(kTrustThreads) void trust_ratio_kernel(const PlanAr
         return;
     const int64_t s0 = G(a.first_seg)[t], s1 = G(a.first_seg)[t + 1];
     double sw = 0.0, sx = 0.0;
-    for (int64_t sg = s0; sg < s1; ++sg) {
+    int64_t sg = s0;
+    for (; sg + 16 <= s1; sg += 16) {  // in order; loads issued 16 at a time
+        double vw[16], vx[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            vw[k] = G(a.seg_partials)[2 * (sg + k)];
+            vx[k] = G(a.seg_partials)[2 * (sg + k) + 1];
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            sw += vw[k];
+            sx += vx[k];
+        }
+    }
+    for (; sg < s1; ++sg) {
         sw += G(a.seg_partials)[2 * sg];
         sx += G(a.seg_partials)[2 * sg + 1];
     }
