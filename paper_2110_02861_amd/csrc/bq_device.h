@@ -231,28 +231,6 @@ __device__ inline float normalize(const Normalizer &z, float x)
     return __builtin_fmaf(e, z.r, q);
 }
 
-// Requantize N values of one thread against map M with block absmax A.
-// GROUP >= 64 means a wave lies inside one block (A is wave-uniform).
-template <int N, int GROUP, bool NONNEG>
-__device__ inline void requantize(const Tables &M, float A, const float (&x)[N], uint32_t (&c)[N])
-{
-    const Normalizer z = make_normalizer(A);
-    bool scaled = (z.s != 1.0f);
-    if constexpr (GROUP >= 64)
-        scaled = __builtin_amdgcn_readfirstlane((int)scaled) != 0;
-    float y[N];
-    if (!scaled) {
-#pragma unroll
-        for (int i = 0; i < N; ++i)
-            y[i] = normalize<false>(z, x[i]);
-    } else {
-#pragma unroll
-        for (int i = 0; i < N; ++i)
-            y[i] = normalize<true>(z, x[i]);
-    }
-    nearest_codes<N, NONNEG>(M, y, c);
-}
-
 // ---------------------------------------------------------------------------
 // Reductions
 // ---------------------------------------------------------------------------
@@ -276,67 +254,6 @@ __device__ inline uint32_t row_umax(uint32_t v)
     v = dpp_umax<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
     v = dpp_umax<0x141, 0xf>(v);  // row_half_mirror
     return dpp_umax<0x140, 0xf>(v);  // row_mirror
-}
-
-// Max of non-negative bit patterns over the wave, valid in lane 63 only.
-__device__ inline uint32_t wave_umax_lane63(uint32_t v)
-{
-    v = dpp_umax<0xb1, 0xf>(v);   // quad_perm [1,0,3,2]
-    v = dpp_umax<0x4e, 0xf>(v);   // quad_perm [2,3,0,1]
-    v = dpp_umax<0x141, 0xf>(v);  // row_half_mirror
-    v = dpp_umax<0x140, 0xf>(v);  // row_mirror: every lane holds its row max
-    v = dpp_umax<0x142, 0xa>(v);  // row_bcast:15 -> rows 1, 3 hold pair maxima
-    v = dpp_umax<0x143, 0xc>(v);  // row_bcast:31 -> lane 63 holds the wave max
-    return v;
-}
-
-// Max of non-negative (x, y) over each group of GROUP consecutive threads
-// (power of two, 32..1024), returned to every thread of the group.  slots: LDS
-// scratch of (threads / 64) float2 not in use by another reduction of the same
-// workgroup.  Contains a barrier when GROUP > 64.
-template <int GROUP>
-__device__ inline float2 group_max(float2 v, float2 *slots)
-{
-    uint32_t x = __float_as_uint(v.x), y = __float_as_uint(v.y);
-    x = dpp_umax<0xb1, 0xf>(x);
-    y = dpp_umax<0xb1, 0xf>(y);
-    x = dpp_umax<0x4e, 0xf>(x);
-    y = dpp_umax<0x4e, 0xf>(y);
-    x = dpp_umax<0x141, 0xf>(x);
-    y = dpp_umax<0x141, 0xf>(y);
-    x = dpp_umax<0x140, 0xf>(x);
-    y = dpp_umax<0x140, 0xf>(y);
-    x = dpp_umax<0x142, 0xa>(x);  // row_bcast:15 -> lanes 31, 63 hold half maxima
-    y = dpp_umax<0x142, 0xa>(y);
-    if constexpr (GROUP == 32) {
-        const bool hi = (threadIdx.x & 32) != 0;
-        const uint32_t x31 = __builtin_amdgcn_readlane(x, 31), x63 = __builtin_amdgcn_readlane(x, 63);
-        const uint32_t y31 = __builtin_amdgcn_readlane(y, 31), y63 = __builtin_amdgcn_readlane(y, 63);
-        return make_float2(__uint_as_float(hi ? x63 : x31), __uint_as_float(hi ? y63 : y31));
-    } else {
-        x = dpp_umax<0x143, 0xc>(x);  // row_bcast:31 -> lane 63 holds the wave max
-        y = dpp_umax<0x143, 0xc>(y);
-        const float2 w = make_float2(__uint_as_float(__builtin_amdgcn_readlane(x, 63)),
-                                     __uint_as_float(__builtin_amdgcn_readlane(y, 63)));
-        if constexpr (GROUP == 64) {
-            return w;
-        } else {
-            constexpr int WPG = GROUP / 64;
-            const int wave = threadIdx.x >> 6;
-            if ((threadIdx.x & 63) == 0)
-                slots[wave] = w;
-            __syncthreads();
-            const int first = (wave / WPG) * WPG;
-            float2 r = slots[first];
-#pragma unroll
-            for (int k = 1; k < WPG; ++k) {
-                const float2 o = slots[first + k];
-                r.x = fmaxf(r.x, o.x);
-                r.y = fmaxf(r.y, o.y);
-            }
-            return r;
-        }
-    }
 }
 
 // ---------------------------------------------------------------------------

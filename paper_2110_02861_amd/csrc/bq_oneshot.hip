@@ -1,13 +1,20 @@
-// One-shot kernels for gfx950: one workgroup of 512 threads per tile, chunks
-// of 2048 elements with 4 contiguous elements per thread, wave-contiguous
-// non-temporal loads and stores (4096-element tiles for the step, 8192 for
-// quantize, 4096 for dequantize).  The decision tables of each
-// codebook are built once per call by prepare_kernel into a prepared-codebook
-// buffer and copied from there (L2) into LDS by every workgroup.
+// Kernels of the fused 8-bit step, block-wise quantize / dequantize and the
+// LAMB / LARS norm pass, for gfx950.
 //
-// On MI355X this shape streams the step's byte mix (read 4 + 2 + 1 + 1 B,
-// write 4 + 1 + 1 B per element) markedly faster than persistent workgroups
-// walking a strided tile list, which is why the hot path is organised this way.
+// One-shot kernels (step plans, prepared codebooks): one workgroup of 512
+// threads per tile, chunks of 2048 elements with 4 contiguous elements per
+// thread, wave-contiguous non-temporal loads and stores (4096-element tiles
+// for the step, 8192 for quantize, 4096 for dequantize).  The decision tables
+// of each codebook are built once per call by prepare_kernel into a
+// prepared-codebook buffer and copied from there (L2) into LDS by every
+// workgroup.  On MI355X this shape streams the step's byte mix (read 4 + 2 +
+// 1 + 1 B, write 4 + 1 + 1 B per element) faster than persistent workgroups,
+// which is why the hot path is organised this way.
+//
+// Persistent kernels (the allocation-free calls, which get only the raw
+// maps): every workgroup builds the tables in its own LDS once and then runs
+// the same tile code (StepOS::tile, QuantOS::tile) over a grid-stride list of
+// tiles.
 #include "bq_device.h"
 
 namespace bq {
