@@ -14,6 +14,11 @@
  * written in float, in the operation order stated next to each function.
  *
  * Readings of points the paper leaves open are marked "Reading:" below.
+ *
+ * Parity unpinned: the exact values of the dynamic and inverse dynamic maps.
+ * The paper's figure of the bit layout is missing, so the values below are a
+ * reading of its text; the tests pin their structure (values per decade, the
+ * 10^-7 .. 1 range, 0 and +-1 present, strictly increasing), not the values.
  */
 #include <math.h>
 #include <stdint.h>
