@@ -80,9 +80,7 @@ bq_status from_hip(hipError_t e) { return e == hipSuccess ? BQ_OK : BQ_ERR_HIP; 
 // Checks every descriptor of a tensor list (no HIP call).
 bq_status check_tensors(const bq_tensor *tensors, int32_t ntensors, int32_t blocksize, bool two)
 {
-    const int64_t tile = bq::tile_elems(blocksize) < bq::step_tile(blocksize)
-                             ? bq::tile_elems(blocksize)
-                             : bq::step_tile(blocksize);
+    const int64_t tile = bq::step_tile(blocksize);
     for (int32_t i = 0; i < ntensors; ++i) {
         const bq_tensor &t = tensors[i];
         if (t.numel < 0)

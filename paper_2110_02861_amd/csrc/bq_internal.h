@@ -55,10 +55,6 @@ struct StepArgs {
 };
 static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must stay below 4 KiB");
 
-// Elements per tile (one workgroup iteration) for a given blocksize, for the
-// persistent kernels and the one-shot quantize kernel.
-constexpr int tile_elems(int blocksize) { return blocksize >= 2048 ? blocksize : 2048; }
-
 // Elements per tile of the prepared-codebook quantize kernel: kQuantChunks
 // chunks of 2048 (512 threads x 4 elements), or one block when the block is
 // larger; of the dequantize kernel: kDequantChunks chunks of 2048.  (Measured
