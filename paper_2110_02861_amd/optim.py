@@ -4,18 +4,20 @@ The paper's 8-bit optimizers replace their 32-bit counterparts without
 hyperparameter changes (Section 1, Section 4): Adam (Eq. 2 with bias
 correction), AdamW, SGD with momentum (Eq. 1), and AdaGrad (App. H); LAMB and
 LARS, whose 8-bit versions App. E times, in their textbook forms (per-tensor
-trust ratios, which need a norm pass and therefore step plans).  Each state is stored as one
-uint8 code per element plus one fp32 absmax per block of ``blocksize`` elements
-(Section 3.1); the signed dynamic map holds the first state and the unsigned
-dynamic map the second (Section 3.2); AdaGrad's single, non-negative state
-(the running sum of squared gradients) uses the unsigned map.  Tensors can keep 32-bit states instead:
-Section 3.3 keeps the embedding layer's states in 32 bit, and tensors below
-``min_8bit_size`` elements may be exempted as well.
+trust ratios, which need a norm pass and therefore step plans).  Each state is
+stored as one uint8 code per element plus one fp32 absmax per block of
+``blocksize`` elements (Section 3.1); the signed dynamic map holds the first
+state and the unsigned dynamic map the second (Section 3.2); AdaGrad's single,
+non-negative state (the running sum of squared gradients) uses the unsigned
+map.  Tensors can keep 32-bit states instead: Section 3.3 keeps the embedding
+layer's states in 32 bit (``override_32bit``, or the weight of
+``nn.StableEmbedding``), and tensors below ``min_8bit_size`` elements may be
+exempted as well.
 
 Every update runs in the HIP kernels of libbq:
-- 8-bit tensors go through a cached step plan (``bq_step_plan_run``: one launch
-  over every tile of every tensor), rebuilt whenever a tensor's storage moves,
-  or through ``bq_optimizer8bit_step`` when ``use_plans=False``;
+- 8-bit tensors go through a step plan (``bq_step_plan_run``: one launch over
+  every tile of every tensor), looked up by every storage pointer and size, or
+  through ``bq_optimizer8bit_step`` when ``use_plans=False``;
 - 32-bit tensors go through ``bq_optimizer32bit_step``.
 
 Params must be fp32 CUDA tensors, contiguous and 16-byte aligned; grads fp32 or
@@ -72,7 +74,9 @@ class Optimizer8bit(torch.optim.Optimizer):
         self._override32.add(id(param))
 
     def _is_8bit(self, p: torch.Tensor) -> bool:
-        return id(p) not in self._override32 and p.numel() >= self.min_8bit_size
+        # a weight flagged bq_32bit_state (nn.StableEmbedding) keeps 32-bit states
+        return (id(p) not in self._override32 and not getattr(p, "bq_32bit_state", False)
+                and p.numel() >= self.min_8bit_size)
 
     # -- hyperparameters of one group (subclasses) ------------------------------
 

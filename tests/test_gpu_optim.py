@@ -320,3 +320,32 @@ def test_state_memory(case):
                      if isinstance(t, torch.Tensor))
         n = p.numel()
         assert nbytes == nstates * (n + 4 * ((n + B - 1) // B)), (case, n, nbytes)
+
+
+def test_stable_embedding_states_are_32_bit():
+    """nn.StableEmbedding's weight gets fp32 states (the oracle's 32-bit step),
+    the other params 8-bit states, in one optimizer step."""
+    from paper_2110_02861_amd import nn
+    torch.manual_seed(3)
+    emb = nn.StableEmbedding(3000, 64).cuda()
+    lin = torch.nn.Linear(64, 64).cuda()
+    opt = optim.Adam8bit(list(emb.parameters()) + list(lin.parameters()), lr=1e-3)
+    w0 = emb.weight.detach().cpu().numpy().copy()
+    tokens = torch.randint(0, 3000, (16, 32), device="cuda")
+    lin(emb(tokens)).square().mean().backward()
+    g = emb.weight.grad.detach().cpu().numpy().copy()
+    say("optim stable embedding step")
+    opt.step()
+    torch.cuda.synchronize()
+    st = opt.state[emb.weight]
+    assert "exp_avg" in st and "state1" not in st
+    assert "state1" in opt.state[lin.weight]
+    m = np.zeros(w0.size, np.float32)
+    v = np.zeros(w0.size, np.float32)
+    w = w0.reshape(-1).copy()
+    oracle.step32(oracle.ADAM, w, g.reshape(-1), m, v, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1)
+    np.testing.assert_array_equal(host(st["exp_avg"]).view(np.uint32), m.view(np.uint32))
+    np.testing.assert_array_equal(host(st["exp_avg_sq"]).view(np.uint32), v.view(np.uint32))
+    ok, worst = param_close(host(emb.weight).reshape(-1), w,
+                            1e-6 * np.abs(w0.reshape(-1).astype(np.float64) - w))
+    assert ok, worst
