@@ -299,3 +299,45 @@ def test_trust_ratio_over_several_segments(opt):
     tiles, then the segments in order), next to a small tensor."""
     n_big = 2 * 2048 * 4096 + 12345
     run_lists(opt, 2048, bq.BQ_F16, [n_big, 777], steps=2, path="plan")
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("opt", ["adam", "adamw", "momentum"])
+def test_zero_learning_rate_keeps_params(opt, path):
+    """lr = 0 (the first step of a warm-up schedule): params stay bit-identical,
+    the states still update, codes and absmax as the oracle's."""
+    B = 2048
+    sizes = [5000, 2049]
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    two = opt in ("adam", "adamw")
+    hp = dict(HPS[opt], lr=0.0)
+    hs, ds, w0 = [], [], []
+    for i, n in enumerate(sizes):
+        w = np.random.default_rng([41, i]).uniform(-0.05, 0.05, n).astype(np.float32)
+        w0.append(w.copy())
+        hs.append(HostState(w, B, two))
+        ds.append(DevState(w, B, two, torch.float16))
+    rows = [d.row() for d in ds]
+    plan = bq.StepPlan(opt, B, bq.BQ_F16, rows) if path == "plan" else None
+    for t in (1, 2):
+        gs = [(np.random.default_rng([41, i, t]).standard_normal(n) * 1e-3).astype(np.float16)
+              for i, n in enumerate(sizes)]
+        for d, g in zip(ds, gs):
+            d.g.copy_(torch.from_numpy(g))
+        say(f"lr=0 step {path} {opt} t={t}")
+        if plan is not None:
+            plan.run(dict(hp, step=t), qs_d, qu_d if two else None)
+        else:
+            bq.bq_optimizer8bit_step(opt, B, bq.BQ_F16, rows, dict(hp, step=t), qs_d,
+                                     qu_d if two else None)
+        torch.cuda.synchronize()
+        for h, g in zip(hs, gs):
+            h.step(opt, B, g, qs, qu if two else None, hp, t)
+    for i in range(len(sizes)):
+        np.testing.assert_array_equal(host(ds[i].w).view(np.uint32), w0[i].view(np.uint32))
+        np.testing.assert_array_equal(hs[i].w.view(np.uint32), w0[i].view(np.uint32))
+        np.testing.assert_array_equal(host(ds[i].c1), hs[i].c1)
+        np.testing.assert_array_equal(host(ds[i].a1).view(np.uint32), hs[i].a1.view(np.uint32))
+        assert np.any(hs[i].c1 != (127 if opt != "adagrad" else 0))  # the state moved
+        if two:
+            np.testing.assert_array_equal(host(ds[i].c2), hs[i].c2)
