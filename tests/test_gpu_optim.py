@@ -349,3 +349,39 @@ def test_stable_embedding_states_are_32_bit():
     ok, worst = param_close(host(emb.weight).reshape(-1), w,
                             1e-6 * np.abs(w0.reshape(-1).astype(np.float64) - w))
     assert ok, worst
+
+
+@pytest.mark.parametrize("use_plans", [True, False])
+def test_param_groups_and_mixed_grad_dtypes(use_plans):
+    """Two param groups with their own lr, betas and weight decay, and fp16 and
+    fp32 grads inside one group: each param steps as the oracle with its group's
+    hyperparameters."""
+    params = init_params(11)
+    g0, g1 = params[:3], params[3:]
+    kw0 = dict(lr=1e-3, betas=(0.9, 0.995), eps=1e-8, weight_decay=0.0)
+    kw1 = dict(lr=3e-3, betas=(0.8, 0.99), eps=1e-7, weight_decay=0.05)
+    opt = optim.Adam8bit([dict(params=g0, **kw0), dict(params=g1, **kw1)], blocksize=B,
+                         use_plans=use_plans)
+    hps = [oracle_hp(kw0)] * 3 + [oracle_hp(kw1)] * 2
+    for t in range(1, 4):
+        # alternate the grad dtype per param and per step
+        gs = [g.astype(np.float16 if (i + t) % 2 else np.float32)
+              for i, g in enumerate(grads(11, t, np.float32))]
+        refs = [oracle_step8(oracle.ADAM, hp, host(p).ravel(), g.ravel(), snapshot(opt, p),
+                             p.numel(), True, t) for p, g, hp in zip(params, gs, hps)]
+        for p, g in zip(params, gs):
+            set_grad(p, g)
+        w_before = [host(p).ravel().astype(np.float64) for p in params]
+        say(f"optim two groups, mixed grad dtypes, plans={use_plans} step {t}")
+        opt.step()
+        torch.cuda.synchronize()
+        for i, (p, ref) in enumerate(zip(params, refs)):
+            s = opt.state[p]
+            w_ref, c1, a1, c2, a2 = ref
+            assert np.array_equal(host(s["state1"]), c1), (i, t)
+            assert np.array_equal(host(s["absmax1"]), a1), (i, t)
+            assert np.array_equal(host(s["state2"]), c2), (i, t)
+            assert np.array_equal(host(s["absmax2"]), a2), (i, t)
+            upd = np.abs(w_before[i] - w_ref.astype(np.float64))
+            ok, worst = param_close(host(p).ravel(), w_ref, 1e-6 * upd)
+            assert ok, (i, t, worst)
