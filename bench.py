@@ -388,6 +388,12 @@ def run_list(args, torch, bq, workloads):
 
         def step(i):
             plans[i % 2].run(dict(hp, step=i + 1), q1, q2, stream=stream)
+    elif args.path == "prepared":
+        plans = [bq.StepPlan(opt, B, gdt, r) for r in rows]
+        prepared = bq.prepare_codebook_pair(q1, q2, stream=stream)
+
+        def step(i):
+            plans[i % 2].run_prepared(dict(hp, step=i + 1), prepared, stream=stream)
     else:
         arrays = [(bq.make_tensor_array(r), len(r)) for r in rows]
 
@@ -424,7 +430,7 @@ def run_list(args, torch, bq, workloads):
             "traffic": measured_traffic(args.workload, B, args.path),
             "bytes_per_step": bytes_step,
             "kernel": kname + (" (+ prepare_kernel, ~7 us, inside the timed launch pair)"
-                               if args.path != "call" else ""),
+                               if args.path == "plan" else ""),
         },
         "stream_ceiling": None if ceiling is None else {
             "gbs": ceiling, "frac_of_peak": ceiling / HBM_PEAK_GBS,
@@ -445,8 +451,9 @@ def run_quant(args, torch, bq, workloads):
     """Standalone quantize or dequantize of 67,108,864 Student-t(3) x 1e-2
     values; four input / output buffer sets rotate so that no call finds its
     operands in the 256 MB last-level cache."""
-    if args.path == "optim":
-        print("--path optim applies to the optimizer-step workloads", file=sys.stderr)
+    if args.path in ("optim", "prepared"):
+        print(f"--path {args.path} applies to the optimizer-step workloads (the quantize plan "
+              "path already reads a codebook prepared once)", file=sys.stderr)
         sys.exit(2)
     B = args.blocksize
     n = QUANT_N
@@ -533,9 +540,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=16)
-    ap.add_argument("--path", choices=["plan", "call", "optim"], default="plan",
-                    help="plan: bq_step_plan_run (one launch over the whole list) or, for "
-                         "quantize, the prepared codebook; call: bq_optimizer8bit_step "
+    ap.add_argument("--path", choices=["plan", "prepared", "call", "optim"], default="plan",
+                    help="plan: bq_step_plan_run (a prepare launch from the raw maps, then one "
+                         "launch over the whole list) or, for quantize, the prepared codebook; "
+                         "prepared: bq_step_plan_run_prepared (the maps' tables prepared once, "
+                         "before the timed steps); call: bq_optimizer8bit_step "
                          "(descriptor chunks of 56 tensors) or bq_quantize_blockwise; optim: "
                          "the drop-in torch optimizer (Adam8bit / AdamW8bit / SGD8bit) with "
                          "the grads of the ring assigned to .grad before each step")

@@ -334,6 +334,25 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
 bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float *qmap1,
                            const float *qmap2, hipStream_t stream);
 
+/*
+ * bq_step_plan_run with codebooks prepared beforehand.  An optimizer's maps
+ * are fixed (the dynamic maps of Sections 2.3 and 3.2), so their tables can be
+ * prepared once and read by every step; the run then skips the prepare launch
+ * and leaves the plan's own codebook workspace untouched.  Results are
+ * identical, bit for bit, to bq_step_plan_run with the maps the tables were
+ * prepared from.
+ *   prepared  device, read, 16-byte aligned, owned by the caller: two prepared
+ *             codebooks back to back, state 1's map at `prepared` and state
+ *             2's at prepared + BQ_PREPARED_CODEBOOK_BYTES (one-state
+ *             optimizers read only the first), each written by
+ *             bq_prepare_codebook.  It must not change while a run that reads
+ *             it is in flight.
+ * Errors: BQ_ERR_NULL, BQ_ERR_ALIGN, BQ_ERR_ARG (step < 1, wrong device),
+ * BQ_ERR_HIP.
+ */
+bq_status bq_step_plan_run_prepared(bq_step_plan plan, const bq_hparams *hp, const void *prepared,
+                                    hipStream_t stream);
+
 /* Free a plan's device memory (synchronizes with the device).  NULL is a no-op. */
 bq_status bq_step_plan_destroy(bq_step_plan plan);
 

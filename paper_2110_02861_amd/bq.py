@@ -33,8 +33,8 @@ EXPORTS = ("bq_make_dynamic_codebook", "bq_make_codebook", "bq_make_quantile_cod
            "bq_quantize_blockwise", "bq_dequantize_blockwise",
            "bq_optimizer8bit_step", "bq_optimizer32bit_step", "bq_prepare_codebook",
            "bq_quantize_blockwise_prepared",
-           "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_destroy",
-           "bq_status_string")
+           "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_run_prepared",
+           "bq_step_plan_destroy", "bq_status_string")
 BQ_PREPARED_CODEBOOK_BYTES = 8720
 BQ_QUANTILE_CHUNK = 4096
 
@@ -102,6 +102,8 @@ def lib() -> ctypes.CDLL:
         L.bq_step_plan_create.restype = I
         L.bq_step_plan_run.argtypes = [P, P, P, P, P]
         L.bq_step_plan_run.restype = I
+        L.bq_step_plan_run_prepared.argtypes = [P, P, P, P]
+        L.bq_step_plan_run_prepared.restype = I
         L.bq_step_plan_destroy.argtypes = [P]
         L.bq_step_plan_destroy.restype = I
         L.bq_status_string.argtypes = [I]
@@ -308,6 +310,19 @@ def bq_quantize_blockwise_prepared(prepared, x, blocksize: int, codes=None, absm
     return codes, absmax
 
 
+def prepare_codebook_pair(qmap1, qmap2=None, stream=None):
+    """Both codebooks of an optimizer prepared back to back in one device
+    buffer (bq_prepare_codebook twice), as bq_step_plan_run_prepared reads
+    them: map 1's tables, then map 2's (absent for one-state optimizers)."""
+    import torch
+    prepared = torch.empty(2 * BQ_PREPARED_CODEBOOK_BYTES, dtype=torch.uint8,
+                           device=qmap1.device)
+    bq_prepare_codebook(qmap1, prepared[:BQ_PREPARED_CODEBOOK_BYTES], stream)
+    if qmap2 is not None:
+        bq_prepare_codebook(qmap2, prepared[BQ_PREPARED_CODEBOOK_BYTES:], stream)
+    return prepared
+
+
 class StepPlan:
     """bq_step_plan_create / bq_step_plan_run / bq_step_plan_destroy.
 
@@ -326,12 +341,24 @@ class StepPlan:
         _check(lib().bq_step_plan_create(int(opt), int(blocksize), int(grad_dtype), arr,
                                          len(tensors), ctypes.byref(h)), "bq_step_plan_create")
         self._h = h
+        self._two = opt in (BQ_ADAM, BQ_ADAMW, BQ_LAMB)
 
     def run(self, hp: dict, qmap1, qmap2=None, stream=None):
         h = _hparams(hp)
         _check(lib().bq_step_plan_run(self._h, ctypes.byref(h), _dev_ptr(qmap1, "qmap1"),
                                       None if qmap2 is None else _dev_ptr(qmap2, "qmap2"),
                                       _stream(stream)), "bq_step_plan_run")
+
+    def run_prepared(self, hp: dict, prepared, stream=None):
+        """One run with codebooks prepared beforehand (prepare_codebook_pair)."""
+        import torch
+        need = (2 if self._two else 1) * BQ_PREPARED_CODEBOOK_BYTES
+        if prepared.dtype != torch.uint8 or prepared.numel() < need:
+            raise ValueError(f"prepared codebooks: need {need} uint8 bytes")
+        h = _hparams(hp)
+        _check(lib().bq_step_plan_run_prepared(self._h, ctypes.byref(h),
+                                               _dev_ptr(prepared, "prepared"), _stream(stream)),
+               "bq_step_plan_run_prepared")
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value is not None:
@@ -352,6 +379,10 @@ def bq_step_plan_create(opt, blocksize, grad_dtype, tensors):
 
 def bq_step_plan_run(plan: StepPlan, hp: dict, qmap1, qmap2=None, stream=None):
     plan.run(hp, qmap1, qmap2, stream)
+
+
+def bq_step_plan_run_prepared(plan: StepPlan, hp: dict, prepared, stream=None):
+    plan.run_prepared(hp, prepared, stream)
 
 
 def bq_step_plan_destroy(plan: StepPlan):

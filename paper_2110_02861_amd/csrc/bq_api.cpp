@@ -515,18 +515,26 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
     return BQ_OK;
 }
 
-bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float *qmap1,
-                           const float *qmap2, hipStream_t stream)
+}  // extern "C"
+
+namespace {
+
+// Checks shared by the two run calls (no HIP call before the device query).
+bq_status check_run(bq_step_plan plan, const bq_hparams *hp)
 {
-    if (!plan || !hp || !qmap1)
-        return BQ_ERR_NULL;
-    const bool two = two_states(plan->opt);
-    if (two && !qmap2)
+    if (!plan || !hp)
         return BQ_ERR_NULL;
     if (hp->step < 1)
         return BQ_ERR_ARG;
-    if (!aligned(qmap1, 4) || (two && !aligned(qmap2, 4)))
-        return BQ_ERR_ALIGN;
+    return BQ_OK;
+}
+
+// Launches one run of a plan.  With qmap1 set, the plan's own workspace is
+// prepared from the raw maps first; otherwise `tables` already holds both
+// prepared codebooks.
+bq_status launch_run(bq_step_plan plan, const bq_hparams *hp, const uint8_t *tables,
+                     const float *qmap1, const float *qmap2, hipStream_t stream)
+{
     if (plan->total_tiles == 0)
         return BQ_OK;
     int dev = -1;
@@ -537,7 +545,7 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
 
     bq::PlanArgs a;
     std::memset(&a, 0, sizeof(a));
-    a.tables = plan->tables;
+    a.tables = tables;
     a.tiles = plan->tiles;
     a.partials = plan->partials;
     a.seg_range = plan->seg_range;
@@ -552,7 +560,10 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
     a.use_wd = (hp->weight_decay != 0.0f && plan->opt != BQ_ADAMW && plan->opt != BQ_LAMB) ? 1
                                                                                           : 0;
     a.total_tiles = (int32_t)plan->total_tiles;
-    hipError_t e = bq::launch_prepare(qmap1, two ? qmap2 : nullptr, plan->tables, stream);
+    hipError_t e = hipSuccess;
+    if (qmap1)
+        e = bq::launch_prepare(qmap1, two_states(plan->opt) ? qmap2 : nullptr, plan->tables,
+                               stream);
     if (e == hipSuccess && trust_opt(plan->opt))
         e = bq::launch_trust_ratios((int)plan->opt, (int)plan->grad_dtype, plan->blocksize, a,
                                     stream);
@@ -560,6 +571,37 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
         e = bq::launch_step_oneshot((int)plan->opt, (int)plan->grad_dtype, plan->blocksize, a,
                                     stream);
     return from_hip(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float *qmap1,
+                           const float *qmap2, hipStream_t stream)
+{
+    bq_status st = check_run(plan, hp);
+    if (st != BQ_OK)
+        return st;
+    const bool two = two_states(plan->opt);
+    if (!qmap1 || (two && !qmap2))
+        return BQ_ERR_NULL;
+    if (!aligned(qmap1, 4) || (two && !aligned(qmap2, 4)))
+        return BQ_ERR_ALIGN;
+    return launch_run(plan, hp, plan->tables, qmap1, qmap2, stream);
+}
+
+bq_status bq_step_plan_run_prepared(bq_step_plan plan, const bq_hparams *hp, const void *prepared,
+                                    hipStream_t stream)
+{
+    bq_status st = check_run(plan, hp);
+    if (st != BQ_OK)
+        return st;
+    if (!prepared)
+        return BQ_ERR_NULL;
+    if (!aligned(prepared, 16))
+        return BQ_ERR_ALIGN;
+    return launch_run(plan, hp, static_cast<const uint8_t *>(prepared), nullptr, nullptr, stream);
 }
 
 bq_status bq_step_plan_destroy(bq_step_plan plan)

@@ -15,8 +15,9 @@ layer's states in 32 bit (``override_32bit``, or the weight of
 exempted as well.
 
 Every update runs in the HIP kernels of libbq:
-- 8-bit tensors go through a step plan (``bq_step_plan_run``: one launch over
-  every tile of every tensor), looked up by every storage pointer and size, or
+- 8-bit tensors go through a step plan (``bq_step_plan_run_prepared``: one
+  launch over every tile of every tensor, with the fixed maps' decision tables
+  prepared once per device), looked up by every storage pointer and size, or
   through ``bq_optimizer8bit_step`` when ``use_plans=False``;
 - 32-bit tensors go through ``bq_optimizer32bit_step``.
 
@@ -43,6 +44,23 @@ def dynamic_codebooks(device: torch.device):
         _CODEBOOKS[key] = (torch.from_numpy(qs).to(device), torch.from_numpy(qu).to(device),
                            int(np.flatnonzero(qs == 0.0)[0]), int(np.flatnonzero(qu == 0.0)[0]))
     return _CODEBOOKS[key]
+
+
+_PREPARED: dict = {}
+
+
+def prepared_codebooks(device: torch.device, state1_unsigned: bool, two_states: bool):
+    """The decision tables of an optimizer's fixed maps, prepared once per
+    device and map pair (bq.prepare_codebook_pair) for plan runs."""
+    key = (device.type, device.index, state1_unsigned, two_states)
+    if key not in _PREPARED:
+        qs, qu, _, _ = dynamic_codebooks(device)
+        q1 = qu if state1_unsigned else qs
+        prepared = bq.prepare_codebook_pair(q1, qu if two_states else None)
+        # the tables are read later from whatever stream steps run on
+        torch.cuda.current_stream(device).synchronize()
+        _PREPARED[key] = prepared
+    return _PREPARED[key]
 
 
 class Optimizer8bit(torch.optim.Optimizer):
@@ -119,19 +137,20 @@ class Optimizer8bit(torch.optim.Optimizer):
                                                   device=p.device)
 
     @staticmethod
-    def _check_param(p: torch.Tensor) -> None:
+    def _check_param(p: torch.Tensor, g: torch.Tensor) -> None:
+        # each attribute read once: this runs for every param on every step
         if not p.is_cuda:
             raise TypeError("8-bit optimizers need GPU tensors (libbq runs on the GPU only)")
-        if p.dtype != torch.float32:
+        if p.dtype is not torch.float32:
             raise TypeError(f"params must be fp32, got {p.dtype}")
         if not p.is_contiguous():
             raise ValueError("params must be contiguous")
-        g = p.grad
-        if g.is_sparse:
+        if g.layout is not torch.strided:
             raise TypeError("sparse gradients are not supported")
-        if g.dtype not in (torch.float32, torch.float16):
-            raise TypeError(f"grads must be fp32 or fp16, got {g.dtype}")
-        if g.shape != p.shape or not g.is_contiguous():
+        gd = g.dtype
+        if gd is not torch.float32 and gd is not torch.float16:
+            raise TypeError(f"grads must be fp32 or fp16, got {gd}")
+        if g.numel() != p.numel() or not g.is_contiguous():
             raise ValueError("grads must be contiguous and shaped like their params")
 
     # -- the step -----------------------------------------------------------------
@@ -142,36 +161,55 @@ class Optimizer8bit(torch.optim.Optimizer):
         if closure is not None:
             with torch.enable_grad():
                 loss = closure()
-        for gi, group in enumerate(self.param_groups):
+        for group in self.param_groups:
+            # one pass over the params, bucketed by (8-bit, grad dtype, step,
+            # device); every launch then covers one bucket
             buckets: dict = {}
             for p in group["params"]:
-                if p.grad is None:
+                g = p.grad
+                if g is None:
                     continue
-                self._check_param(p)
+                self._check_param(p, g)
                 state = self.state[p]
                 if not state:
                     self._init_state(p, state)
-                state["step"] += 1
-                eight = "state1" in state
-                gdt = bq.BQ_F16 if p.grad.dtype == torch.float16 else bq.BQ_F32
-                buckets.setdefault((eight, gdt, state["step"], p.device), []).append(p)
-            for (eight, gdt, step, device), ps in buckets.items():
+                dev = p.get_device()
+                # the states were sized and placed for the param when they were made
+                s1 = state.get("state1")
+                if s1 is None:
+                    s1 = state["exp_avg"]
+                if s1.numel() != p.numel() or s1.get_device() != dev:
+                    raise ValueError("a param changed size or device after its optimizer state "
+                                     "was created")
+                step = state["step"] + 1
+                state["step"] = step
+                key = ("state1" in state, g.dtype, step, dev)
+                items = buckets.get(key)
+                if items is None:
+                    buckets[key] = items = []
+                items.append((p, g, state))
+            for (eight, gdtype, step, _), items in buckets.items():
+                gdt = bq.BQ_F16 if gdtype is torch.float16 else bq.BQ_F32
                 hp = self._hparams(group, step)
+                device = items[0][0].device
                 if eight:
-                    self._step8(gi, gdt, device, ps, hp)
+                    self._step8(gdt, device, items, hp)
                 else:
-                    rows = [(p, p.grad, self.state[p]["exp_avg"],
-                             self.state[p].get("exp_avg_sq")) for p in ps]
+                    rows = [(p, g, s["exp_avg"], s.get("exp_avg_sq")) for p, g, s in items]
                     bq.bq_optimizer32bit_step(self.OPT, gdt, rows, hp)
         return loss
 
-    def _step8(self, gi: int, gdt: int, device, ps, hp: dict) -> None:
-        q1, q2, _, _ = self._maps(device)
+    def _step8(self, gdt: int, device, items, hp: dict) -> None:
         rows = []
-        for p in ps:
-            s = self.state[p]
-            rows.append((p, p.grad, s["state1"], s.get("state2"), s["absmax1"], s.get("absmax2")))
+        key = [gdt, device.index]
+        for p, g, s in items:
+            s1, s2, a1, a2 = s["state1"], s.get("state2"), s["absmax1"], s.get("absmax2")
+            n = p.numel()
+            rows.append((p, g, s1, s2, a1, a2))
+            key += (p.data_ptr(), g.data_ptr(), s1.data_ptr(), a1.data_ptr(),
+                    0 if s2 is None else s2.data_ptr(), 0 if a2 is None else a2.data_ptr(), n)
         if not self.use_plans and self.OPT not in (bq.BQ_LAMB, bq.BQ_LARS):
+            q1, q2, _, _ = self._maps(device)
             bq.bq_optimizer8bit_step(self.OPT, self.blocksize, gdt, rows, hp, q1, q2)
             return
         # A plan holds device pointers and is a function of them and the sizes
@@ -180,9 +218,7 @@ class Optimizer8bit(torch.optim.Optimizer):
         # the tensors, so grads freed by zero_grad(set_to_none=True) can be
         # reallocated at the same addresses (and the plan reused); several
         # plans per param set serve alternating grad buffers.
-        key = (gdt, device.index)
-        key += tuple(0 if t is None else t.data_ptr() for row in rows for t in row)
-        key += tuple(p.numel() for p in ps)
+        key = tuple(key)
         plan = self._plans.pop(key, None)
         if plan is None:
             plan = bq.StepPlan(self.OPT, self.blocksize, gdt, rows, keep=False)
@@ -190,7 +226,7 @@ class Optimizer8bit(torch.optim.Optimizer):
         while len(self._plans) > self.MAX_PLANS:
             oldest = next(iter(self._plans))
             self._plans.pop(oldest).close()
-        plan.run(hp, q1, q2)
+        plan.run_prepared(hp, prepared_codebooks(device, self._state1_unsigned, self._two_states))
 
     def load_state_dict(self, state_dict):
         for plan in self._plans.values():

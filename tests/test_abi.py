@@ -187,6 +187,7 @@ def test_step_plan_argument_checks(L):
     hp = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 1)
     r = L.bq_step_plan_run
     assert r(None, ctypes.byref(hp), A16, A16, None) == bq.BQ_ERR_NULL
+    assert L.bq_step_plan_run_prepared(None, ctypes.byref(hp), A16, None) == bq.BQ_ERR_NULL
     assert L.bq_step_plan_destroy(None) == bq.BQ_OK
 
 

@@ -385,3 +385,24 @@ def test_param_groups_and_mixed_grad_dtypes(use_plans):
             upd = np.abs(w_before[i] - w_ref.astype(np.float64))
             ok, worst = param_close(host(p).ravel(), w_ref, 1e-6 * upd)
             assert ok, (i, t, worst)
+
+
+@pytest.mark.parametrize("case", ["adam", "sgd"])
+def test_param_resized_after_state_raises(case):
+    """A param whose storage is swapped for a larger one after its first step
+    is refused before any launch: its states were sized for the old storage.
+    The 32-bit-state path checks the same."""
+    cls, kw, _ = CASES[case]
+    for override in (False, True):
+        p = torch.nn.Parameter(torch.zeros(3000, device="cuda"))
+        opt = cls([p], **kw)
+        if override:
+            opt.override_32bit(p)
+        p.grad = torch.zeros_like(p)
+        say(f"optim resized param {case} 32-bit={override}: first step")
+        opt.step()
+        p.data = torch.zeros(5000, device="cuda")
+        p.grad = torch.zeros_like(p)
+        with pytest.raises(ValueError, match="changed size"):
+            opt.step()
+        torch.cuda.synchronize()

@@ -48,7 +48,11 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
         hs.append(HostState(w, B, two))
         ds.append(DevState(w, B, two, tdt))
     arr = bq.make_tensor_array([d.row() for d in ds])
-    plan = bq.StepPlan(opt, B, grad_dtype, [d.row() for d in ds]) if path == "plan" else None
+    plan = None
+    if path in ("plan", "prepared"):
+        plan = bq.StepPlan(opt, B, grad_dtype, [d.row() for d in ds])
+    if path == "prepared":
+        prepared = bq.prepare_codebook_pair(qs_d, qu_d if two else None)
     for t in range(1, steps + 1):
         grads = []
         for i, n in enumerate(sizes):
@@ -59,7 +63,9 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
             grads.append(g)
             ds[i].g.copy_(torch.from_numpy(g))
         say(f"step {path} opt={opt} B={B} grad={ndt.__name__} tensors={len(sizes)} t={t}")
-        if plan is not None:
+        if path == "prepared":
+            plan.run_prepared(dict(hp, step=t), prepared)
+        elif plan is not None:
             plan.run(dict(hp, step=t), qs_d, qu_d if two else None)
         else:
             bq.bq_optimizer8bit_step(opt, B, grad_dtype, (arr, len(ds)), dict(hp, step=t),
@@ -94,6 +100,20 @@ PATHS = ["call", "plan"]
 @pytest.mark.parametrize("B", [256, 512, 1024, 2048, 4096])
 def test_ragged_list(opt, grad_dtype, B, path):
     run_lists(opt, B, grad_dtype, RAGGED, steps=3, path=path)
+
+
+@pytest.mark.parametrize("opt", ["adam", "adamw", "momentum", "adagrad", "lamb", "lars"])
+@pytest.mark.parametrize("grad_dtype", [bq.BQ_F16, bq.BQ_F32])
+def test_plan_with_prepared_codebooks(opt, grad_dtype):
+    run_lists(opt, 2048, grad_dtype, RAGGED, steps=3, path="prepared")
+
+
+@pytest.mark.parametrize("family", ["inverse_dynamic", "linear", "quantile"])
+def test_plan_with_prepared_other_codebooks(family):
+    """Prepared tables of the App. F maps, including the inverse unsigned map's
+    buckets of up to 28 thresholds."""
+    run_lists("adam", 1024, bq.BQ_F16, RAGGED, steps=2, seed=3, path="prepared",
+              maps=_map_families()[family])
 
 
 @pytest.mark.parametrize("path", PATHS)
@@ -325,7 +345,9 @@ def test_zero_learning_rate_keeps_params(opt, path):
         for d, g in zip(ds, gs):
             d.g.copy_(torch.from_numpy(g))
         say(f"lr=0 step {path} {opt} t={t}")
-        if plan is not None:
+        if path == "prepared":
+            plan.run_prepared(dict(hp, step=t), prepared)
+        elif plan is not None:
             plan.run(dict(hp, step=t), qs_d, qu_d if two else None)
         else:
             bq.bq_optimizer8bit_step(opt, B, bq.BQ_F16, rows, dict(hp, step=t), qs_d,
