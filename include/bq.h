@@ -67,7 +67,11 @@ typedef enum bq_optimizer {
     BQ_LAMB = 4,  /* step plans only */
     BQ_LARS = 5   /* step plans only */
 } bq_optimizer;
-typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1 } bq_dtype;
+/* Gradient element types.  Every grad is converted to fp32 exactly before the
+ * update (Section 3: the update itself runs in 32 bit); the paper's setups use
+ * fp16 (mixed precision) and fp32 grads, bfloat16 is the common mixed-precision
+ * type on MI355X. */
+typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1, BQ_BF16 = 2 } bq_dtype;
 
 /*
  * Build a 256-entry dynamic codebook on the host (synchronous, no GPU call).
@@ -178,7 +182,7 @@ bq_status bq_dequantize_blockwise(const float *qmap, const uint8_t *codes,
 /* One parameter tensor of the step; all pointers are device pointers. */
 typedef struct bq_tensor {
     float *param;       /* numel fp32, updated in place */
-    const void *grad;   /* numel fp32 or fp16 (see grad_dtype), read only */
+    const void *grad;   /* numel fp32, fp16 or bf16 (see grad_dtype), read only */
     uint8_t *state1;    /* numel codes of the first state (m), in place */
     uint8_t *state2;    /* numel codes of the second state (r); NULL for Momentum, AdaGrad */
     float *absmax1;     /* ceil(numel / B) block absmax of state 1, in place */
@@ -235,7 +239,7 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
 /* One tensor with 32-bit states; all pointers are device pointers. */
 typedef struct bq_tensor32 {
     float *param;       /* numel fp32, updated in place */
-    const void *grad;   /* numel fp32 or fp16 (see grad_dtype), read only */
+    const void *grad;   /* numel fp32, fp16 or bf16 (see grad_dtype), read only */
     float *state1;      /* numel fp32 first state (m), in place */
     float *state2;      /* numel fp32 second state (r); NULL for Momentum, AdaGrad */
     int64_t numel;

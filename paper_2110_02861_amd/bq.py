@@ -24,7 +24,7 @@ CODEBOOKS = {"dynamic": (BQ_SIGNED, BQ_UNSIGNED),
              "inverse_dynamic": (BQ_INVERSE_SIGNED, BQ_INVERSE_UNSIGNED),
              "linear": (BQ_LINEAR_SIGNED, BQ_LINEAR_UNSIGNED)}
 BQ_ADAM, BQ_ADAMW, BQ_MOMENTUM, BQ_ADAGRAD, BQ_LAMB, BQ_LARS = 0, 1, 2, 3, 4, 5
-BQ_F32, BQ_F16 = 0, 1
+BQ_F32, BQ_F16, BQ_BF16 = 0, 1, 2
 OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM,
               "adagrad": BQ_ADAGRAD, "lamb": BQ_LAMB, "lars": BQ_LARS}
 

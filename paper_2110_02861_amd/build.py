@@ -38,10 +38,25 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+OBJ_DIR = os.path.join(PKG, "_build", "obj")
+
+
 def _link(out: str, sources, verbose: bool) -> str:
-    srcs = [os.path.join(CSRC, s) for s in sources]
+    """Compile every source to an object, all at once in parallel, then link."""
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    objs, procs = [], []
+    for name in sources:
+        obj = os.path.join(OBJ_DIR, os.path.splitext(name)[0] + ".o")
+        cmd = [hipcc(), *FLAGS, "-c", "-o", obj, os.path.join(CSRC, name)]
+        if verbose:
+            print(" ".join(cmd))
+        objs.append(obj)
+        procs.append((cmd, subprocess.Popen(cmd)))
+    failed = [cmd for cmd, proc in procs if proc.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, failed[0])
     tmp = out + ".tmp"
-    cmd = [hipcc(), *FLAGS, "-shared", "-o", tmp, *srcs]
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)

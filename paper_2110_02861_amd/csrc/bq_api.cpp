@@ -26,7 +26,7 @@ bool valid_opt(bq_optimizer o)
 bool valid_plan_opt(bq_optimizer o) { return valid_opt(o) || o == BQ_LAMB || o == BQ_LARS; }
 bool trust_opt(bq_optimizer o) { return o == BQ_LAMB || o == BQ_LARS; }
 bool two_states(bq_optimizer o) { return o == BQ_ADAM || o == BQ_ADAMW || o == BQ_LAMB; }
-bool valid_dtype(bq_dtype d) { return d == BQ_F32 || d == BQ_F16; }
+bool valid_dtype(bq_dtype d) { return d == BQ_F32 || d == BQ_F16 || d == BQ_BF16; }
 
 // beta^t in double by right-to-left binary exponentiation.
 double beta_pow(double beta, int64_t t)
@@ -421,7 +421,7 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
         return st;
 
     const int64_t tile = bq::step_tile(blocksize);
-    const size_t gbytes = grad_dtype == BQ_F16 ? 2 : 4;
+    const size_t gbytes = grad_dtype == BQ_F32 ? 4 : 2;
     int64_t total = 0;
     int32_t nonempty = 0;
     for (int32_t i = 0; i < ntensors; ++i) {

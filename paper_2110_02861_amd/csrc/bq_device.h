@@ -289,5 +289,36 @@ __device__ inline float half_hi(uint32_t w)
     return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
 }
 
+// 16-bit grads (GRAD kF16 or kBF16): the low and high element of a packed word,
+// converted to fp32 exactly (a bf16 is the top half of an fp32).
+template <int GRAD>
+__device__ inline float g16_lo(uint32_t w)
+{
+    if constexpr (GRAD == kBF16)
+        return __uint_as_float(w << 16);
+    else
+        return half_lo(w);
+}
+template <int GRAD>
+__device__ inline float g16_hi(uint32_t w)
+{
+    if constexpr (GRAD == kBF16)
+        return __uint_as_float(w & 0xffff0000u);
+    else
+        return half_hi(w);
+}
+
+// Element i of a grad array of type GRAD, converted to fp32 exactly.
+template <int GRAD>
+__device__ inline float grad_at(const void *grad, int64_t i)
+{
+    if constexpr (GRAD == kF32)
+        return G(static_cast<const float *>(grad))[i];
+    else if constexpr (GRAD == kF16)
+        return (float)G(static_cast<const _Float16 *>(grad))[i];
+    else
+        return __uint_as_float((uint32_t)G(static_cast<const uint16_t *>(grad))[i] << 16);
+}
+
 }  // namespace dev
 }  // namespace bq

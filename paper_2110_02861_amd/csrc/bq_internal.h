@@ -177,7 +177,7 @@ enum { kAdam = 0, kAdamW = 1, kMomentum = 2, kAdaGrad = 3, kLamb = 4, kLars = 5 
 constexpr bool has_two_states(int opt) { return opt == kAdam || opt == kAdamW || opt == kLamb; }
 // optimizers with a per-tensor trust ratio (two passes: norms, then the step)
 constexpr bool has_trust_ratio(int opt) { return opt == kLamb || opt == kLars; }
-enum { kF32 = 0, kF16 = 1 };
+enum { kF32 = 0, kF16 = 1, kBF16 = 2 };
 
 // the fused step from raw maps: the one-shot tile code in persistent
 // workgroups (tile_begin in units of step_tile(blocksize))

@@ -181,9 +181,9 @@ struct StepOS {
             if (FULL) {
                 valid[c] = 4;
                 wr[c] = ld_nt(reinterpret_cast<const vf4 *>(D.param + e));
-                if constexpr (GRAD == kF16)
+                if constexpr (GRAD != kF32)
                     gr16[c] = ld_nt(reinterpret_cast<const vu2 *>(
-                        static_cast<const _Float16 *>(D.grad) + e));
+                        static_cast<const uint16_t *>(D.grad) + e));
                 else
                     gr32[c] = ld_nt(reinterpret_cast<const vf4 *>(
                         static_cast<const float *>(D.grad) + e));
@@ -199,10 +199,7 @@ struct StepOS {
                     const bool ok = r < valid[c];
                     const int64_t i = e + r;
                     wv[r] = ok ? G(D.param)[i] : 0.0f;
-                    if constexpr (GRAD == kF16)
-                        gv[r] = ok ? (float)G(static_cast<const _Float16 *>(D.grad))[i] : 0.0f;
-                    else
-                        gv[r] = ok ? G(static_cast<const float *>(D.grad))[i] : 0.0f;
+                    gv[r] = ok ? grad_at<GRAD>(D.grad, i) : 0.0f;
                     a1 |= (ok ? (uint32_t)G(D.s1)[i] : 0u) << (8 * r);
                     if constexpr (kTwo)
                         a2 |= (ok ? (uint32_t)G(D.s2)[i] : 0u) << (8 * r);
@@ -262,11 +259,11 @@ struct StepOS {
             w[4 * c + 1] = wr[c].y;
             w[4 * c + 2] = wr[c].z;
             w[4 * c + 3] = wr[c].w;
-            if (GRAD == kF16 && FULL) {
-                g[4 * c] = half_lo(gr16[c].x);
-                g[4 * c + 1] = half_hi(gr16[c].x);
-                g[4 * c + 2] = half_lo(gr16[c].y);
-                g[4 * c + 3] = half_hi(gr16[c].y);
+            if (GRAD != kF32 && FULL) {
+                g[4 * c] = g16_lo<GRAD>(gr16[c].x);
+                g[4 * c + 1] = g16_hi<GRAD>(gr16[c].x);
+                g[4 * c + 2] = g16_lo<GRAD>(gr16[c].y);
+                g[4 * c + 3] = g16_hi<GRAD>(gr16[c].y);
             } else {
                 g[4 * c] = gr32[c].x;
                 g[4 * c + 1] = gr32[c].y;
@@ -540,7 +537,7 @@ __global__ __launch_bounds__(kST) void step_persistent_kernel(const StepArgs a)
         const int64_t t0 = (int64_t)(tile - S.tile_begin) * K::TILE;
         TensorDesc D;
         D.param = S.param + t0;
-        D.grad = static_cast<const char *>(S.grad) + t0 * (GRAD == kF16 ? 2 : 4);
+        D.grad = static_cast<const char *>(S.grad) + t0 * (GRAD == kF32 ? 4 : 2);
         D.s1 = S.s1 + t0;
         D.s2 = K::kTwo ? S.s2 + t0 : nullptr;
         D.a1 = S.a1 + t0 / B;
@@ -599,13 +596,13 @@ __global__ __launch_bounds__(kST) void norms_kernel(const PlanArgs a)
             w[4 * c + 1] = wv.y;
             w[4 * c + 2] = wv.z;
             w[4 * c + 3] = wv.w;
-            if constexpr (GRAD == kF16) {
+            if constexpr (GRAD != kF32) {
                 const vu2 gv =
-                    ld_nt(reinterpret_cast<const vu2 *>(static_cast<const _Float16 *>(grad) + e0));
-                g[4 * c] = half_lo(gv.x);
-                g[4 * c + 1] = half_hi(gv.x);
-                g[4 * c + 2] = half_lo(gv.y);
-                g[4 * c + 3] = half_hi(gv.y);
+                    ld_nt(reinterpret_cast<const vu2 *>(static_cast<const uint16_t *>(grad) + e0));
+                g[4 * c] = g16_lo<GRAD>(gv.x);
+                g[4 * c + 1] = g16_hi<GRAD>(gv.x);
+                g[4 * c + 2] = g16_lo<GRAD>(gv.y);
+                g[4 * c + 3] = g16_hi<GRAD>(gv.y);
             } else {
                 const vf4 gv =
                     ld_nt(reinterpret_cast<const vf4 *>(static_cast<const float *>(grad) + e0));
@@ -623,10 +620,7 @@ __global__ __launch_bounds__(kST) void norms_kernel(const PlanArgs a)
                 const bool ok = r < valid[c];
                 const int64_t e = e0 + r;
                 w[4 * c + r] = ok ? G(param)[e] : 0.0f;
-                if constexpr (GRAD == kF16)
-                    g[4 * c + r] = ok ? (float)G(static_cast<const _Float16 *>(grad))[e] : 0.0f;
-                else
-                    g[4 * c + r] = ok ? G(static_cast<const float *>(grad))[e] : 0.0f;
+                g[4 * c + r] = ok ? grad_at<GRAD>(grad, e) : 0.0f;
                 if constexpr (kIsLamb) {
                     b1 |= (ok ? (uint32_t)G(s1)[e] : 0u) << (8 * r);
                     b2 |= (ok ? (uint32_t)G(s2)[e] : 0u) << (8 * r);
@@ -1051,8 +1045,11 @@ hipError_t launch_persist_b(int blocksize, const StepArgs &a, hipStream_t s)
 template <int OPT>
 hipError_t launch_persist_g(int grad_dtype, int blocksize, const StepArgs &a, hipStream_t s)
 {
-    return grad_dtype == kF16 ? launch_persist_b<OPT, kF16>(blocksize, a, s)
-                              : launch_persist_b<OPT, kF32>(blocksize, a, s);
+    switch (grad_dtype) {
+    case kF16: return launch_persist_b<OPT, kF16>(blocksize, a, s);
+    case kBF16: return launch_persist_b<OPT, kBF16>(blocksize, a, s);
+    default: return launch_persist_b<OPT, kF32>(blocksize, a, s);
+    }
 }
 
 template <int OPT, int GRAD, int B>
@@ -1079,8 +1076,11 @@ hipError_t launch_os_b(int blocksize, const PlanArgs &a, hipStream_t s)
 template <int OPT>
 hipError_t launch_os_g(int grad_dtype, int blocksize, const PlanArgs &a, hipStream_t s)
 {
-    return grad_dtype == kF16 ? launch_os_b<OPT, kF16>(blocksize, a, s)
-                              : launch_os_b<OPT, kF32>(blocksize, a, s);
+    switch (grad_dtype) {
+    case kF16: return launch_os_b<OPT, kF16>(blocksize, a, s);
+    case kBF16: return launch_os_b<OPT, kBF16>(blocksize, a, s);
+    default: return launch_os_b<OPT, kF32>(blocksize, a, s);
+    }
 }
 
 template <int B>
@@ -1142,8 +1142,11 @@ hipError_t launch_norms_b(int blocksize, const PlanArgs &a, hipStream_t stream)
 template <int OPT>
 hipError_t launch_norms_g(int grad_dtype, int blocksize, const PlanArgs &a, hipStream_t stream)
 {
-    return grad_dtype == kF16 ? launch_norms_b<OPT, kF16>(blocksize, a, stream)
-                              : launch_norms_b<OPT, kF32>(blocksize, a, stream);
+    switch (grad_dtype) {
+    case kF16: return launch_norms_b<OPT, kF16>(blocksize, a, stream);
+    case kBF16: return launch_norms_b<OPT, kBF16>(blocksize, a, stream);
+    default: return launch_norms_b<OPT, kF32>(blocksize, a, stream);
+    }
 }
 
 hipError_t launch_trust_ratios(int opt, int grad_dtype, int blocksize, const PlanArgs &a,

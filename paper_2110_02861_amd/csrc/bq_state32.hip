@@ -45,11 +45,11 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
             const vf4 vv = ld_nt(reinterpret_cast<const vf4 *>(D.v + e0));
             v[0] = vv.x; v[1] = vv.y; v[2] = vv.z; v[3] = vv.w;
         }
-        if constexpr (GRAD == kF16) {
+        if constexpr (GRAD != kF32) {
             const vu2 gv = ld_nt(reinterpret_cast<const vu2 *>(
-                static_cast<const _Float16 *>(D.grad) + e0));
-            g[0] = half_lo(gv.x); g[1] = half_hi(gv.x);
-            g[2] = half_lo(gv.y); g[3] = half_hi(gv.y);
+                static_cast<const uint16_t *>(D.grad) + e0));
+            g[0] = g16_lo<GRAD>(gv.x); g[1] = g16_hi<GRAD>(gv.x);
+            g[2] = g16_lo<GRAD>(gv.y); g[3] = g16_hi<GRAD>(gv.y);
         } else {
             const vf4 gv = ld_nt(reinterpret_cast<const vf4 *>(static_cast<const float *>(D.grad) + e0));
             g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
@@ -61,10 +61,7 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
             w[r] = ok ? G(D.param)[e0 + r] : 0.0f;
             m[r] = ok ? G(D.m)[e0 + r] : 0.0f;
             v[r] = (kTwo && ok) ? G(D.v)[e0 + r] : 0.0f;
-            if constexpr (GRAD == kF16)
-                g[r] = ok ? (float)G(static_cast<const _Float16 *>(D.grad))[e0 + r] : 0.0f;
-            else
-                g[r] = ok ? G(static_cast<const float *>(D.grad))[e0 + r] : 0.0f;
+            g[r] = ok ? grad_at<GRAD>(D.grad, e0 + r) : 0.0f;
         }
     }
 
@@ -113,12 +110,13 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
 template <int OPT>
 hipError_t launch32_g(int grad_dtype, const State32Args &a, hipStream_t stream)
 {
+    const dim3 grid((unsigned)a.total_tiles), block(kThreads32);
     if (grad_dtype == kF16)
-        hipLaunchKernelGGL((step32_kernel<OPT, kF16>), dim3((unsigned)a.total_tiles),
-                           dim3(kThreads32), 0, stream, a);
+        hipLaunchKernelGGL((step32_kernel<OPT, kF16>), grid, block, 0, stream, a);
+    else if (grad_dtype == kBF16)
+        hipLaunchKernelGGL((step32_kernel<OPT, kBF16>), grid, block, 0, stream, a);
     else
-        hipLaunchKernelGGL((step32_kernel<OPT, kF32>), dim3((unsigned)a.total_tiles),
-                           dim3(kThreads32), 0, stream, a);
+        hipLaunchKernelGGL((step32_kernel<OPT, kF32>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 

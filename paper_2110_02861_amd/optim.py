@@ -21,8 +21,8 @@ Every update runs in the HIP kernels of libbq:
   through ``bq_optimizer8bit_step`` when ``use_plans=False``;
 - 32-bit tensors go through ``bq_optimizer32bit_step``.
 
-Params must be fp32 CUDA tensors, contiguous and 16-byte aligned; grads fp32 or
-fp16 of the same shape.  ``state_dict`` / ``load_state_dict`` carry the codes,
+Params must be fp32 CUDA tensors, contiguous and 16-byte aligned; grads fp32,
+fp16 or bf16 of the same shape.  ``state_dict`` / ``load_state_dict`` carry the codes,
 the absmax arrays and the step count of every tensor.
 """
 from __future__ import annotations
@@ -45,6 +45,8 @@ def dynamic_codebooks(device: torch.device):
                            int(np.flatnonzero(qs == 0.0)[0]), int(np.flatnonzero(qu == 0.0)[0]))
     return _CODEBOOKS[key]
 
+
+_GRAD_DTYPES = {torch.float32: bq.BQ_F32, torch.float16: bq.BQ_F16, torch.bfloat16: bq.BQ_BF16}
 
 _PREPARED: dict = {}
 
@@ -148,8 +150,8 @@ class Optimizer8bit(torch.optim.Optimizer):
         if g.layout is not torch.strided:
             raise TypeError("sparse gradients are not supported")
         gd = g.dtype
-        if gd is not torch.float32 and gd is not torch.float16:
-            raise TypeError(f"grads must be fp32 or fp16, got {gd}")
+        if gd is not torch.float32 and gd is not torch.float16 and gd is not torch.bfloat16:
+            raise TypeError(f"grads must be fp32, fp16 or bf16, got {gd}")
         if g.numel() != p.numel() or not g.is_contiguous():
             raise ValueError("grads must be contiguous and shaped like their params")
 
@@ -189,7 +191,7 @@ class Optimizer8bit(torch.optim.Optimizer):
                     buckets[key] = items = []
                 items.append((p, g, state))
             for (eight, gdtype, step, _), items in buckets.items():
-                gdt = bq.BQ_F16 if gdtype is torch.float16 else bq.BQ_F32
+                gdt = _GRAD_DTYPES[gdtype]
                 hp = self._hparams(group, step)
                 device = items[0][0].device
                 if eight:

@@ -110,7 +110,7 @@ def test_step_argument_checks(L):
     H = ctypes.byref(hp)
     assert s(4, 2048, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_ENUM
     assert s(-1, 2048, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_ENUM
-    assert s(0, 2048, 2, good, 1, H, A16, A16, None) == bq.BQ_ERR_DTYPE
+    assert s(0, 2048, 3, good, 1, H, A16, A16, None) == bq.BQ_ERR_DTYPE
     assert s(0, 1536, 0, good, 1, H, A16, A16, None) == bq.BQ_ERR_BLOCKSIZE
     assert s(0, 2048, 0, good, -1, H, A16, A16, None) == bq.BQ_ERR_SIZE
     assert s(0, 2048, 0, None, 1, H, A16, A16, None) == bq.BQ_ERR_NULL

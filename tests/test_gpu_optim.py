@@ -71,11 +71,27 @@ def grads(seed, step, dtype):
 
 
 def set_grad(p, g):
-    """Attach a host grad; an fp16 grad on an fp32 param needs grad_dtype None."""
-    t = torch.from_numpy(np.ascontiguousarray(g)).cuda()
+    """Attach a host grad (numpy or torch); a 16-bit grad on an fp32 param
+    needs grad_dtype None."""
+    t = g if isinstance(g, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(g))
+    t = t.cuda()
     if t.dtype != p.dtype and hasattr(p, "grad_dtype"):
         p.grad_dtype = None
     p.grad = t
+
+
+def grad_pair(g, gdt):
+    """(grad to attach, its values for the oracle).  bf16: torch rounds the
+    fp32 grad on the host and the oracle takes the exact fp32 values of the
+    bf16 result."""
+    if gdt == "bf16":
+        gt = torch.from_numpy(np.ascontiguousarray(g, dtype=np.float32)).to(torch.bfloat16)
+        return gt, gt.float().numpy()
+    return g, g
+
+
+def host_dtype(gdt):
+    return np.float32 if gdt == "bf16" else gdt
 
 
 def snapshot(opt, p):
@@ -107,7 +123,7 @@ def oracle_step8(kind, hp, w, g, snap, n, two, t):
 
 
 @pytest.mark.parametrize("use_plans", [True, False])
-@pytest.mark.parametrize("gdt", [np.float32, np.float16])
+@pytest.mark.parametrize("gdt", [np.float32, np.float16, "bf16"])
 @pytest.mark.parametrize("case", list(CASES))
 def test_optimizer_matches_oracle(case, gdt, use_plans):
     cls, kw, kind = CASES[case]
@@ -116,13 +132,15 @@ def test_optimizer_matches_oracle(case, gdt, use_plans):
     params = init_params(7)
     opt = cls(params, blocksize=B, use_plans=use_plans, **kw)
     for t in range(1, 4):
-        gs = grads(7, t, gdt)
+        gs = grads(7, t, host_dtype(gdt))
         refs = []
         for p, g in zip(params, gs):
-            refs.append(oracle_step8(kind, hp, host(p).ravel(), g.ravel(), snapshot(opt, p),
-                                     p.numel(), two, t))
-            set_grad(p, g)
-        say(f"optim {case} {np.dtype(gdt).name} plans={use_plans} step {t}")
+            g_dev, g_ref = grad_pair(g, gdt)
+            refs.append(oracle_step8(kind, hp, host(p).ravel(), g_ref.ravel(),
+                                     snapshot(opt, p), p.numel(), two, t))
+            set_grad(p, g_dev)
+        say(f"optim {case} {gdt if gdt == 'bf16' else np.dtype(gdt).name} "
+            f"plans={use_plans} step {t}")
         w_before = [host(p).ravel().astype(np.float64) for p in params]
         opt.step()
         torch.cuda.synchronize()
@@ -140,8 +158,9 @@ def test_optimizer_matches_oracle(case, gdt, use_plans):
             assert ok, f"{case} tensor {i} step {t}: params off by {worst}"
 
 
+@pytest.mark.parametrize("gdt", [np.float32, "bf16"])
 @pytest.mark.parametrize("case", ["adam", "adamw", "sgd", "adagrad"])
-def test_32bit_override_and_min_size(case):
+def test_32bit_override_and_min_size(case, gdt):
     """override_32bit and min_8bit_size keep fp32 states, updated like the
     oracle's step with fp32 states; the other tensors stay 8-bit."""
     cls, kw, kind = CASES[case]
@@ -154,6 +173,7 @@ def test_32bit_override_and_min_size(case):
         gs = grads(11, t, np.float32)
         refs = {}
         for i, (p, g) in enumerate(zip(params, gs)):
+            g_dev, g = grad_pair(g, gdt)
             snap = snapshot(opt, p)
             if i in (1, 3, 4):  # overridden, and below min_8bit_size
                 w = host(p).ravel().copy()
@@ -163,8 +183,8 @@ def test_32bit_override_and_min_size(case):
                 oracle.step32(kind, w, g.ravel(), m, v, hp["lr"], hp["beta1"], hp["beta2"],
                               hp["eps"], hp["wd"], t)
                 refs[i] = (w, m, v)
-            set_grad(p, g)
-        say(f"optim override {case} step {t}")
+            set_grad(p, g_dev)
+        say(f"optim override {case} {gdt} step {t}")
         w_before = [host(p).ravel().astype(np.float64) for p in params]
         opt.step()
         torch.cuda.synchronize()

@@ -39,7 +39,8 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
         qs_d, qu_d = torch.from_numpy(qs).cuda(), torch.from_numpy(qu).cuda()
     two = opt in ("adam", "adamw", "lamb")
     hp = dict(HPS[opt] if hp is None else hp)
-    tdt = torch.float16 if grad_dtype == bq.BQ_F16 else torch.float32
+    tdt = {bq.BQ_F32: torch.float32, bq.BQ_F16: torch.float16,
+           bq.BQ_BF16: torch.bfloat16}[grad_dtype]
     ndt = np.float16 if grad_dtype == bq.BQ_F16 else np.float32
     hs, ds = [], []
     for i, n in enumerate(sizes):
@@ -59,10 +60,17 @@ def run_lists(opt, B, grad_dtype, sizes, steps, seed=0, hp=None, exact_codes=Tru
             rng = np.random.default_rng([seed, i, t])
             g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
             g[rng.random(n) < 1e-3] *= 100.0
-            g = g.astype(ndt)
+            if grad_dtype == bq.BQ_BF16:
+                # torch rounds to bf16 on the host; the oracle takes the exact
+                # fp32 values of those bf16 grads
+                gt = torch.from_numpy(g).to(torch.bfloat16)
+                ds[i].g.copy_(gt)
+                g = gt.float().numpy()
+            else:
+                g = g.astype(ndt)
+                ds[i].g.copy_(torch.from_numpy(g))
             grads.append(g)
-            ds[i].g.copy_(torch.from_numpy(g))
-        say(f"step {path} opt={opt} B={B} grad={ndt.__name__} tensors={len(sizes)} t={t}")
+        say(f"step {path} opt={opt} B={B} grad={tdt} tensors={len(sizes)} t={t}")
         if path == "prepared":
             plan.run_prepared(dict(hp, step=t), prepared)
         elif plan is not None:
@@ -100,6 +108,17 @@ PATHS = ["call", "plan"]
 @pytest.mark.parametrize("B", [256, 512, 1024, 2048, 4096])
 def test_ragged_list(opt, grad_dtype, B, path):
     run_lists(opt, B, grad_dtype, RAGGED, steps=3, path=path)
+
+
+@pytest.mark.parametrize("path", ["call", "plan", "prepared"])
+@pytest.mark.parametrize("opt", ["adam", "adamw", "momentum", "adagrad", "lamb", "lars"])
+@pytest.mark.parametrize("B", [256, 2048, 4096])
+def test_bf16_grads(opt, B, path):
+    """bf16 grads are widened exactly to fp32 before the update, so the step
+    equals the oracle's on those fp32 values, codes and absmax bit for bit."""
+    if path == "call" and opt in ("lamb", "lars"):
+        pytest.skip("LAMB and LARS run through plans only")
+    run_lists(opt, B, bq.BQ_BF16, RAGGED, steps=3, seed=11, path=path)
 
 
 @pytest.mark.parametrize("opt", ["adam", "adamw", "momentum", "adagrad", "lamb", "lars"])
