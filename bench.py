@@ -141,7 +141,7 @@ def setup_list(torch, bq, workloads, config, nstates, blocksize=BLOCKSIZE, seed=
     map).  Returns (specs, params, grads, states, rows) with rows[r] the
     bq_tensor tuples that use grad buffer r."""
     specs = workloads.SPECS[config]()
-    gdt = torch.float16 if workloads.GRADS[config][0] == "float16" else torch.float32
+    gdt = getattr(torch, workloads.GRADS[config][0])
     dev = torch.device("cuda:0")
     B = blocksize
     params, grads, states = [], [[], []], []
@@ -223,6 +223,8 @@ LIST_WORKLOADS = {
     # (per param, per block and state)
     "lm1p5b-adam": dict(config="c5", opt="adam", desc="8-bit Adam, " + _LM, hp=None,
                         norms=(0, 0)),
+    "lm1p5b-adam-bf16": dict(config="c5bf16", opt="adam", norms=(0, 0), hp=None,
+                             desc="8-bit Adam, " + _LM.replace("fp16 grads", "bf16 grads")),
     "gpt2m-adamw": dict(config="c4", opt="adamw", hp=None, norms=(0, 0),
                         desc="8-bit AdamW, GPT-2-medium-shaped list: 24 layers, d=1024, ffn 4096, "
                              "vocab 50257, ctx 1024; fp32 params N(0,0.02), fp16 grads N(0,1e-4), "
@@ -317,7 +319,8 @@ def run_list(args, torch, bq, workloads):
     opt = bq.OPTIMIZERS[opt_name]
     nstates = 2 if opt_name in ("adam", "adamw", "lamb") else 1
     gdt_name = workloads.GRADS[config][0]
-    gdt = bq.BQ_F16 if gdt_name == "float16" else bq.BQ_F32
+    gdt = {"float16": bq.BQ_F16, "bfloat16": bq.BQ_BF16, "float32": bq.BQ_F32}[gdt_name]
+    gname = {"float16": "fp16", "bfloat16": "bf16", "float32": "fp32"}[gdt_name]
     torch.cuda.set_device(0)
     qs_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)).cuda()
     qu_d = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)).cuda()
@@ -329,7 +332,7 @@ def run_list(args, torch, bq, workloads):
                                                     zero1=zero1)
     numels = [s.numel for s in specs]
     nparams = sum(numels)
-    bytes_step = workload_bytes(args.workload, numels, B, 2 if gdt == bq.BQ_F16 else 4)
+    bytes_step = workload_bytes(args.workload, numels, B, 4 if gdt == bq.BQ_F32 else 2)
     if W["hp"]:
         hp = dict(W["hp"])
     else:
@@ -413,9 +416,9 @@ def run_list(args, torch, bq, workloads):
         args, metric, nparams / (ms / 1e3), "params/s", ms, seg, "f32",
         f"synthetic (seeded torch Philox on the GPU; shapes of the {args.workload} list)",
         {"workload": f"{desc}, blocksize {B}", "tensors": len(specs), "params": nparams,
-         "blocksize": B, "grad_dtype": "fp16" if gdt == bq.BQ_F16 else "fp32",
+         "blocksize": B, "grad_dtype": gname,
          "state_dtype": "u8", "path": args.path})
-    kname = (f"step_oneshot_kernel<{tag}, {'fp16' if gdt == bq.BQ_F16 else 'fp32'} grad, {B}>"
+    kname = (f"step_oneshot_kernel<{tag}, {gname} grad, {B}>"
              if args.path != "call" else f"step_kernel<{tag}> (persistent, call path)")
     if opt_name in ("lamb", "lars"):
         kname += " (+ norms_kernel and trust_ratio_kernel: the per-tensor norm pass)"

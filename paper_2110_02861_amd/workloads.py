@@ -25,8 +25,9 @@ C1 = dict(opt="adam", lr=1e-3, beta1=0.9, beta2=0.995, eps=1e-8, wd=0.0, blocksi
 C3 = dict(opt="momentum", lr=0.1, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4, blocksize=2048)
 C4 = dict(opt="adamw", lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.01, blocksize=2048)
 C5 = dict(opt="adam", lr=1e-3, beta1=0.9, beta2=0.995, eps=1e-8, wd=0.0, blocksize=2048)
+C5BF16 = C5  # the same list and optimizer with bf16 grads
 
-CONFIG_IDS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5, "p1b": 6}
+CONFIG_IDS = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5, "p1b": 6, "c5bf16": 7}
 
 
 @dataclass(frozen=True)
@@ -123,7 +124,7 @@ def paper_1b_specs():
 
 
 SPECS = {"c1": c1_specs, "c3": resnet50_specs, "c4": gpt2_medium_specs, "c5": lm_1p5b_specs,
-         "p1b": paper_1b_specs}
+         "p1b": paper_1b_specs, "c5bf16": lm_1p5b_specs}
 
 # Gradient distributions per configuration: (dtype, std, outlier prob, outlier factor).
 GRADS = {
@@ -132,6 +133,8 @@ GRADS = {
     "c4": ("float16", 1e-4, 0.0, 1.0),
     "c5": ("float16", 1e-4, 1e-4, 1000.0),
     "p1b": ("float32", 1.0, 0.0, 1.0),
+    # the 1.5B list with bf16 grads (generated on the GPU only)
+    "c5bf16": ("bfloat16", 1e-4, 1e-4, 1000.0),
 }
 
 
@@ -203,7 +206,7 @@ def init_param_device(spec: TensorSpec, out, seed: int, config: str, index: int)
 
 
 def grad_device(config: str, spec: TensorSpec, out, seed: int, index: int, step: int):
-    """Fill the flat grad tensor ``out`` (fp16 or fp32, on the GPU)."""
+    """Fill the flat grad tensor ``out`` (fp16, bf16 or fp32, on the GPU)."""
     import torch
     _, std, p, factor = GRADS[config]
     g = torch.Generator(device=out.device)
