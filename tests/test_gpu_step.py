@@ -364,9 +364,7 @@ def test_zero_learning_rate_keeps_params(opt, path):
         for d, g in zip(ds, gs):
             d.g.copy_(torch.from_numpy(g))
         say(f"lr=0 step {path} {opt} t={t}")
-        if path == "prepared":
-            plan.run_prepared(dict(hp, step=t), prepared)
-        elif plan is not None:
+        if plan is not None:
             plan.run(dict(hp, step=t), qs_d, qu_d if two else None)
         else:
             bq.bq_optimizer8bit_step(opt, B, bq.BQ_F16, rows, dict(hp, step=t), qs_d,
