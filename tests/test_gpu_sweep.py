@@ -1,6 +1,7 @@
-"""A seeded sweep over random combinations of the step's parameters against the
-oracle: optimizer, grad dtype, blocksize, path, codebook family, weight decay
-and a ragged tensor list, two steps each.
+"""Seeded sweeps over random configurations against the oracle: for the step,
+optimizer, grad dtype, blocksize, path, codebook family, weight decay and a
+ragged tensor list, two steps each; for quantize / dequantize (both quantize
+paths), length, blocksize, codebook and blocks of differing character.
 
 Every case is drawn from a fixed seed, so the sweep is the same on every run;
 it looks for interactions that the per-parameter grids elsewhere do not reach.
@@ -13,9 +14,11 @@ from __future__ import annotations
 
 import numpy as np
 import pytest
+import torch
 
 from paper_2110_02861_amd import bq
-from tests.gpu_helpers import needs_gpu
+from tests.gpu_helpers import codebooks_on_device, needs_gpu
+from tests.test_gpu_quant import _other_maps, run_pair
 from tests.test_gpu_step import HPS, _map_families, run_lists
 
 pytestmark = [pytest.mark.gpu, needs_gpu]
@@ -69,3 +72,67 @@ def test_random_configuration(opt, gdt, B, path, family, sizes, hp, seed):
     feedback = hp["wd"] != 0.0 and opt in ("adam", "momentum", "lars")
     run_lists(opt, B, gdt, sizes, steps=2, seed=seed, hp=hp, exact_codes=not feedback,
               path=path, maps=maps)
+
+
+# --- standalone quantize / dequantize ------------------------------------------
+
+QMAPS = ["signed", "unsigned", "inverse_signed", "inverse_unsigned", "linear_signed",
+         "linear_unsigned", "quantile_normal", "quantile_abs_t"]
+
+
+def _quant_cases():
+    rng = np.random.default_rng(20211006)
+    out = []
+    for k in range(30):
+        B = BLOCKS[rng.integers(len(BLOCKS))]
+        qname = QMAPS[rng.integers(len(QMAPS))]
+        kind = rng.integers(3)
+        if kind == 0:
+            n = int(rng.integers(1, 3 * 8192 + 10))
+        elif kind == 1:
+            n = int(B * rng.integers(1, 40) + rng.integers(-1, 2))
+        else:
+            n = int(rng.integers(100_000, 600_000))
+        out.append(pytest.param(B, qname, n, int(rng.integers(1 << 30)),
+                                id=f"{k:02d}-B{B}-{qname}-n{n}"))
+    return out
+
+
+def _mixed_values(n, B, seed):
+    """Blocks of differing character: normal, heavy-tailed, uniform, all zero,
+    tiny and huge scales, subnormals, and repeated values."""
+    rng = np.random.default_rng(seed)
+    x = np.empty(n, np.float32)
+    for b0 in range(0, n, B):
+        m = min(B, n - b0)
+        kind = rng.integers(8)
+        if kind == 0:
+            v = rng.standard_normal(m)
+        elif kind == 1:
+            v = rng.standard_t(3, m) * 1e-2
+        elif kind == 2:
+            v = rng.uniform(-1, 1, m)
+        elif kind == 3:
+            v = np.zeros(m)
+        elif kind == 4:
+            v = rng.standard_normal(m) * 1e-30
+        elif kind == 5:
+            v = rng.standard_normal(m) * 1e30
+        elif kind == 6:
+            v = rng.integers(-1000, 1001, m) * 2.0 ** -149  # subnormals
+        else:
+            v = np.repeat(rng.standard_normal(1), m)
+        x[b0:b0 + m] = v.astype(np.float32)
+    return x
+
+
+@pytest.mark.parametrize("B,qname,n,seed", _quant_cases())
+def test_random_quantize_configuration(B, qname, n, seed):
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    if qname in ("signed", "unsigned"):
+        q_h, q_d, signed = (qs, qs_d, True) if qname == "signed" else (qu, qu_d, False)
+    else:
+        q_h, signed = _other_maps()[qname]
+        q_d = torch.from_numpy(q_h).cuda()
+    x = _mixed_values(n, B, seed)
+    run_pair(q_h, q_d, x if signed else np.abs(x), B)
