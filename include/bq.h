@@ -5,7 +5,9 @@
  * "8-bit Optimizers via Block-wise Quantization" (ICLR 2022):
  *   - the dynamic (tree) quantization codebooks          (Sections 2.3, 3.2)
  *   - block-wise quantization and dequantization         (Sections 2.2, 3.1, Eq. 3-4)
- *   - the fused 8-bit Adam / AdamW / Momentum / AdaGrad step (Section 3, Eq. 1-2, App. H)
+ *   - the fused 8-bit Adam / AdamW / Momentum / AdaGrad step (Section 3, Eq. 1-2, App. H),
+ *     and LAMB / LARS through step plans (App. E)
+ *   - the quantile maps and their GPU estimator                 (App. F.2, App. G)
  *
  * Conventions shared by every call
  *   - Pointers named "device" must point to GPU memory of the current HIP
