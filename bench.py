@@ -513,6 +513,18 @@ def run_quant(args, torch, bq, workloads):
     ms, seg = timed(torch, stream, call, steps, warmup, 20)
     nbytes = n * 5 + nb * 4
     gbs = nbytes / (ms / 1e3) / 1e9
+    # round-trip error of the timed data, outside the timed region: quantize
+    # buffer set 0 again, dequantize it, compare with the input
+    torch.cuda.synchronize()
+    bq.bq_quantize_blockwise_prepared(prepared, xs[0], B, codes[0], absmax[0], stream=stream)
+    bq.bq_dequantize_blockwise(qs_d, codes[0], absmax[0], B, outs[0], stream=stream)
+    err = (outs[0].double() - xs[0].double()).abs()
+    round_trip = {"mean_abs_err": float(err.mean()), "max_abs_err": float(err.max()),
+                  "max_rel_err_of_block_absmax": float(
+                      (err.view(-1, B) / absmax[0].double().clamp_min(1e-300)[:, None]).max()
+                      if n % B == 0 else float("nan")),
+                  "mean_abs_value": float(xs[0].double().abs().mean())}
+    del err
     res = base_record(
         args, f"{what} elements/sec and achieved HBM GB/s (% of peak), 67M Student-t values",
         n / (ms / 1e3), "elements/s", ms, seg, "f32",
@@ -528,6 +540,7 @@ def run_quant(args, torch, bq, workloads):
                      "traffic": measured_traffic(args.workload, B, path), "bytes_per_step": nbytes,
                      "kernel": kname},
         "stream_ceiling": None, "cpu_baseline": None,
+        "round_trip": round_trip,
     })
     return res
 
