@@ -159,6 +159,11 @@ class Optimizer8bit(torch.optim.Optimizer):
 
     @torch.no_grad()
     def step(self, closure=None):
+        if torch.cuda.is_available() and torch.cuda.is_current_stream_capturing():
+            # the step count and hyperparameters travel as launch arguments: a
+            # replayed graph would repeat the captured step's bias correction
+            raise RuntimeError("8-bit optimizer steps cannot be captured into a graph; capture "
+                               "bq.StepPlan runs instead, with their hyperparameters fixed")
         loss = None
         if closure is not None:
             with torch.enable_grad():

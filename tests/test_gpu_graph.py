@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 import torch
 
-from paper_2110_02861_amd import bq
+from paper_2110_02861_amd import bq, optim
 from tests.gpu_helpers import codebooks_on_device, host, needs_gpu, say
 
 pytestmark = [pytest.mark.gpu, needs_gpu]
@@ -34,19 +34,22 @@ def grads_for(sizes, r):
                              .astype(np.float16)).cuda() for i, n in enumerate(sizes)]
 
 
-@pytest.mark.parametrize("path", ["plan", "call"])
+@pytest.mark.parametrize("path", ["plan", "prepared", "call"])
 def test_captured_step_replays_match_eager(path):
     sizes = [5000, 3 * 4096 + 11, 300]
     _, _, qs_d, qu_d = codebooks_on_device()
     eager, graphed = make_state(sizes, 1), make_state(sizes, 1)
     plans = {}
-    if path == "plan":
+    if path != "call":
         plans = {"e": bq.StepPlan(bq.BQ_ADAM, 2048, bq.BQ_F16, eager),
                  "g": bq.StepPlan(bq.BQ_ADAM, 2048, bq.BQ_F16, graphed)}
+    prepared = bq.prepare_codebook_pair(qs_d, qu_d)
 
     def run(rows, key, stream=None):
         if path == "plan":
             plans[key].run(HP, qs_d, qu_d, stream=stream)
+        elif path == "prepared":
+            plans[key].run_prepared(HP, prepared, stream=stream)
         else:
             bq.bq_optimizer8bit_step(bq.BQ_ADAM, 2048, bq.BQ_F16, rows, HP, qs_d, qu_d,
                                      stream=stream)
@@ -85,3 +88,24 @@ def test_captured_step_replays_match_eager(path):
                 assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), (path, r, i, name)
     for p in plans.values():
         p.close()
+
+
+def test_optimizer_step_refuses_capture():
+    """A drop-in optimizer step passes its step count as a launch argument, so a
+    replayed graph would repeat one step's bias correction: step() refuses to
+    run under capture, before it counts the step or launches anything."""
+    p = torch.nn.Parameter(torch.zeros(5000, device="cuda"))
+    p.grad = torch.full_like(p, 1e-3)
+    opt = optim.Adam8bit([p])
+    opt.step()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    say("capturing an optimizer step (refused)")
+    with pytest.raises(RuntimeError, match="cannot be captured"):
+        with torch.cuda.graph(graph):
+            opt.step()
+    torch.cuda.synchronize()
+    assert opt.state[p]["step"] == 1
+    opt.step()
+    torch.cuda.synchronize()
+    assert opt.state[p]["step"] == 2
