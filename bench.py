@@ -45,13 +45,13 @@ BLOCKSIZE = 2048
 # same-byte-mix stream) read their true bytes on MI355X.  Valid only for the
 # kernel sources the counters were taken on (sha256 below); otherwise the
 # bench reports traffic null.  Keys: (workload, blocksize, path).
-KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h"]
-TRAFFIC_SOURCES_SHA256 = "0d76975d85e08f302f3d5bee6550c143a59de91a2bc83a62588023a09456eea5"
+KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h", "bq_scalars.h"]
+TRAFFIC_SOURCES_SHA256 = "37425fe2ad9be4723820dba9d20c25bf4451292900e7dc9ae4286eadd3e382b9"
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132444.5, "write_kib": 9150411.633},
-    ("quantize", 2048, "plan"): {"fetch_kib": 131142.507, "write_kib": 65792.0},
-    ("dequantize", 2048, "call"): {"fetch_kib": 33809.151, "write_kib": 262165.391},
+    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132443.734, "write_kib": 9150411.539},
+    ("quantize", 2048, "plan"): {"fetch_kib": 131136.455, "write_kib": 65792.0},
+    ("dequantize", 2048, "call"): {"fetch_kib": 33815.63, "write_kib": 262176.85},
 }
 
 
@@ -397,6 +397,13 @@ def run_list(args, torch, bq, workloads):
 
         def step(i):
             plans[i % 2].run_prepared(dict(hp, step=i + 1), prepared, stream=stream)
+    elif args.path == "device":
+        plans = [bq.StepPlan(opt, B, gdt, r) for r in rows]
+        prepared = bq.prepare_codebook_pair(q1, q2, stream=stream)
+        hp_dev = bq.device_hparams(dict(hp, step=0))
+
+        def step(i):
+            plans[i % 2].run_device(hp_dev, prepared, advance=True, stream=stream)
     else:
         arrays = [(bq.make_tensor_array(r), len(r)) for r in rows]
 
@@ -432,8 +439,9 @@ def run_list(args, torch, bq, workloads):
             "frac": gbs / HBM_PEAK_GBS,
             "traffic": measured_traffic(args.workload, B, args.path),
             "bytes_per_step": bytes_step,
-            "kernel": kname + (" (+ prepare_kernel, ~7 us, inside the timed launch pair)"
-                               if args.path == "plan" else ""),
+            "kernel": kname + {"plan": " (+ prepare_kernel, ~7 us, inside the timed launch pair)",
+                               "device": " (+ scalars_kernel: the step's scalars from device "
+                                         "hyperparameters)"}.get(args.path, ""),
         },
         "stream_ceiling": None if ceiling is None else {
             "gbs": ceiling, "frac_of_peak": ceiling / HBM_PEAK_GBS,
@@ -454,7 +462,7 @@ def run_quant(args, torch, bq, workloads):
     """Standalone quantize or dequantize of 67,108,864 Student-t(3) x 1e-2
     values; four input / output buffer sets rotate so that no call finds its
     operands in the 256 MB last-level cache."""
-    if args.path in ("optim", "prepared"):
+    if args.path in ("optim", "prepared", "device"):
         print(f"--path {args.path} applies to the optimizer-step workloads (the quantize plan "
               "path already reads a codebook prepared once)", file=sys.stderr)
         sys.exit(2)
@@ -556,11 +564,14 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=16)
-    ap.add_argument("--path", choices=["plan", "prepared", "call", "optim"], default="plan",
+    ap.add_argument("--path", choices=["plan", "prepared", "device", "call", "optim"],
+                    default="plan",
                     help="plan: bq_step_plan_run (a prepare launch from the raw maps, then one "
                          "launch over the whole list) or, for quantize, the prepared codebook; "
                          "prepared: bq_step_plan_run_prepared (the maps' tables prepared once, "
-                         "before the timed steps); call: bq_optimizer8bit_step "
+                         "before the timed steps); device: bq_step_plan_run_device (as prepared, "
+                         "the hyperparameters read and the step advanced in device memory); "
+                         "call: bq_optimizer8bit_step "
                          "(descriptor chunks of 56 tensors) or bq_quantize_blockwise; optim: "
                          "the drop-in torch optimizer (Adam8bit / AdamW8bit / SGD8bit) with "
                          "the grads of the ring assigned to .grad before each step")

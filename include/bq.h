@@ -305,9 +305,9 @@ typedef struct bq_step_plan_s *bq_step_plan;
  * tensor list.  This is the only allocating call: it writes one 64-byte record
  * per tile (4096 elements; pointers at the tile's first element and block) to
  * device memory of the current device -- 16 bytes per 1,024 params -- and
- * reserves space for two prepared codebooks (and, for LAMB and LARS, 16 bytes
- * of partial norms per tile, 32 bytes per segment of up to 2048 tiles of one
- * tensor, and 12 bytes per tensor).
+ * reserves space for two prepared codebooks and 64 bytes of step scalars
+ * (and, for LAMB and LARS, 16 bytes of partial norms per tile, 32 bytes per
+ * segment of up to 2048 tiles of one tensor, and 12 bytes per tensor).
  * Besides the optimizers of bq_optimizer8bit_step, plans run (App. E lists
  * 8-bit versions of both; textbook forms, one trust ratio per tensor, from
  * the norms before the update, 1 when a norm is zero):
@@ -358,6 +358,30 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
  */
 bq_status bq_step_plan_run_prepared(bq_step_plan plan, const bq_hparams *hp, const void *prepared,
                                     hipStream_t stream);
+
+/*
+ * bq_step_plan_run_prepared with the hyperparameters read from device memory
+ * when the run executes, not when it is enqueued: the run can be captured into
+ * a HIP graph once and replayed as successive steps, with the learning rate
+ * (or any other field) changed in device memory between replays.  A one-wave
+ * launch first forms the per-step scalars from *hp_device, in the same double
+ * arithmetic as the host path, so a run gives the same bits as
+ * bq_step_plan_run_prepared with the same values.
+ *   hp_device     device, one bq_hparams, 8-byte aligned, owned by the caller;
+ *                 with advance_step = 1 its step is incremented by one and
+ *                 written back before it is used (start from step = 0 for a
+ *                 first step); with 0 it is read as is.  step must be >= 1
+ *                 when the run uses it (the host cannot check it).
+ *   advance_step  0 or 1
+ *   prepared      as bq_step_plan_run_prepared
+ * The plan's scalar workspace (64 bytes, allocated by bq_step_plan_create) is
+ * written by every such run: runs of one plan must not overlap.  An empty
+ * plan still advances the step.  Allocates nothing.
+ * Errors: BQ_ERR_NULL, BQ_ERR_ALIGN, BQ_ERR_ARG (advance_step not 0 or 1,
+ * wrong device), BQ_ERR_HIP.
+ */
+bq_status bq_step_plan_run_device(bq_step_plan plan, bq_hparams *hp_device, int32_t advance_step,
+                                  const void *prepared, hipStream_t stream);
 
 /* Free a plan's device memory (synchronizes with the device).  NULL is a no-op. */
 bq_status bq_step_plan_destroy(bq_step_plan plan);

@@ -34,7 +34,7 @@ EXPORTS = ("bq_make_dynamic_codebook", "bq_make_codebook", "bq_make_quantile_cod
            "bq_optimizer8bit_step", "bq_optimizer32bit_step", "bq_prepare_codebook",
            "bq_quantize_blockwise_prepared",
            "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_run_prepared",
-           "bq_step_plan_destroy", "bq_status_string")
+           "bq_step_plan_run_device", "bq_step_plan_destroy", "bq_status_string")
 BQ_PREPARED_CODEBOOK_BYTES = 8720
 BQ_QUANTILE_CHUNK = 4096
 
@@ -104,6 +104,8 @@ def lib() -> ctypes.CDLL:
         L.bq_step_plan_run.restype = I
         L.bq_step_plan_run_prepared.argtypes = [P, P, P, P]
         L.bq_step_plan_run_prepared.restype = I
+        L.bq_step_plan_run_device.argtypes = [P, P, I32, P, P]
+        L.bq_step_plan_run_device.restype = I
         L.bq_step_plan_destroy.argtypes = [P]
         L.bq_step_plan_destroy.restype = I
         L.bq_status_string.argtypes = [I]
@@ -360,6 +362,20 @@ class StepPlan:
                                                _dev_ptr(prepared, "prepared"), _stream(stream)),
                "bq_step_plan_run_prepared")
 
+    def run_device(self, hp_device, prepared, advance: bool = True, stream=None):
+        """One run whose hyperparameters are read from device memory when it
+        executes (hp_device: device_hparams); capturable into a graph."""
+        import torch
+        need = (2 if self._two else 1) * BQ_PREPARED_CODEBOOK_BYTES
+        if prepared.dtype != torch.uint8 or prepared.numel() < need:
+            raise ValueError(f"prepared codebooks: need {need} uint8 bytes")
+        if hp_device.dtype != torch.uint8 or hp_device.numel() != ctypes.sizeof(bq_hparams):
+            raise ValueError("hp_device must come from device_hparams()")
+        _check(lib().bq_step_plan_run_device(self._h, _dev_ptr(hp_device, "hp_device"),
+                                             1 if advance else 0,
+                                             _dev_ptr(prepared, "prepared"), _stream(stream)),
+               "bq_step_plan_run_device")
+
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value is not None:
             lib().bq_step_plan_destroy(self._h)
@@ -383,6 +399,27 @@ def bq_step_plan_run(plan: StepPlan, hp: dict, qmap1, qmap2=None, stream=None):
 
 def bq_step_plan_run_prepared(plan: StepPlan, hp: dict, prepared, stream=None):
     plan.run_prepared(hp, prepared, stream)
+
+
+def bq_step_plan_run_device(plan: StepPlan, hp_device, prepared, advance=True, stream=None):
+    plan.run_device(hp_device, prepared, advance, stream)
+
+
+def device_hparams(hp: dict, device=None):
+    """A bq_hparams packed into a device uint8 tensor, for run_device.  Start
+    from step 0 with advance=True for a first step."""
+    import torch
+    h = _hparams(dict(hp, step=hp.get("step", 0)))
+    raw = ctypes.string_at(ctypes.addressof(h), ctypes.sizeof(h))
+    t = torch.frombuffer(bytearray(raw), dtype=torch.uint8)
+    return t.to("cuda" if device is None else device)
+
+
+def read_device_hparams(t) -> dict:
+    """The fields of a device bq_hparams (as written by device_hparams)."""
+    h = bq_hparams.from_buffer_copy(bytes(t.cpu().numpy().tobytes()))
+    return dict(lr=h.lr, beta1=h.beta1, beta2=h.beta2, eps=h.eps, wd=h.weight_decay,
+                step=h.step, trust=h.trust_coeff)
 
 
 def bq_step_plan_destroy(plan: StepPlan):

@@ -11,6 +11,7 @@
 
 #include "bq.h"
 #include "bq_internal.h"
+#include "bq_scalars.h"
 
 namespace {
 
@@ -28,51 +29,10 @@ bool trust_opt(bq_optimizer o) { return o == BQ_LAMB || o == BQ_LARS; }
 bool two_states(bq_optimizer o) { return o == BQ_ADAM || o == BQ_ADAMW || o == BQ_LAMB; }
 bool valid_dtype(bq_dtype d) { return d == BQ_F32 || d == BQ_F16 || d == BQ_BF16; }
 
-// beta^t in double by right-to-left binary exponentiation.
-double beta_pow(double beta, int64_t t)
-{
-    double acc = 1.0;
-    for (double sq = beta; t > 0; t >>= 1, sq *= sq)
-        if (t & 1)
-            acc *= sq;
-    return acc;
-}
-
-// Bias-corrected Adam (the paper's Eq. 2 omits the correction constants),
-// decoupled AdamW decay, and the L2 weight-decay term; each scalar is formed in
-// double from the fp32 inputs and rounded once to fp32.  AdaGrad has neither
-// bias correction nor momentum: its update w - lr g / (sqrt(r) + eps) uses
-// step_size = lr and inv_sqrt_bc2 = 1.
 bq::StepScalars make_scalars(const bq_hparams &hp, bq_optimizer opt)
 {
-    const double lr = hp.lr, b1 = hp.beta1, b2 = hp.beta2, wd = hp.weight_decay;
-    bq::StepScalars s;
-    s.b1 = hp.beta1;
-    s.omb1 = static_cast<float>(1.0 - b1);
-    s.b2 = hp.beta2;
-    s.omb2 = static_cast<float>(1.0 - b2);
-    s.eps = hp.eps;
-    s.lr = hp.lr;
-    s.wd = hp.weight_decay;
-    if (opt == BQ_ADAGRAD) {
-        s.step_size = hp.lr;
-        s.inv_sqrt_bc2 = 1.0f;
-    } else {
-        s.step_size = static_cast<float>(lr / (1.0 - beta_pow(b1, hp.step)));
-        s.inv_sqrt_bc2 = static_cast<float>(1.0 / std::sqrt(1.0 - beta_pow(b2, hp.step)));
-    }
-    s.decay = static_cast<float>(1.0 - lr * wd);
-    s.bc1_inv = static_cast<float>(1.0 / (1.0 - beta_pow(b1, hp.step)));
-    s.trust = hp.trust_coeff;
-    const double ss = static_cast<double>(s.step_size), fmax = 3.4028234663852886e38;
-    if (ss == 0.0) {
-        s.sdiv_c = 0.0f;
-        s.sdiv_eps = INFINITY;
-    } else {
-        s.sdiv_c = static_cast<float>(std::fmax(-fmax, std::fmin(fmax, s.inv_sqrt_bc2 / ss)));
-        s.sdiv_eps = static_cast<float>(std::fmax(-fmax, std::fmin(fmax, hp.eps / ss)));
-    }
-    return s;
+    return bq::make_scalars(hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay, hp.step,
+                            hp.trust_coeff, static_cast<int>(opt));
 }
 
 bq_status from_hip(hipError_t e) { return e == hipSuccess ? BQ_OK : BQ_ERR_HIP; }
@@ -138,6 +98,7 @@ struct bq_step_plan_s {
     int64_t *first_seg;
     float *lr_ratio;
     int64_t nsegments;
+    bq::DevScalars *dev_scalars;  // device, the scalars of device-hyperparameter runs
 };
 
 extern "C" {
@@ -271,7 +232,7 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
     args.q1 = qmap1;
     args.q2 = two ? qmap2 : qmap1;
     args.sc = make_scalars(*hp, opt);
-    args.use_wd = (hp->weight_decay != 0.0f && opt != BQ_ADAMW) ? 1 : 0;
+    args.use_wd = bq::l2_on_grad(hp->weight_decay, static_cast<int>(opt));
 
     // Pack non-empty tensors into launches of at most kMaxDescPerLaunch
     // descriptors, or fewer when a launch's tile count would overflow int32.
@@ -336,7 +297,7 @@ bq_status bq_optimizer32bit_step(bq_optimizer opt, bq_dtype grad_dtype,
     bq::State32Args args;
     std::memset(&args, 0, sizeof(args));
     args.sc = make_scalars(*hp, opt);
-    args.use_wd = (hp->weight_decay != 0.0f && opt != BQ_ADAMW) ? 1 : 0;
+    args.use_wd = bq::l2_on_grad(hp->weight_decay, static_cast<int>(opt));
     int32_t i = 0;
     while (i < ntensors) {
         int32_t k = 0;
@@ -480,6 +441,8 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
     hipError_t e = hipGetDevice(&p->device);
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&p->tables), 2 * bq::kPreparedBytes);
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&p->dev_scalars), sizeof(bq::DevScalars));
     if (e == hipSuccess && !recs.empty()) {
         e = hipMalloc(reinterpret_cast<void **>(&p->tiles), recs.size() * sizeof(bq::TensorDesc));
         if (e == hipSuccess)
@@ -529,14 +492,15 @@ bq_status check_run(bq_step_plan plan, const bq_hparams *hp)
     return BQ_OK;
 }
 
-// Launches one run of a plan.  With qmap1 set, the plan's own workspace is
-// prepared from the raw maps first; otherwise `tables` already holds both
-// prepared codebooks.
-bq_status launch_run(bq_step_plan plan, const bq_hparams *hp, const uint8_t *tables,
-                     const float *qmap1, const float *qmap2, hipStream_t stream)
+// Launches one run of a plan.  The hyperparameters come from the host (hp)
+// or, with hp NULL, from device memory (hp_dev, read by scalars_kernel when
+// the run executes; advance increments its step first).  With qmap1 set, the
+// plan's own workspace is prepared from the raw maps first; otherwise `tables`
+// already holds both prepared codebooks.
+bq_status launch_run(bq_step_plan plan, const bq_hparams *hp, bq_hparams *hp_dev, int advance,
+                     const uint8_t *tables, const float *qmap1, const float *qmap2,
+                     hipStream_t stream)
 {
-    if (plan->total_tiles == 0)
-        return BQ_OK;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess)
         return BQ_ERR_HIP;
@@ -554,14 +518,24 @@ bq_status launch_run(bq_step_plan plan, const bq_hparams *hp, const uint8_t *tab
     a.lr_ratio = plan->lr_ratio;
     a.ntensors = plan->ntensors;
     a.nsegments = (int32_t)plan->nsegments;
-    a.sc = make_scalars(*hp, plan->opt);
-    // decoupled decay for AdamW, inside the update direction for LAMB, an L2
-    // term on the gradient otherwise
-    a.use_wd = (hp->weight_decay != 0.0f && plan->opt != BQ_ADAMW && plan->opt != BQ_LAMB) ? 1
-                                                                                          : 0;
+    if (hp) {
+        a.sc = make_scalars(*hp, plan->opt);
+        // decoupled decay for AdamW, inside the update direction for LAMB, an
+        // L2 term on the gradient otherwise
+        a.use_wd = bq::l2_on_grad(hp->weight_decay, static_cast<int>(plan->opt));
+    } else {
+        a.dev = plan->dev_scalars;
+    }
     a.total_tiles = (int32_t)plan->total_tiles;
     hipError_t e = hipSuccess;
-    if (qmap1)
+    // a device step advances even for an empty plan, so that step counts stay
+    // in line with the caller's other plans
+    if (!hp)
+        e = bq::launch_scalars(static_cast<int>(plan->opt), hp_dev, advance, plan->dev_scalars,
+                               stream);
+    if (plan->total_tiles == 0)
+        return from_hip(e);
+    if (e == hipSuccess && qmap1)
         e = bq::launch_prepare(qmap1, two_states(plan->opt) ? qmap2 : nullptr, plan->tables,
                                stream);
     if (e == hipSuccess && trust_opt(plan->opt))
@@ -588,7 +562,9 @@ bq_status bq_step_plan_run(bq_step_plan plan, const bq_hparams *hp, const float 
         return BQ_ERR_NULL;
     if (!aligned(qmap1, 4) || (two && !aligned(qmap2, 4)))
         return BQ_ERR_ALIGN;
-    return launch_run(plan, hp, plan->tables, qmap1, qmap2, stream);
+    if (plan->total_tiles == 0)
+        return BQ_OK;
+    return launch_run(plan, hp, nullptr, 0, plan->tables, qmap1, qmap2, stream);
 }
 
 bq_status bq_step_plan_run_prepared(bq_step_plan plan, const bq_hparams *hp, const void *prepared,
@@ -601,7 +577,23 @@ bq_status bq_step_plan_run_prepared(bq_step_plan plan, const bq_hparams *hp, con
         return BQ_ERR_NULL;
     if (!aligned(prepared, 16))
         return BQ_ERR_ALIGN;
-    return launch_run(plan, hp, static_cast<const uint8_t *>(prepared), nullptr, nullptr, stream);
+    if (plan->total_tiles == 0)
+        return BQ_OK;
+    return launch_run(plan, hp, nullptr, 0, static_cast<const uint8_t *>(prepared), nullptr,
+                      nullptr, stream);
+}
+
+bq_status bq_step_plan_run_device(bq_step_plan plan, bq_hparams *hp_device, int32_t advance_step,
+                                  const void *prepared, hipStream_t stream)
+{
+    if (!plan || !hp_device || !prepared)
+        return BQ_ERR_NULL;
+    if (advance_step != 0 && advance_step != 1)
+        return BQ_ERR_ARG;
+    if (!aligned(hp_device, 8) || !aligned(prepared, 16))
+        return BQ_ERR_ALIGN;
+    return launch_run(plan, nullptr, hp_device, advance_step,
+                      static_cast<const uint8_t *>(prepared), nullptr, nullptr, stream);
 }
 
 bq_status bq_step_plan_destroy(bq_step_plan plan)
@@ -612,7 +604,7 @@ bq_status bq_step_plan_destroy(bq_step_plan plan)
     for (void *ptr : {static_cast<void *>(plan->tiles), static_cast<void *>(plan->tables),
                       static_cast<void *>(plan->partials), static_cast<void *>(plan->lr_ratio),
                       static_cast<void *>(plan->seg_range), static_cast<void *>(plan->seg_partials),
-                      static_cast<void *>(plan->first_seg)}) {
+                      static_cast<void *>(plan->first_seg), static_cast<void *>(plan->dev_scalars)}) {
         if (ptr && hipFree(ptr) != hipSuccess)
             e = hipErrorUnknown;
     }

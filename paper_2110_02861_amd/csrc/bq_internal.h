@@ -93,6 +93,15 @@ constexpr int kPreparedSignedBytes = kPreparedOffKmax;            // q, t, both 
 constexpr int kPreparedNonnegBytes = kPreparedOffBase + kPreparedBuckets;  // q, t, + half
 static_assert(kPreparedBytes % 16 == 0 && kPreparedNonnegBytes % 16 == 0, "16 B granules");
 
+// Scalars of a plan run formed on the device from device-resident
+// hyperparameters (scalars_kernel), read by the run's kernels in place of the
+// kernel-argument copy.
+struct DevScalars {
+    StepScalars sc;
+    int32_t use_wd;
+    int32_t pad;
+};
+
 // Arguments of the one-shot step kernel (one workgroup per tile).
 struct PlanArgs {
     const uint8_t *tables;        // prepared map of state 1, then of state 2
@@ -104,6 +113,8 @@ struct PlanArgs {
     StepScalars sc;
     int32_t use_wd;
     int32_t total_tiles;
+    // when set, sc and use_wd are read from here instead (formed on the device)
+    const DevScalars *dev;
     // LAMB / LARS only: per-tile partial squared norms (2 doubles per tile);
     // each tensor's tiles cut into segments of at most kTrustSegTiles tiles:
     // per segment its tile range [begin, end) and its 2 partial sums; first
@@ -163,6 +174,9 @@ hipError_t launch_step32(int opt, int grad_dtype, const State32Args &args, hipSt
 
 hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *tables,
                           hipStream_t stream);
+// The scalars of optimizer opt from device hyperparameters hp (a bq_hparams;
+// with advance, hp's step is incremented first and written back) into out.
+hipError_t launch_scalars(int opt, void *hp, int advance, DevScalars *out, hipStream_t stream);
 hipError_t launch_step_oneshot(int opt, int grad_dtype, int blocksize, const PlanArgs &args,
                                hipStream_t stream);
 // LAMB / LARS: per-tile partial norms, then the per-tensor lr * ratio.

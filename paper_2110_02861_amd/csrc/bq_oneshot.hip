@@ -15,12 +15,71 @@
 // maps): every workgroup builds the tables in its own LDS once and then runs
 // the same tile code (StepOS::tile, QuantOS::tile) over a grid-stride list of
 // tiles.
+#include "bq.h"
 #include "bq_device.h"
+#include "bq_scalars.h"
 
 namespace bq {
 namespace {
 
 using namespace dev;
+
+// The run's per-step scalars: formed on the device from device-resident
+// hyperparameters when the run has them (PlanArgs::dev), else the copy the
+// host placed in the kernel arguments.  The device copy does not change while
+// a kernel of the run executes, so it is read through the constant address
+// space: one scalar load, whose wait does not also wait for the tile's HBM
+// loads (a generic load became one vector load per field).
+__device__ inline DevScalars load_dev_scalars(const DevScalars *p)
+{
+    typedef const __attribute__((address_space(4))) uint32_t *cword;
+    constexpr int kWords = (int)(sizeof(DevScalars) / 4);
+    const cword src = (cword)p;
+    uint32_t w[kWords];
+#pragma unroll
+    for (int i = 0; i < kWords; ++i)
+        w[i] = src[i];
+    DevScalars d;
+    __builtin_memcpy(&d, w, sizeof(d));
+    return d;
+}
+__device__ inline StepScalars run_scalars(const PlanArgs &a)
+{
+    return a.dev ? load_dev_scalars(a.dev).sc : a.sc;
+}
+__device__ inline int run_use_wd(const PlanArgs &a)
+{
+    return a.dev ? load_dev_scalars(a.dev).use_wd : a.use_wd;
+}
+__device__ inline StepScalars run_scalars(const StepArgs &a) { return a.sc; }
+__device__ inline int run_use_wd(const StepArgs &a) { return a.use_wd; }
+
+// ---------------------------------------------------------------------------
+// Scalars of a run from device-resident hyperparameters (one wave)
+// ---------------------------------------------------------------------------
+
+// hp: a bq_hparams in device memory.  With advance, the step is incremented
+// first and written back, so that a captured run replays as the next step.
+// Every lane forms the same scalars; lane i stores word i, and lanes 0 and 1
+// the two halves of the new step count.
+__global__ __launch_bounds__(64) void scalars_kernel(bq_hparams *hp, int opt, int advance,
+                                                     DevScalars *out)
+{
+    const bq_hparams h = *hp;
+    const int64_t t = h.step + (advance ? 1 : 0);
+    DevScalars d;
+    d.sc = make_scalars(h.lr, h.beta1, h.beta2, h.eps, h.weight_decay, t, h.trust_coeff, opt);
+    d.use_wd = l2_on_grad(h.weight_decay, opt);
+    d.pad = 0;
+    constexpr int kWords = (int)(sizeof(DevScalars) / 4);
+    uint32_t w[kWords];
+    __builtin_memcpy(w, &d, sizeof(d));
+    const int i = threadIdx.x;
+    if (i < kWords)
+        G(reinterpret_cast<uint32_t *>(out))[i] = w[i];
+    if (advance && i < 2)
+        G(reinterpret_cast<uint32_t *>(&hp->step))[i] = (uint32_t)((uint64_t)t >> (32 * i));
+}
 
 constexpr int kOS = 512;  // threads per workgroup (quantize, dequantize)
 constexpr int kOSWaves = kOS / 64;
@@ -276,8 +335,8 @@ struct StepOS {
                 c2[4 * c + r] = (k2r[c] >> (8 * r)) & 0xffu;
             }
         }
-        const StepScalars &sc = a.sc;
-        if (a.use_wd) {
+        const StepScalars sc = run_scalars(a);
+        if (run_use_wd(a)) {
 #pragma unroll
             for (int i = 0; i < N; ++i)
                 g[i] = g[i] + sc.wd * w[i];
@@ -647,7 +706,7 @@ __global__ __launch_bounds__(kST) void norms_kernel(const PlanArgs a)
         }
         __syncthreads();
     }
-    const StepScalars &sc = a.sc;
+    const StepScalars sc = run_scalars(a);
     double sw = 0.0, sx = 0.0;
 #pragma unroll
     for (int i = 0; i < 4 * C; ++i) {
@@ -754,9 +813,10 @@ __global__ __launch_bounds__(kTrustThreads) void trust_ratio_kernel(const PlanAr
     }
     const double nw = sqrt(sw), nx = sqrt(sx);
     double ratio = 1.0;
+    const StepScalars sc = run_scalars(a);
     if (nw > 0.0 && nx > 0.0)
-        ratio = lamb ? nw / nx : (double)a.sc.trust * nw / (nx + (double)a.sc.wd * nw);
-    G(a.lr_ratio)[t] = (float)((double)a.sc.lr * ratio);
+        ratio = lamb ? nw / nx : (double)sc.trust * nw / (nx + (double)sc.wd * nw);
+    G(a.lr_ratio)[t] = (float)((double)sc.lr * ratio);
 }
 
 // ---------------------------------------------------------------------------
@@ -1114,6 +1174,13 @@ hipError_t launch_qp_t(const uint8_t *tables, const float *x, int64_t n, uint8_t
 }
 
 }  // namespace
+
+hipError_t launch_scalars(int opt, void *hp, int advance, DevScalars *out, hipStream_t stream)
+{
+    hipLaunchKernelGGL(scalars_kernel, dim3(1), dim3(64), 0, stream, static_cast<bq_hparams *>(hp),
+                       opt, advance, out);
+    return hipGetLastError();
+}
 
 hipError_t launch_prepare(const float *qmap1, const float *qmap2, uint8_t *tables,
                           hipStream_t stream)

@@ -163,7 +163,8 @@ class Optimizer8bit(torch.optim.Optimizer):
             # the step count and hyperparameters travel as launch arguments: a
             # replayed graph would repeat the captured step's bias correction
             raise RuntimeError("8-bit optimizer steps cannot be captured into a graph; capture "
-                               "bq.StepPlan runs instead, with their hyperparameters fixed")
+                               "bq.StepPlan.run_device runs instead (hyperparameters and step "
+                               "count in device memory)")
         loss = None
         if closure is not None:
             with torch.enable_grad():

@@ -188,6 +188,7 @@ def test_step_plan_argument_checks(L):
     r = L.bq_step_plan_run
     assert r(None, ctypes.byref(hp), A16, A16, None) == bq.BQ_ERR_NULL
     assert L.bq_step_plan_run_prepared(None, ctypes.byref(hp), A16, None) == bq.BQ_ERR_NULL
+    assert L.bq_step_plan_run_device(None, A16, 1, A16, None) == bq.BQ_ERR_NULL
     assert L.bq_step_plan_destroy(None) == bq.BQ_OK
 
 

@@ -109,3 +109,59 @@ def test_optimizer_step_refuses_capture():
     opt.step()
     torch.cuda.synchronize()
     assert opt.state[p]["step"] == 2
+
+
+def test_captured_device_hparam_run_replays_as_successive_steps():
+    """One captured run with device-resident hyperparameters, replayed four
+    times, is four successive steps (t = 1..4): each replay advances the step
+    in device memory.  The lr is rewritten in device memory between replays 2
+    and 3, as a schedule would.  Every replay equals an eager run given the
+    same step and lr by the host."""
+    sizes = [5000, 3 * 4096 + 11, 300]
+    _, _, qs_d, qu_d = codebooks_on_device()
+    eager, graphed = make_state(sizes, 2), make_state(sizes, 2)
+    pe = bq.StepPlan(bq.BQ_ADAM, 2048, bq.BQ_F16, eager)
+    pg = bq.StepPlan(bq.BQ_ADAM, 2048, bq.BQ_F16, graphed)
+    prepared = bq.prepare_codebook_pair(qs_d, qu_d)
+    hp = {k: v for k, v in HP.items() if k != "step"}
+    hp_dev = bq.device_hparams(dict(hp, step=0))
+    # warm up on a side stream with advance off (the step stays 0), then
+    # restore the graphed copy to the eager copy's state
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        warm = bq.device_hparams(dict(hp, step=1))
+        pg.run_device(warm, prepared, advance=False, stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for e, g in zip(eager, graphed):
+        for te, tg in zip(e, g):
+            tg.copy_(te)
+    torch.cuda.synchronize()
+    say("capturing a device-hyperparameter run")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        pg.run_device(hp_dev, prepared, advance=True, stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert bq.read_device_hparams(hp_dev)["step"] == 0  # capture ran nothing
+    for t in range(1, 5):
+        if t == 3:
+            hp["lr"] = hp["lr"] * 0.25
+            hp_dev.copy_(bq.device_hparams(dict(hp, step=t - 1)))
+        gs = grads_for(sizes, 10 + t)
+        for e, g, gr in zip(eager, graphed, gs):
+            e[1].copy_(gr)
+            g[1].copy_(gr)
+        torch.cuda.synchronize()
+        say(f"device-hyperparameter replay t={t}")
+        pe.run_prepared(dict(hp, step=t), prepared)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert bq.read_device_hparams(hp_dev)["step"] == t
+        for i, (e, g) in enumerate(zip(eager, graphed)):
+            for k, name in ((0, "param"), (2, "codes1"), (3, "codes2"), (4, "absmax1"),
+                            (5, "absmax2")):
+                a, b = host(e[k]), host(g[k])
+                assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), (t, i, name)
+    pe.close()
+    pg.close()

@@ -380,3 +380,53 @@ def test_zero_learning_rate_keeps_params(opt, path):
         assert np.any(hs[i].c1 != (127 if opt != "adagrad" else 0))  # the state moved
         if two:
             np.testing.assert_array_equal(host(ds[i].c2), hs[i].c2)
+
+
+@pytest.mark.parametrize("start", [0, 999_998])
+@pytest.mark.parametrize("opt", ["adam", "adamw", "momentum", "adagrad", "lamb", "lars"])
+def test_device_hyperparameters_match_host(opt, start):
+    """A run that reads its hyperparameters from device memory (advancing the
+    step there) gives the same bits as a run given the same values by the
+    host: the per-step scalars are formed by the same double arithmetic on
+    both sides.  The lr changes between steps 2 and 3."""
+    B = 2048
+    sizes = [1, 4097, 3 * 4096 + 77, 20000]
+    qs, qu, qs_d, qu_d = codebooks_on_device()
+    if opt == "adagrad":
+        qs, qs_d = qu, qu_d
+    two = opt in ("adam", "adamw", "lamb")
+    hp = dict(HPS[opt])
+    a, b = [], []
+    for i, n in enumerate(sizes):
+        w = np.random.default_rng([59, i]).uniform(-0.05, 0.05, n).astype(np.float32)
+        a.append(DevState(w, B, two, torch.float16))
+        b.append(DevState(w, B, two, torch.float16))
+    if opt == "adagrad":  # the unsigned map's zero code
+        for d in a + b:
+            d.c1.fill_(0)
+    pa = bq.StepPlan(opt, B, bq.BQ_F16, [d.row() for d in a])
+    pb = bq.StepPlan(opt, B, bq.BQ_F16, [d.row() for d in b])
+    prepared = bq.prepare_codebook_pair(qs_d, qu_d if two else None)
+    hp_dev = bq.device_hparams(dict(hp, step=start))
+    for k in range(1, 4):
+        t = start + k
+        if k == 3:  # a schedule: new lr in device memory, same on the host
+            hp["lr"] *= 0.5
+            hp_dev = bq.device_hparams(dict(hp, step=t - 1))
+        for i, n in enumerate(sizes):
+            g = (np.random.default_rng([59, i, k]).standard_normal(n) * 1e-3).astype(np.float16)
+            a[i].g.copy_(torch.from_numpy(g))
+            b[i].g.copy_(torch.from_numpy(g))
+        say(f"device hparams {opt} t={t}")
+        pa.run_prepared(dict(hp, step=t), prepared)
+        pb.run_device(hp_dev, prepared, advance=True)
+        torch.cuda.synchronize()
+        assert bq.read_device_hparams(hp_dev)["step"] == t
+        for da, db in zip(a, b):
+            for x, y in ((da.w, db.w), (da.c1, db.c1), (da.a1, db.a1)):
+                assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (opt, t)
+            if two:
+                for x, y in ((da.c2, db.c2), (da.a2, db.a2)):
+                    assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (opt, t)
+    pa.close()
+    pb.close()
