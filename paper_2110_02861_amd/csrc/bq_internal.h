@@ -8,7 +8,8 @@
 
 namespace bq {
 
-// Per-step fp32 scalars, each formed in double on the host and rounded once.
+// Per-step fp32 scalars, each formed in double and rounded once (make_scalars
+// in bq_scalars.h: on the host for the kernel arguments, or on the device).
 struct StepScalars {
     float b1, omb1;        // beta1, 1 - beta1
     float b2, omb2;        // beta2, 1 - beta2

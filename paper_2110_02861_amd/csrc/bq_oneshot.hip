@@ -5,9 +5,9 @@
 // threads per tile, chunks of 2048 elements with 4 contiguous elements per
 // thread, wave-contiguous non-temporal loads and stores (4096-element tiles
 // for the step, 8192 for quantize, 4096 for dequantize).  The decision tables
-// of each codebook are built once per call by prepare_kernel into a
-// prepared-codebook buffer and copied from there (L2) into LDS by every
-// workgroup.  On MI355X this shape streams the step's byte mix (read 4 + 2 +
+// of each codebook are built by prepare_kernel into a prepared-codebook buffer
+// (once per call, or once for all steps when the caller keeps the buffer) and
+// copied from there (L2) into LDS by every workgroup.  On MI355X this shape streams the step's byte mix (read 4 + 2 +
 // 1 + 1 B, write 4 + 1 + 1 B per element) faster than persistent workgroups,
 // which is why the hot path is organised this way.
 //
