@@ -359,33 +359,52 @@ def run_list(args, torch, bq, workloads):
         sys.exit(2)
 
     # a ring of two gradient buffers, one plan (or descriptor array) for each
-    if args.path == "optim":
+    if args.path in ("optim", "optim-graph"):
         from paper_2110_02861_amd import optim
         del states, rows
         torch.cuda.empty_cache()
         ps = [torch.nn.Parameter(w) for w in params]
         for p in ps:
             p.grad_dtype = None  # fp16 grads on fp32 params
+        cap = dict(capturable=args.path == "optim-graph")
         if opt_name == "momentum":
             opt_obj = optim.SGD8bit(ps, lr=hp["lr"], momentum=hp["beta1"],
-                                    weight_decay=hp["wd"], blocksize=B)
+                                    weight_decay=hp["wd"], blocksize=B, **cap)
         elif opt_name == "adagrad":
             opt_obj = optim.Adagrad8bit(ps, lr=hp["lr"], eps=hp["eps"], weight_decay=hp["wd"],
-                                        blocksize=B)
+                                        blocksize=B, **cap)
         elif opt_name == "lars":
             opt_obj = optim.Lars8bit(ps, lr=hp["lr"], momentum=hp["beta1"],
                                      weight_decay=hp["wd"], trust_coefficient=hp["trust"],
-                                     blocksize=B)
+                                     blocksize=B, **cap)
         else:
             cls = {"adam": optim.Adam8bit, "adamw": optim.AdamW8bit,
                    "lamb": optim.Lamb8bit}[opt_name]
             opt_obj = cls(ps, lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
-                          weight_decay=hp["wd"], blocksize=B)
+                          weight_decay=hp["wd"], blocksize=B, **cap)
 
         def step(i):
             for p, g in zip(ps, grads[i % 2]):
                 p.grad = g
             opt_obj.step()
+
+        if args.path == "optim-graph":
+            # one eager step per grad buffer creates the states and both plans;
+            # then step() is captured once per buffer and replayed
+            step(0)
+            step(1)
+            graphs = []
+            for r in (0, 1):
+                for p, g in zip(ps, grads[r]):
+                    p.grad = g
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph):
+                    opt_obj.step()
+                graphs.append(graph)
+            torch.cuda.synchronize()
+
+            def step(i):  # noqa: F811
+                graphs[i % 2].replay()
     elif args.path == "plan":
         plans = [bq.StepPlan(opt, B, gdt, r) for r in rows]
 
@@ -431,6 +450,9 @@ def run_list(args, torch, bq, workloads):
         kname += " (+ norms_kernel and trust_ratio_kernel: the per-tensor norm pass)"
     if args.path == "optim":
         kname += f" via optim.{type(opt_obj).__name__}.step()"
+    if args.path == "optim-graph":
+        kname += (f" via optim.{type(opt_obj).__name__}(capturable=True).step() captured in a "
+                  "HIP graph (+ scalars_kernel)")
     res.update({
         "gbs": gbs,
         "hbm_frac": gbs / HBM_PEAK_GBS,
@@ -462,7 +484,7 @@ def run_quant(args, torch, bq, workloads):
     """Standalone quantize or dequantize of 67,108,864 Student-t(3) x 1e-2
     values; four input / output buffer sets rotate so that no call finds its
     operands in the 256 MB last-level cache."""
-    if args.path in ("optim", "prepared", "device"):
+    if args.path in ("optim", "optim-graph", "prepared", "device"):
         print(f"--path {args.path} applies to the optimizer-step workloads (the quantize plan "
               "path already reads a codebook prepared once)", file=sys.stderr)
         sys.exit(2)
@@ -564,7 +586,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=16)
-    ap.add_argument("--path", choices=["plan", "prepared", "device", "call", "optim"],
+    ap.add_argument("--path", choices=["plan", "prepared", "device", "call", "optim",
+                                       "optim-graph"],
                     default="plan",
                     help="plan: bq_step_plan_run (a prepare launch from the raw maps, then one "
                          "launch over the whole list) or, for quantize, the prepared codebook; "
@@ -574,7 +597,9 @@ def main():
                          "call: bq_optimizer8bit_step "
                          "(descriptor chunks of 56 tensors) or bq_quantize_blockwise; optim: "
                          "the drop-in torch optimizer (Adam8bit / AdamW8bit / SGD8bit) with "
-                         "the grads of the ring assigned to .grad before each step")
+                         "the grads of the ring assigned to .grad before each step; "
+                         "optim-graph: the same optimizer built with capturable=True, its step() "
+                         "captured into a HIP graph once per grad buffer and replayed")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the 8-bit step has no cross-GPU exchange, and "

@@ -72,16 +72,24 @@ class Optimizer8bit(torch.optim.Optimizer):
     MAX_PLANS = 8  # cached step plans per optimizer (one per param subset)
 
     def __init__(self, params, defaults: dict, blocksize: int = 2048, min_8bit_size: int = 0,
-                 use_plans: bool = True):
+                 use_plans: bool = True, capturable: bool = False):
         if blocksize not in (256, 512, 1024, 2048, 4096):
             raise ValueError(f"blocksize must be a power of two in [256, 4096], got {blocksize}")
         if min_8bit_size < 0:
             raise ValueError("min_8bit_size must be >= 0")
+        if capturable and not use_plans:
+            raise ValueError("capturable steps run through step plans (use_plans=True)")
         self.blocksize = int(blocksize)
         self.min_8bit_size = int(min_8bit_size)
         self.use_plans = bool(use_plans)
+        # capturable: the hyperparameters and step count of every (group, grad
+        # dtype, device) bucket live in device memory (bq.device_hparams) and
+        # every step advances the count there, so a captured step() replays as
+        # successive steps
+        self.capturable = bool(capturable)
         self._override32: set = set()
         self._plans: dict = {}
+        self._hp_dev: dict = {}  # (group, grad dtype, device) -> (device hparams, params)
         super().__init__(params, defaults)
 
     # -- configuration --------------------------------------------------------
@@ -159,17 +167,18 @@ class Optimizer8bit(torch.optim.Optimizer):
 
     @torch.no_grad()
     def step(self, closure=None):
-        if torch.cuda.is_available() and torch.cuda.is_current_stream_capturing():
+        capturing = torch.cuda.is_available() and torch.cuda.is_current_stream_capturing()
+        if capturing and not self.capturable:
             # the step count and hyperparameters travel as launch arguments: a
             # replayed graph would repeat the captured step's bias correction
-            raise RuntimeError("8-bit optimizer steps cannot be captured into a graph; capture "
-                               "bq.StepPlan.run_device runs instead (hyperparameters and step "
-                               "count in device memory)")
+            raise RuntimeError("8-bit optimizer steps cannot be captured into a graph unless the "
+                               "optimizer is built with capturable=True (hyperparameters and "
+                               "step count in device memory)")
         loss = None
         if closure is not None:
             with torch.enable_grad():
                 loss = closure()
-        for group in self.param_groups:
+        for gi, group in enumerate(self.param_groups):
             # one pass over the params, bucketed by (8-bit, grad dtype, step,
             # device); every launch then covers one bucket
             buckets: dict = {}
@@ -180,6 +189,9 @@ class Optimizer8bit(torch.optim.Optimizer):
                 self._check_param(p, g)
                 state = self.state[p]
                 if not state:
+                    if capturing:
+                        raise RuntimeError("run one step outside graph capture first: it "
+                                           "creates the optimizer states and step plans")
                     self._init_state(p, state)
                 dev = p.get_device()
                 # the states were sized and placed for the param when they were made
@@ -189,8 +201,18 @@ class Optimizer8bit(torch.optim.Optimizer):
                 if s1.numel() != p.numel() or s1.get_device() != dev:
                     raise ValueError("a param changed size or device after its optimizer state "
                                      "was created")
-                step = state["step"] + 1
-                state["step"] = step
+                if self.capturable:
+                    if "state1" not in state:
+                        raise ValueError("capturable optimizers keep every state in 8 bit "
+                                         "(no override_32bit, min_8bit_size or stable embedding)")
+                    # the device count is the step; the host count follows it
+                    # at eager steps and in state_dict()
+                    step = 0
+                    if not capturing:
+                        state["step"] += 1
+                else:
+                    step = state["step"] + 1
+                    state["step"] = step
                 key = ("state1" in state, g.dtype, step, dev)
                 items = buckets.get(key)
                 if items is None:
@@ -198,8 +220,12 @@ class Optimizer8bit(torch.optim.Optimizer):
                 items.append((p, g, state))
             for (eight, gdtype, step, _), items in buckets.items():
                 gdt = _GRAD_DTYPES[gdtype]
-                hp = self._hparams(group, step)
                 device = items[0][0].device
+                if self.capturable:
+                    hp_dev = self._device_hparams(gi, group, gdt, device, items, capturing)
+                    self._step8(gdt, device, items, None, hp_dev, capturing)
+                    continue
+                hp = self._hparams(group, step)
                 if eight:
                     self._step8(gdt, device, items, hp)
                 else:
@@ -207,7 +233,56 @@ class Optimizer8bit(torch.optim.Optimizer):
                     bq.bq_optimizer32bit_step(self.OPT, gdt, rows, hp)
         return loss
 
-    def _step8(self, gdt: int, device, items, hp: dict) -> None:
+    def _device_hparams(self, gi, group, gdt, device, items, capturing):
+        """The device hyperparameters of one bucket: made at its first step
+        (from the host step count, which the run then advances), refreshed
+        from the group at every eager step except for the step count."""
+        key = (gi, gdt, device.index)
+        entry = self._hp_dev.get(key)
+        steps = {s["step"] for _, _, s in items}
+        if entry is None:
+            if capturing:
+                raise RuntimeError("run one step outside graph capture first: it creates the "
+                                   "device hyperparameters")
+            if len(steps) != 1:
+                raise RuntimeError("params of one capturable bucket must share their step count")
+            t = bq.device_hparams(self._hparams(group, steps.pop() - 1), device)
+            self._hp_dev[key] = (t, [p for p, _, _ in items])
+            return t
+        t, params = entry
+        if len(items) != len(params) or any(p is not q for (p, _, _), q in zip(items, params)):
+            raise RuntimeError("a capturable optimizer steps the same params every time")
+        if not capturing:
+            self._refresh(t, group)
+        return t
+
+    def _refresh(self, t, group) -> None:
+        """Copy a group's hyperparameters, but not the step count, to t."""
+        new = bq.device_hparams(self._hparams(group, 0), t.device)
+        t[:20].copy_(new[:20])   # lr, beta1, beta2, eps, weight_decay
+        t[32:].copy_(new[32:])   # trust coefficient (and padding)
+
+    def update_device_hparams(self) -> None:
+        """Capturable optimizers: copy every group's hyperparameters (e.g. a new
+        lr) to device memory, for graph replays that run no eager step.  Not
+        under capture."""
+        for (gi, _, _), (t, _) in self._hp_dev.items():
+            self._refresh(t, self.param_groups[gi])
+
+    def _sync_steps(self) -> None:
+        """Capturable optimizers: the host step counts from device memory."""
+        for t, params in self._hp_dev.values():
+            step = bq.read_device_hparams(t)["step"]
+            for p in params:
+                if self.state.get(p):
+                    self.state[p]["step"] = step
+
+    def state_dict(self):
+        if self._hp_dev:
+            self._sync_steps()
+        return super().state_dict()
+
+    def _step8(self, gdt: int, device, items, hp, hp_dev=None, capturing=False) -> None:
         rows = []
         key = [gdt, device.index]
         for p, g, s in items:
@@ -229,17 +304,25 @@ class Optimizer8bit(torch.optim.Optimizer):
         key = tuple(key)
         plan = self._plans.pop(key, None)
         if plan is None:
+            if capturing:
+                raise RuntimeError("no step plan for these tensors: run one step outside graph "
+                                   "capture with the same grad tensors first")
             plan = bq.StepPlan(self.OPT, self.blocksize, gdt, rows, keep=False)
         self._plans[key] = plan  # most recently used last
         while len(self._plans) > self.MAX_PLANS:
             oldest = next(iter(self._plans))
             self._plans.pop(oldest).close()
-        plan.run_prepared(hp, prepared_codebooks(device, self._state1_unsigned, self._two_states))
+        prepared = prepared_codebooks(device, self._state1_unsigned, self._two_states)
+        if hp_dev is not None:
+            plan.run_device(hp_dev, prepared, advance=True)
+        else:
+            plan.run_prepared(hp, prepared)
 
     def load_state_dict(self, state_dict):
         for plan in self._plans.values():
             plan.close()
         self._plans = {}
+        self._hp_dev = {}  # made again from the loaded step counts
         super().load_state_dict(state_dict)
         # torch casts every non-step state tensor to the param's dtype; the
         # codes (0..255) come through fp32 exactly and go back to uint8

@@ -165,3 +165,94 @@ def test_captured_device_hparam_run_replays_as_successive_steps():
                 assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), (t, i, name)
     pe.close()
     pg.close()
+
+
+CAPTURABLE = {
+    "adam": (optim.Adam8bit, dict(lr=1e-3, betas=(0.9, 0.995))),
+    "sgd": (optim.SGD8bit, dict(lr=0.1, momentum=0.9, weight_decay=1e-4)),
+    "lamb": (optim.Lamb8bit, dict(lr=1e-3, weight_decay=0.01)),
+}
+
+
+@pytest.mark.parametrize("case", list(CAPTURABLE))
+def test_capturable_optimizer_replays_match_eager(case):
+    """capturable=True: two eager steps, one captured step() replayed three
+    times (the lr halved through update_device_hparams before the last), then
+    an eager step again.  Every step equals a plain optimizer's eager step on
+    the same grads, bit for bit, and state_dict() reports the device count."""
+    cls, kw = CAPTURABLE[case]
+    sizes = [5000, 3 * 4096 + 11, 300]
+    rng = np.random.default_rng(3)
+    ws = [rng.uniform(-0.05, 0.05, n).astype(np.float32) for n in sizes]
+    pa = [torch.nn.Parameter(torch.from_numpy(w).cuda()) for w in ws]
+    pb = [torch.nn.Parameter(torch.from_numpy(w).cuda()) for w in ws]
+    grads = [torch.zeros(n, dtype=torch.float16, device="cuda") for n in sizes]
+    for p, q, g in zip(pa, pb, grads):
+        for x in (p, q):
+            if hasattr(x, "grad_dtype"):
+                x.grad_dtype = None  # fp16 grads on fp32 params
+            x.grad = g
+    oa = cls(pa, capturable=True, **kw)
+    ob = cls(pb, **kw)
+
+    def new_grads(t):
+        for i, (g, n) in enumerate(zip(grads, sizes)):
+            h = (np.random.default_rng([5, i, t]).standard_normal(n) * 1e-3).astype(np.float16)
+            g.copy_(torch.from_numpy(h))
+
+    def compare(t):
+        for i, (p, q) in enumerate(zip(pa, pb)):
+            assert torch.equal(p.detach().view(torch.uint8), q.detach().view(torch.uint8)), \
+                (case, t, i, "param")
+            sa, sb = oa.state[p], ob.state[q]
+            for k in ("state1", "absmax1", "state2", "absmax2"):
+                if k in sb:
+                    assert torch.equal(sa[k].view(torch.uint8), sb[k].view(torch.uint8)), \
+                        (case, t, i, k)
+
+    for t in (1, 2):
+        new_grads(t)
+        say(f"capturable {case}: eager step {t}")
+        oa.step()
+        ob.step()
+        torch.cuda.synchronize()
+        compare(t)
+    graph = torch.cuda.CUDAGraph()
+    say(f"capturable {case}: capturing step()")
+    with torch.cuda.graph(graph):
+        oa.step()
+    torch.cuda.synchronize()
+    for t in (3, 4, 5):
+        if t == 5:
+            for o in (oa, ob):
+                o.param_groups[0]["lr"] *= 0.5
+            oa.update_device_hparams()
+        new_grads(t)
+        say(f"capturable {case}: replay as step {t}")
+        graph.replay()
+        ob.step()
+        torch.cuda.synchronize()
+        compare(t)
+    assert all(s["step"] == 5 for s in oa.state_dict()["state"].values())
+    new_grads(6)
+    oa.step()
+    ob.step()
+    torch.cuda.synchronize()
+    compare(6)
+    assert all(s["step"] == 6 for s in oa.state_dict()["state"].values())
+
+
+def test_capturable_optimizer_needs_an_eager_step_first():
+    p = torch.nn.Parameter(torch.zeros(5000, device="cuda"))
+    p.grad = torch.full_like(p, 1e-3)
+    opt = optim.Adam8bit([p], capturable=True)
+    graph = torch.cuda.CUDAGraph()
+    say("capturing a capturable optimizer's first step (refused)")
+    with pytest.raises(RuntimeError, match="outside graph capture first"):
+        with torch.cuda.graph(graph):
+            opt.step()
+    torch.cuda.synchronize()
+    assert not opt.state[p]  # nothing was created
+    opt.step()
+    torch.cuda.synchronize()
+    assert opt.state[p]["step"] == 1

@@ -21,6 +21,8 @@ def test_hyperparameter_checks():
         optim.Adam8bit(p, blocksize=1000)
     with pytest.raises(ValueError):
         optim.Adam8bit(p, min_8bit_size=-1)
+    with pytest.raises(ValueError, match="plans"):
+        optim.Adam8bit(p, capturable=True, use_plans=False)
 
 
 def test_defaults_follow_torch():
