@@ -18,7 +18,11 @@ Every update runs in the HIP kernels of libbq:
 - 8-bit tensors go through a step plan (``bq_step_plan_run_prepared``: one
   launch over every tile of every tensor, with the fixed maps' decision tables
   prepared once per device), looked up by every storage pointer and size, or
-  through ``bq_optimizer8bit_step`` when ``use_plans=False``;
+  through ``bq_optimizer8bit_step`` when ``use_plans=False``; with
+  ``capturable=True`` through ``bq_step_plan_run_device``, whose
+  hyperparameters and step count live in device memory, so that ``step()``
+  can be captured into a HIP graph (after one eager step) and replayed as
+  successive steps;
 - 32-bit tensors go through ``bq_optimizer32bit_step``.
 
 Params must be fp32 CUDA tensors, contiguous and 16-byte aligned; grads fp32,
