@@ -46,12 +46,12 @@ BLOCKSIZE = 2048
 # kernel sources the counters were taken on (sha256 below); otherwise the
 # bench reports traffic null.  Keys: (workload, blocksize, path).
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h", "bq_scalars.h"]
-TRAFFIC_SOURCES_SHA256 = "37425fe2ad9be4723820dba9d20c25bf4451292900e7dc9ae4286eadd3e382b9"
+TRAFFIC_SOURCES_SHA256 = "c2525c131bd9c75cc24091f20c0c68f5659bfcc734dba514b16a5536d06de0bc"
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132443.734, "write_kib": 9150411.539},
-    ("quantize", 2048, "plan"): {"fetch_kib": 131136.455, "write_kib": 65792.0},
-    ("dequantize", 2048, "call"): {"fetch_kib": 33815.63, "write_kib": 262176.85},
+    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132444.016, "write_kib": 9150411.758},
+    ("quantize", 2048, "plan"): {"fetch_kib": 131136.466, "write_kib": 65792.0},
+    ("dequantize", 2048, "call"): {"fetch_kib": 33815.625, "write_kib": 262169.435},
 }
 
 
