@@ -46,12 +46,12 @@ BLOCKSIZE = 2048
 # kernel sources the counters were taken on (sha256 below); otherwise the
 # bench reports traffic null.  Keys: (workload, blocksize, path).
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h", "bq_scalars.h"]
-TRAFFIC_SOURCES_SHA256 = "c2525c131bd9c75cc24091f20c0c68f5659bfcc734dba514b16a5536d06de0bc"
+TRAFFIC_SOURCES_SHA256 = "1ef25aa5acf915a9ecf1492ad1dcfafe7cbca3408fa2bb3d4142b2574d253fcb"
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132444.016, "write_kib": 9150411.758},
-    ("quantize", 2048, "plan"): {"fetch_kib": 131136.466, "write_kib": 65792.0},
-    ("dequantize", 2048, "call"): {"fetch_kib": 33815.625, "write_kib": 262169.435},
+    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132447.781, "write_kib": 9150412.367},
+    ("quantize", 2048, "plan"): {"fetch_kib": 131136.489, "write_kib": 65792.0},
+    ("dequantize", 2048, "call"): {"fetch_kib": 33815.685, "write_kib": 262170.998},
 }
 
 

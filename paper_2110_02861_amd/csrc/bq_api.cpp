@@ -449,7 +449,8 @@ bq_status bq_step_plan_create(bq_optimizer opt, int32_t blocksize, bq_dtype grad
             e = hipMemcpy(p->tiles, recs.data(), recs.size() * sizeof(bq::TensorDesc),
                           hipMemcpyHostToDevice);
         if (e == hipSuccess && trust) {
-            e = hipMalloc(reinterpret_cast<void **>(&p->partials), recs.size() * 2 * sizeof(double));
+            e = hipMalloc(reinterpret_cast<void **>(&p->partials),
+                          recs.size() * 2 * sizeof(double));
             if (e == hipSuccess)
                 e = hipMalloc(reinterpret_cast<void **>(&p->lr_ratio),
                               (size_t)nonempty * sizeof(float));
@@ -604,7 +605,8 @@ bq_status bq_step_plan_destroy(bq_step_plan plan)
     for (void *ptr : {static_cast<void *>(plan->tiles), static_cast<void *>(plan->tables),
                       static_cast<void *>(plan->partials), static_cast<void *>(plan->lr_ratio),
                       static_cast<void *>(plan->seg_range), static_cast<void *>(plan->seg_partials),
-                      static_cast<void *>(plan->first_seg), static_cast<void *>(plan->dev_scalars)}) {
+                      static_cast<void *>(plan->first_seg),
+                      static_cast<void *>(plan->dev_scalars)}) {
         if (ptr && hipFree(ptr) != hipSuccess)
             e = hipErrorUnknown;
     }

@@ -7,9 +7,10 @@
 // for the step, 8192 for quantize, 4096 for dequantize).  The decision tables
 // of each codebook are built by prepare_kernel into a prepared-codebook buffer
 // (once per call, or once for all steps when the caller keeps the buffer) and
-// copied from there (L2) into LDS by every workgroup.  On MI355X this shape streams the step's byte mix (read 4 + 2 +
-// 1 + 1 B, write 4 + 1 + 1 B per element) faster than persistent workgroups,
-// which is why the hot path is organised this way.
+// copied from there (L2) into LDS by every workgroup.  On MI355X this shape
+// streams the step's byte mix (read 4 + 2 + 1 + 1 B, write 4 + 1 + 1 B per
+// element) faster than persistent workgroups, which is why the hot path is
+// organised this way.
 //
 // Persistent kernels (the allocation-free calls, which get only the raw
 // maps): every workgroup builds the tables in its own LDS once and then runs
@@ -1196,11 +1197,21 @@ hipError_t launch_norms_b(int blocksize, const PlanArgs &a, hipStream_t stream)
 {
     const dim3 grid((unsigned)a.total_tiles), block(kST);
     switch (blocksize) {
-    case 256: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 256>), grid, block, 0, stream, a); break;
-    case 512: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 512>), grid, block, 0, stream, a); break;
-    case 1024: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 1024>), grid, block, 0, stream, a); break;
-    case 2048: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 2048>), grid, block, 0, stream, a); break;
-    case 4096: hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 4096>), grid, block, 0, stream, a); break;
+    case 256:
+        hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 256>), grid, block, 0, stream, a);
+        break;
+    case 512:
+        hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 512>), grid, block, 0, stream, a);
+        break;
+    case 1024:
+        hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 1024>), grid, block, 0, stream, a);
+        break;
+    case 2048:
+        hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 2048>), grid, block, 0, stream, a);
+        break;
+    case 4096:
+        hipLaunchKernelGGL((norms_kernel<OPT, GRAD, 4096>), grid, block, 0, stream, a);
+        break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -51,7 +51,8 @@ __global__ __launch_bounds__(kThreads32) void step32_kernel(const State32Args a)
             g[0] = g16_lo<GRAD>(gv.x); g[1] = g16_hi<GRAD>(gv.x);
             g[2] = g16_lo<GRAD>(gv.y); g[3] = g16_hi<GRAD>(gv.y);
         } else {
-            const vf4 gv = ld_nt(reinterpret_cast<const vf4 *>(static_cast<const float *>(D.grad) + e0));
+            const vf4 gv =
+                ld_nt(reinterpret_cast<const vf4 *>(static_cast<const float *>(D.grad) + e0));
             g[0] = gv.x; g[1] = gv.y; g[2] = gv.z; g[3] = gv.w;
         }
     } else {

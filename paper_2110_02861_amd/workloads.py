@@ -150,7 +150,8 @@ def host_rng(seed: int, config: str, tensor: int = 0, step: int = 0) -> np.rando
 def init_param_host(spec: TensorSpec, rng: np.random.Generator) -> np.ndarray:
     n = spec.numel
     if spec.init == "normal":
-        return (rng.standard_normal(n, dtype=np.float32) * np.float32(spec.scale)).astype(np.float32)
+        g = rng.standard_normal(n, dtype=np.float32)
+        return (g * np.float32(spec.scale)).astype(np.float32)
     if spec.init == "uniform":
         return rng.uniform(-spec.scale, spec.scale, n).astype(np.float32)
     if spec.init == "ones":
