@@ -169,8 +169,11 @@ def test_captured_device_hparam_run_replays_as_successive_steps():
 
 CAPTURABLE = {
     "adam": (optim.Adam8bit, dict(lr=1e-3, betas=(0.9, 0.995))),
+    "adamw": (optim.AdamW8bit, dict(lr=1e-3, weight_decay=0.01)),
     "sgd": (optim.SGD8bit, dict(lr=0.1, momentum=0.9, weight_decay=1e-4)),
+    "adagrad": (optim.Adagrad8bit, dict(lr=1e-2)),
     "lamb": (optim.Lamb8bit, dict(lr=1e-3, weight_decay=0.01)),
+    "lars": (optim.Lars8bit, dict(lr=0.5, momentum=0.9, weight_decay=1e-4)),
 }
 
 
