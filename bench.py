@@ -603,7 +603,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the 8-bit step has no cross-GPU exchange, and "
-              "this build runs on a single MI355X (use --gpus 1)", file=sys.stderr)
+              "the library runs on a single MI355X (use --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import torch
