@@ -430,3 +430,27 @@ def test_device_hyperparameters_match_host(opt, start):
                     assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (opt, t)
     pa.close()
     pb.close()
+
+
+def test_device_hyperparameter_run_edges():
+    """An empty plan still advances the device step; a misaligned hparams
+    pointer and an advance flag other than 0 / 1 are refused before launch."""
+    import ctypes
+    plan = bq.StepPlan("adam", 2048, bq.BQ_F16, [])
+    _, _, qs_d, qu_d = codebooks_on_device()
+    prepared = bq.prepare_codebook_pair(qs_d, qu_d)
+    hp_dev = bq.device_hparams(dict(HPS["adam"], step=41))
+    say("device hparams: empty plan")
+    plan.run_device(hp_dev, prepared, advance=True)
+    torch.cuda.synchronize()
+    assert bq.read_device_hparams(hp_dev)["step"] == 42
+    L = bq.lib()
+    P = ctypes.c_void_p
+    buf = torch.zeros(2 * ctypes.sizeof(bq.bq_hparams), dtype=torch.uint8, device="cuda")
+    assert L.bq_step_plan_run_device(plan._h, P(buf.data_ptr() + 4), 1, P(prepared.data_ptr()),
+                                     None) == bq.BQ_ERR_ALIGN
+    assert L.bq_step_plan_run_device(plan._h, P(hp_dev.data_ptr()), 2, P(prepared.data_ptr()),
+                                     None) == bq.BQ_ERR_ARG
+    torch.cuda.synchronize()
+    assert bq.read_device_hparams(hp_dev)["step"] == 42  # nothing ran
+    plan.close()
