@@ -315,8 +315,8 @@ def test_training_loop_reduces_loss():
         loss = torch.nn.functional.mse_loss(model(x), y)
         loss.backward()
         opt.step()
-        first = first if first is not None else float(loss)
-    final = float(loss)
+        first = first if first is not None else float(loss.detach())
+    final = float(loss.detach())
     assert final < 1e-3 * first, (first, final)
 
 

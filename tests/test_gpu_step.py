@@ -382,7 +382,7 @@ def test_zero_learning_rate_keeps_params(opt, path):
             np.testing.assert_array_equal(host(ds[i].c2), hs[i].c2)
 
 
-@pytest.mark.parametrize("start", [0, 999_998])
+@pytest.mark.parametrize("start", [0, 999_998, 2**40])
 @pytest.mark.parametrize("opt", ["adam", "adamw", "momentum", "adagrad", "lamb", "lars"])
 def test_device_hyperparameters_match_host(opt, start):
     """A run that reads its hyperparameters from device memory (advancing the
