@@ -94,6 +94,9 @@ class Optimizer8bit(torch.optim.Optimizer):
         self._override32: set = set()
         self._plans: dict = {}
         self._hp_dev: dict = {}  # (group, grad dtype, device) -> (device hparams, params)
+        # group index -> the last two steps' params, grad storages, pointers
+        # and launches; a step equal to one of them replays its launches
+        self._fast: dict = {}
         super().__init__(params, defaults)
 
     # -- configuration --------------------------------------------------------
@@ -182,10 +185,14 @@ class Optimizer8bit(torch.optim.Optimizer):
         if closure is not None:
             with torch.enable_grad():
                 loss = closure()
+        fast = self.use_plans and not self.capturable
         for gi, group in enumerate(self.param_groups):
+            if fast and self._replay(gi, group):
+                continue
             # one pass over the params, bucketed by (8-bit, grad dtype, step,
             # device); every launch then covers one bucket
             buckets: dict = {}
+            entries = []
             for p in group["params"]:
                 g = p.grad
                 if g is None:
@@ -222,6 +229,10 @@ class Optimizer8bit(torch.optim.Optimizer):
                 if items is None:
                     buckets[key] = items = []
                 items.append((p, g, state))
+                if fast:
+                    entries.append((p, state, s1, p.data_ptr(), g.data_ptr(), g.dtype,
+                                    p.numel()))
+            launches = []
             for (eight, gdtype, step, _), items in buckets.items():
                 gdt = _GRAD_DTYPES[gdtype]
                 device = items[0][0].device
@@ -231,11 +242,63 @@ class Optimizer8bit(torch.optim.Optimizer):
                     continue
                 hp = self._hparams(group, step)
                 if eight:
-                    self._step8(gdt, device, items, hp)
+                    plan = self._step8(gdt, device, items, hp)
+                    launches.append((plan, gdt, items[0][2], device))
                 else:
                     rows = [(p, g, s["exp_avg"], s.get("exp_avg_sq")) for p, g, s in items]
                     bq.bq_optimizer32bit_step(self.OPT, gdt, rows, hp)
+                    # params and states only: a record holds no grad
+                    launches.append(([(p, s) for p, _, s in items], gdt, items[0][2], None))
+            if fast:
+                # most recent first; two serve alternating grad buffers
+                self._fast[gi] = [(entries, launches)] + self._fast.get(gi, [])[:1]
         return loss
+
+    def _replay(self, gi: int, group: dict) -> bool:
+        """Repeat one of group gi's last two steps if this step is the same:
+        the same params, each with a grad at the same storage (pointer, dtype,
+        size, dense and contiguous), and the same param storages and state
+        tensors.  The checks, buckets and plan lookups of that step then still
+        hold, and only the step counts advance.  Returns False, having changed
+        nothing, otherwise."""
+        for entries, launches in self._fast.get(gi, ()):
+            if self._same_step(group, entries):
+                break
+        else:
+            return False
+        for e in entries:
+            e[1]["step"] += 1
+        for what, gdt, ref, device in launches:
+            hp = self._hparams(group, ref["step"])
+            if device is None:
+                rows = [(p, p.grad, s["exp_avg"], s.get("exp_avg_sq")) for p, s in what]
+                bq.bq_optimizer32bit_step(self.OPT, gdt, rows, hp)
+            else:
+                what.run_prepared(hp, prepared_codebooks(device, self._state1_unsigned,
+                                                         self._two_states))
+        return True
+
+    @staticmethod
+    def _same_step(group: dict, entries) -> bool:
+        n = len(entries)
+        i = 0
+        for p in group["params"]:
+            g = p.grad
+            if g is None:
+                continue
+            if i == n:
+                return False
+            q, state, s1, pp, gp, gdtype, numel = entries[i]
+            if q is not p or p.data_ptr() != pp or g.dtype is not gdtype:
+                return False
+            if g.layout is not torch.strided or g.data_ptr() != gp:
+                return False
+            if g.numel() != numel or p.numel() != numel or not g.is_contiguous():
+                return False
+            if state.get("state1", state.get("exp_avg")) is not s1:
+                return False
+            i += 1
+        return i == n
 
     def _device_hparams(self, gi, group, gdt, device, items, capturing):
         """The device hyperparameters of one bucket: made at its first step
@@ -298,7 +361,7 @@ class Optimizer8bit(torch.optim.Optimizer):
         if not self.use_plans and self.OPT not in (bq.BQ_LAMB, bq.BQ_LARS):
             q1, q2, _, _ = self._maps(device)
             bq.bq_optimizer8bit_step(self.OPT, self.blocksize, gdt, rows, hp, q1, q2)
-            return
+            return None
         # A plan holds device pointers and is a function of them and the sizes
         # alone: look it up by every storage pointer and size, so a plan runs
         # only on the storages it was built for.  Plans keep no references to
@@ -316,17 +379,20 @@ class Optimizer8bit(torch.optim.Optimizer):
         while len(self._plans) > self.MAX_PLANS:
             oldest = next(iter(self._plans))
             self._plans.pop(oldest).close()
+            self._fast = {}  # a remembered step may hold the closed plan
         prepared = prepared_codebooks(device, self._state1_unsigned, self._two_states)
         if hp_dev is not None:
             plan.run_device(hp_dev, prepared, advance=True)
         else:
             plan.run_prepared(hp, prepared)
+        return plan
 
     def load_state_dict(self, state_dict):
         for plan in self._plans.values():
             plan.close()
         self._plans = {}
         self._hp_dev = {}  # made again from the loaded step counts
+        self._fast = {}
         super().load_state_dict(state_dict)
         # torch casts every non-step state tensor to the param's dtype; the
         # codes (0..255) come through fp32 exactly and go back to uint8

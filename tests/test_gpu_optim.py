@@ -426,3 +426,67 @@ def test_param_resized_after_state_raises(case):
         with pytest.raises(ValueError, match="changed size"):
             opt.step()
         torch.cuda.synchronize()
+
+
+def test_repeated_steps_replay_and_match_oracle():
+    """Steps whose params, grad storages and states equal one of the last two
+    steps replay that step's launches (two grad buffers in turn, updated in
+    place; one param on 32-bit states).  Every step still matches the oracle,
+    a new lr takes effect in a replay, and a param moved to new storage falls
+    back to the full path."""
+    kind = oracle.ADAM
+    kw = dict(lr=1e-3, betas=(0.9, 0.995), eps=1e-8, weight_decay=0.0)
+    hp = oracle_hp(kw)
+    params = init_params(13)
+    opt = optim.Adam8bit(params, blocksize=B, **kw)
+    opt.override_32bit(params[2])
+    bufs = [[torch.zeros(p.numel(), dtype=torch.float16, device="cuda").view(p.shape)
+             for p in params] for _ in range(2)]
+    replays = []
+    real_replay = opt._replay
+    opt._replay = lambda gi, group: replays.append(real_replay(gi, group)) or replays[-1]
+    for t in range(1, 7):
+        if t == 4:
+            hp["lr"] = kw["lr"] * 0.5
+            opt.param_groups[0]["lr"] = hp["lr"]
+        if t == 6:  # a param moved to new storage: the full path again
+            params[0].data = params[0].data.clone()
+        gs = grads(13, t, np.float16)
+        buf = bufs[t % 2]
+        refs = []
+        for i, (p, g) in enumerate(zip(params, gs)):
+            buf[i].copy_(torch.from_numpy(np.ascontiguousarray(g)))
+            snap = snapshot(opt, p)
+            if i == 2:
+                w = host(p).ravel().copy()
+                m = snap["exp_avg"].copy() if snap else np.zeros(p.numel(), np.float32)
+                v = snap["exp_avg_sq"].copy() if snap else np.zeros(p.numel(), np.float32)
+                oracle.step32(kind, w, g.ravel().astype(np.float32), m, v, hp["lr"],
+                              hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], t)
+                refs.append((w, m, v))
+            else:
+                refs.append(oracle_step8(kind, hp, host(p).ravel(), g.ravel(), snap, p.numel(),
+                                         True, t))
+            if hasattr(p, "grad_dtype"):
+                p.grad_dtype = None
+            p.grad = buf[i]
+        say(f"optim replay step {t}")
+        w_before = [host(p).ravel().astype(np.float64) for p in params]
+        opt.step()
+        torch.cuda.synchronize()
+        for i, (p, ref) in enumerate(zip(params, refs)):
+            s = opt.state[p]
+            assert s["step"] == t
+            if i == 2:
+                w, m, v = ref
+                assert np.array_equal(host(s["exp_avg"]), m), (t, "m")
+                assert np.array_equal(host(s["exp_avg_sq"]), v), (t, "v")
+            else:
+                w, c1, a1, c2, a2 = ref
+                for k, r in (("state1", c1), ("absmax1", a1), ("state2", c2), ("absmax2", a2)):
+                    assert np.array_equal(host(s[k]), r), (t, i, k)
+            upd = np.abs(w_before[i] - w.astype(np.float64))
+            ok, worst = param_close(host(p).ravel(), w, 1e-6 * upd)
+            assert ok, (t, i, worst)
+    # steps 3-5 repeat the storages of steps 1-3; step 6 has a moved param
+    assert replays == [False, False, True, True, True, False], replays
