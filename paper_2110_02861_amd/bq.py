@@ -376,6 +376,9 @@ class StepPlan:
                                              _dev_ptr(prepared, "prepared"), _stream(stream)),
                "bq_step_plan_run_device")
 
+    def is_open(self) -> bool:
+        return getattr(self, "_h", None) is not None and self._h.value is not None
+
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value is not None:
             lib().bq_step_plan_destroy(self._h)

@@ -262,7 +262,8 @@ class Optimizer8bit(torch.optim.Optimizer):
         hold, and only the step counts advance.  Returns False, having changed
         nothing, otherwise."""
         for entries, launches in self._fast.get(gi, ()):
-            if self._same_step(group, entries):
+            if self._same_step(group, entries) and all(
+                    device is None or what.is_open() for what, _, _, device in launches):
                 break
         else:
             return False
@@ -376,7 +377,9 @@ class Optimizer8bit(torch.optim.Optimizer):
                                    "capture with the same grad tensors first")
             plan = bq.StepPlan(self.OPT, self.blocksize, gdt, rows, keep=False)
         self._plans[key] = plan  # most recently used last
-        while len(self._plans) > self.MAX_PLANS:
+        # at least MAX_PLANS, and room for two grad buffers per param group and
+        # grad dtype, so that a step never evicts a plan it is about to reuse
+        while len(self._plans) > max(self.MAX_PLANS, 4 * len(self.param_groups)):
             oldest = next(iter(self._plans))
             self._plans.pop(oldest).close()
             self._fast = {}  # a remembered step may hold the closed plan

@@ -490,3 +490,40 @@ def test_repeated_steps_replay_and_match_oracle():
             assert ok, (t, i, worst)
     # steps 3-5 repeat the storages of steps 1-3; step 6 has a moved param
     assert replays == [False, False, True, True, True, False], replays
+
+
+def test_many_param_groups_keep_their_plans():
+    """Twelve param groups and two grad buffers in turn: after the first two
+    steps no plan is built again (the cache makes room for every group), and
+    every step equals the plan-free path."""
+    ngroups = 12
+    rng = np.random.default_rng(17)
+    ws = [rng.uniform(-0.05, 0.05, 3000 + 500 * i).astype(np.float32) for i in range(ngroups)]
+    pa = [torch.nn.Parameter(torch.from_numpy(w).cuda()) for w in ws]
+    pb = [torch.nn.Parameter(torch.from_numpy(w).cuda()) for w in ws]
+    opt_a = optim.Adam8bit([dict(params=[p], lr=1e-3 * (1 + i)) for i, p in enumerate(pa)])
+    opt_b = optim.Adam8bit([dict(params=[p], lr=1e-3 * (1 + i)) for i, p in enumerate(pb)],
+                           use_plans=False)
+    bufs = [[torch.zeros_like(p) for p in pa] for _ in range(2)]
+    seen = {}
+    for t in range(1, 7):
+        buf = bufs[t % 2]
+        for i, g in enumerate(buf):
+            g.copy_(torch.from_numpy(np.random.default_rng([17, i, t]).standard_normal(g.numel())
+                                     .astype(np.float32) * 1e-3))
+            pa[i].grad = g
+            pb[i].grad = g
+        say(f"optim 12 groups step {t}")
+        opt_a.step()
+        opt_b.step()
+        torch.cuda.synchronize()
+        if t > 2:
+            assert set(opt_a._plans) == set(seen), "a plan was built again"
+        for key, plan in opt_a._plans.items():
+            assert seen.setdefault(key, plan) is plan
+        for p, q in zip(pa, pb):
+            sa, sb = opt_a.state[p], opt_b.state[q]
+            for k in ("state1", "absmax1", "state2", "absmax2"):
+                assert torch.equal(sa[k], sb[k]), (t, k)
+            assert torch.all((p - q).abs() <= 1e-6 * p.abs() + 1e-8)
+    assert len(opt_a._plans) == 2 * ngroups
