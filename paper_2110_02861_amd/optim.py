@@ -93,6 +93,7 @@ class Optimizer8bit(torch.optim.Optimizer):
         self.capturable = bool(capturable)
         self._override32: set = set()
         self._plans: dict = {}
+        self._pinned: set = set()  # keys of plans used under graph capture: never evicted
         self._hp_dev: dict = {}  # (group, grad dtype, device) -> (device hparams, params)
         # group index -> the last two steps' params, grad storages, pointers
         # and launches; a step equal to one of them replays its launches
@@ -377,10 +378,13 @@ class Optimizer8bit(torch.optim.Optimizer):
                                    "capture with the same grad tensors first")
             plan = bq.StepPlan(self.OPT, self.blocksize, gdt, rows, keep=False)
         self._plans[key] = plan  # most recently used last
+        if capturing:
+            self._pinned.add(key)  # a captured graph reads this plan's memory
         # at least MAX_PLANS, and room for two grad buffers per param group and
         # grad dtype, so that a step never evicts a plan it is about to reuse
-        while len(self._plans) > max(self.MAX_PLANS, 4 * len(self.param_groups)):
-            oldest = next(iter(self._plans))
+        cap = max(self.MAX_PLANS, 4 * len(self.param_groups))
+        while len(self._plans) - len(self._pinned) > cap:
+            oldest = next(k for k in self._plans if k not in self._pinned)
             self._plans.pop(oldest).close()
             self._fast = {}  # a remembered step may hold the closed plan
         prepared = prepared_codebooks(device, self._state1_unsigned, self._two_states)
@@ -394,6 +398,7 @@ class Optimizer8bit(torch.optim.Optimizer):
         for plan in self._plans.values():
             plan.close()
         self._plans = {}
+        self._pinned = set()  # graphs captured before a load must be captured again
         self._hp_dev = {}  # made again from the loaded step counts
         self._fast = {}
         super().load_state_dict(state_dict)

@@ -261,3 +261,56 @@ def test_capturable_optimizer_needs_an_eager_step_first():
     opt.step()
     torch.cuda.synchronize()
     assert opt.state[p]["step"] == 1
+
+
+def test_captured_plans_survive_plan_cache_eviction():
+    """After a capture, eager steps on ten new grad storages overflow the plan
+    cache; the captured step's plan is never evicted, and a later replay still
+    equals an eager optimizer given the same sequence of grads."""
+    sizes = [5000, 300]
+    ws = [np.random.default_rng([8, i]).uniform(-0.05, 0.05, n).astype(np.float32)
+          for i, n in enumerate(sizes)]
+    pa = [torch.nn.Parameter(torch.from_numpy(w).cuda()) for w in ws]
+    pb = [torch.nn.Parameter(torch.from_numpy(w).cuda()) for w in ws]
+    oa = optim.Adam8bit(pa, capturable=True)
+    ob = optim.Adam8bit(pb)
+    static = [torch.zeros(n, device="cuda") for n in sizes]
+    keep = []  # every grad buffer stays alive, so each one is a new storage
+
+    def fill(bufs, t):
+        for i, (g, n) in enumerate(zip(bufs, sizes)):
+            g.copy_(torch.from_numpy(np.random.default_rng([9, i, t]).standard_normal(n)
+                                     .astype(np.float32) * 1e-3))
+
+    for p, q, g in zip(pa, pb, static):
+        p.grad, q.grad = g, g
+    fill(static, 0)
+    oa.step()
+    ob.step()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        oa.step()
+    torch.cuda.synchronize()
+    (pinned,) = oa._pinned
+    for t in range(1, 11):
+        bufs = [torch.zeros(n, device="cuda") for n in sizes]
+        keep.append(bufs)
+        fill(bufs, t)
+        for p, q, g in zip(pa, pb, bufs):
+            p.grad, q.grad = g, g
+        say(f"eager step on new grad storage {t}")
+        oa.step()
+        ob.step()
+    assert len(keep) > optim.Optimizer8bit.MAX_PLANS
+    assert pinned in oa._plans and oa._plans[pinned].is_open()
+    fill(static, 11)
+    for q, g in zip(pb, static):
+        q.grad = g
+    say("replay after evictions")
+    graph.replay()
+    ob.step()
+    torch.cuda.synchronize()
+    for p, q in zip(pa, pb):
+        assert torch.equal(p.detach().view(torch.uint8), q.detach().view(torch.uint8))
+        for k in ("state1", "absmax1", "state2", "absmax2"):
+            assert torch.equal(oa.state[p][k], ob.state[q][k]), k
