@@ -216,6 +216,45 @@ def bq_dequantize_blockwise(qmap, codes, absmax, blocksize: int, out=None, strea
     return out
 
 
+def _grad_torch_dtype(grad_dtype):
+    import torch
+    return {BQ_F32: torch.float32, BQ_F16: torch.float16,
+            BQ_BF16: torch.bfloat16}.get(int(grad_dtype))
+
+
+def check_step_tensors(opt, blocksize: int, grad_dtype: int, tensors) -> None:
+    """Sizes, dtypes and device of a step's (param, grad, state1, state2,
+    absmax1, absmax2) tuples.  The C ABI takes plain pointers and cannot see
+    them: a state or absmax array shorter than its param would be written
+    past its end.  Raises ValueError / TypeError."""
+    import torch
+    if isinstance(opt, str):
+        opt = OPTIMIZERS[opt]
+    two = int(opt) in (BQ_ADAM, BQ_ADAMW, BQ_LAMB)
+    gdt = _grad_torch_dtype(grad_dtype)
+    cur = torch.cuda.current_device()
+    B = int(blocksize)
+    for i, (p, g, s1, s2, a1, a2) in enumerate(tensors):
+        n = p.numel()
+        want = [(p, "param", torch.float32, n), (g, "grad", gdt, n), (s1, "state1", torch.uint8, n)]
+        if B > 0:
+            want.append((a1, "absmax1", torch.float32, (n + B - 1) // B))
+        if two:
+            want.append((s2, "state2", torch.uint8, n))
+            if B > 0:
+                want.append((a2, "absmax2", torch.float32, (n + B - 1) // B))
+        for t, name, dtype, size in want:
+            if not isinstance(t, torch.Tensor):
+                raise TypeError(f"tensor {i}: {name} must be a torch tensor")
+            if dtype is not None and t.dtype != dtype:
+                raise TypeError(f"tensor {i}: {name} must be {dtype}, got {t.dtype}")
+            if t.numel() < size:
+                raise ValueError(f"tensor {i}: {name} holds {t.numel()} elements, needs {size}")
+            if t.is_cuda and t.get_device() != cur:
+                raise ValueError(f"tensor {i}: {name} is on cuda:{t.get_device()}, the current "
+                                 f"device is cuda:{cur}")
+
+
 def make_tensor_array(tensors):
     """Pack (param, grad, state1, state2, absmax1, absmax2) tuples of GPU
     tensors (state2 / absmax2 may be None) into a ctypes bq_tensor array."""
@@ -238,8 +277,9 @@ def bq_optimizer8bit_step(opt, blocksize: int, grad_dtype: int, tensors, hp: dic
     if isinstance(opt, str):
         opt = OPTIMIZERS[opt]
     if isinstance(tensors, tuple) and len(tensors) == 2 and isinstance(tensors[1], int):
-        arr, count = tensors
+        arr, count = tensors  # prebuilt by the caller, who vouches for the sizes
     else:
+        check_step_tensors(opt, blocksize, grad_dtype, tensors)
         arr, count = make_tensor_array(tensors), len(tensors)
     h = _hparams(hp)
     _check(lib().bq_optimizer8bit_step(int(opt), int(blocksize), int(grad_dtype), arr, count,
@@ -264,8 +304,27 @@ def make_tensor32_array(tensors):
 
 def bq_optimizer32bit_step(opt, grad_dtype: int, tensors, hp: dict, stream=None):
     """One step with fp32 states over (param, grad, state1, state2) tuples."""
+    import torch
     if isinstance(opt, str):
         opt = OPTIMIZERS[opt]
+    two = int(opt) in (BQ_ADAM, BQ_ADAMW)
+    gdt = _grad_torch_dtype(grad_dtype)
+    cur = torch.cuda.current_device()
+    for i, (p, g, m, v) in enumerate(tensors):
+        n = p.numel()
+        want = [(p, "param", torch.float32), (g, "grad", gdt), (m, "state1", torch.float32)]
+        if two:
+            want.append((v, "state2", torch.float32))
+        for t, name, dtype in want:
+            if not isinstance(t, torch.Tensor):
+                raise TypeError(f"tensor {i}: {name} must be a torch tensor")
+            if dtype is not None and t.dtype != dtype:
+                raise TypeError(f"tensor {i}: {name} must be {dtype}, got {t.dtype}")
+            if t.numel() < n:
+                raise ValueError(f"tensor {i}: {name} holds {t.numel()} elements, needs {n}")
+            if t.is_cuda and t.get_device() != cur:
+                raise ValueError(f"tensor {i}: {name} is on cuda:{t.get_device()}, the current "
+                                 f"device is cuda:{cur}")
     arr = make_tensor32_array(tensors)
     h = _hparams(hp)
     _check(lib().bq_optimizer32bit_step(int(opt), int(grad_dtype), arr, len(tensors),
@@ -338,6 +397,7 @@ class StepPlan:
         if isinstance(opt, str):
             opt = OPTIMIZERS[opt]
         self._keep = [t for row in tensors for t in row if t is not None] if keep else []
+        check_step_tensors(opt, blocksize, grad_dtype, tensors)
         arr = make_tensor_array(tensors)
         h = ctypes.c_void_p()
         _check(lib().bq_step_plan_create(int(opt), int(blocksize), int(grad_dtype), arr,

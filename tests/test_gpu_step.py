@@ -454,3 +454,34 @@ def test_device_hyperparameter_run_edges():
     torch.cuda.synchronize()
     assert bq.read_device_hparams(hp_dev)["step"] == 42  # nothing ran
     plan.close()
+
+
+def test_binding_refuses_mismatched_tensors():
+    """The C ABI sees only pointers, so the binding checks sizes and dtypes
+    before a launch: a state or absmax array too short for its param, or a
+    grad of another dtype than declared, raises and writes nothing."""
+    n, B = 5000, 2048
+    d = DevState(np.zeros(n, np.float32), B, True, torch.float16)
+    _, _, qs_d, qu_d = codebooks_on_device()
+    hp = dict(HPS["adam"], step=1)
+    short = torch.zeros(n - 1, dtype=torch.uint8, device="cuda")
+    short_absmax = torch.zeros(2, dtype=torch.float32, device="cuda")  # needs 3
+    bad = [
+        ((d.w, d.g, short, d.c2, d.a1, d.a2), ValueError),
+        ((d.w, d.g, d.c1, short, d.a1, d.a2), ValueError),
+        ((d.w, d.g, d.c1, d.c2, short_absmax, d.a2), ValueError),
+        ((d.w, d.g.float(), d.c1, d.c2, d.a1, d.a2), TypeError),
+        ((d.w.half(), d.g, d.c1, d.c2, d.a1, d.a2), TypeError),
+    ]
+    before = [t.clone() for t in d.row() if t is not None]
+    for row, err in bad:
+        with pytest.raises(err):
+            bq.bq_optimizer8bit_step("adam", B, bq.BQ_F16, [row], hp, qs_d, qu_d)
+        with pytest.raises(err):
+            bq.StepPlan("adam", B, bq.BQ_F16, [row])
+    torch.cuda.synchronize()
+    for x, y in zip(before, [t for t in d.row() if t is not None]):
+        assert torch.equal(x.view(torch.uint8), y.view(torch.uint8))  # bytes: g is uninitialised
+    m = torch.zeros(n - 1, device="cuda")
+    with pytest.raises(ValueError):
+        bq.bq_optimizer32bit_step("adam", bq.BQ_F16, [(d.w, d.g, m, torch.zeros_like(d.w))], hp)
