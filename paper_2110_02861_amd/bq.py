@@ -129,7 +129,19 @@ def _dev_ptr(t, name):
         raise TypeError(f"{name} must be a GPU torch tensor")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    if t.get_device() != torch.cuda.current_device():
+        # the C calls run on the current device
+        raise ValueError(f"{name} is on cuda:{t.get_device()}, the current device is "
+                         f"cuda:{torch.cuda.current_device()}")
     return t.data_ptr()
+
+
+def _map_ptr(q, name):
+    """A codebook: 256 fp32 values on the current device."""
+    import torch
+    if not isinstance(q, torch.Tensor) or q.dtype != torch.float32 or q.numel() != 256:
+        raise TypeError(f"{name} must be a tensor of 256 fp32 values")
+    return _dev_ptr(q, name)
 
 
 def _stream(stream):
@@ -159,11 +171,18 @@ def bq_estimate_quantile_codebook(x, out=None, workspace=None, stream=None):
     allocated here by torch unless given."""
     import torch
     n = x.numel()
+    if x.dtype != torch.float32:
+        raise TypeError("x must be fp32")
+    nbytes = max(8, int(lib().bq_quantile_workspace_bytes(n)))
     if workspace is None:
-        nbytes = max(8, int(lib().bq_quantile_workspace_bytes(n)))
         workspace = torch.empty(nbytes // 8, dtype=torch.float64, device=x.device)
+    elif workspace.numel() * workspace.element_size() < nbytes:
+        raise ValueError(f"workspace holds {workspace.numel() * workspace.element_size()} "
+                         f"bytes, needs {nbytes}")
     if out is None:
         out = torch.empty(256, dtype=torch.float32, device=x.device)
+    elif out.dtype != torch.float32 or out.numel() != 256:
+        raise TypeError("out must be a tensor of 256 fp32 values")
     _check(lib().bq_estimate_quantile_codebook(_dev_ptr(x, "x") if n else None, n,
                                                _dev_ptr(workspace, "workspace"),
                                                _dev_ptr(out, "out"), _stream(stream)),
@@ -193,7 +212,7 @@ def bq_quantize_blockwise(qmap, x, blocksize: int, codes=None, absmax=None, stre
         raise TypeError("x fp32, codes uint8, absmax fp32")
     if codes.numel() < n or absmax.numel() < (n + blocksize - 1) // blocksize:
         raise ValueError("output buffers too small")
-    _check(lib().bq_quantize_blockwise(_dev_ptr(qmap, "qmap"), _dev_ptr(x, "x"), n,
+    _check(lib().bq_quantize_blockwise(_map_ptr(qmap, "qmap"), _dev_ptr(x, "x"), n,
                                        int(blocksize), _dev_ptr(codes, "codes"),
                                        _dev_ptr(absmax, "absmax"), _stream(stream)),
            "bq_quantize_blockwise")
@@ -209,7 +228,7 @@ def bq_dequantize_blockwise(qmap, codes, absmax, blocksize: int, out=None, strea
         raise TypeError("codes uint8, absmax fp32, out fp32")
     if out.numel() < n or absmax.numel() < (n + blocksize - 1) // blocksize:
         raise ValueError("buffers too small")
-    _check(lib().bq_dequantize_blockwise(_dev_ptr(qmap, "qmap"), _dev_ptr(codes, "codes"),
+    _check(lib().bq_dequantize_blockwise(_map_ptr(qmap, "qmap"), _dev_ptr(codes, "codes"),
                                          _dev_ptr(absmax, "absmax"), n, int(blocksize),
                                          _dev_ptr(out, "out"), _stream(stream)),
            "bq_dequantize_blockwise")
@@ -283,8 +302,8 @@ def bq_optimizer8bit_step(opt, blocksize: int, grad_dtype: int, tensors, hp: dic
         arr, count = make_tensor_array(tensors), len(tensors)
     h = _hparams(hp)
     _check(lib().bq_optimizer8bit_step(int(opt), int(blocksize), int(grad_dtype), arr, count,
-                                       ctypes.byref(h), _dev_ptr(qmap1, "qmap1"),
-                                       None if qmap2 is None else _dev_ptr(qmap2, "qmap2"),
+                                       ctypes.byref(h), _map_ptr(qmap1, "qmap1"),
+                                       None if qmap2 is None else _map_ptr(qmap2, "qmap2"),
                                        _stream(stream)),
            "bq_optimizer8bit_step")
 
@@ -346,7 +365,7 @@ def bq_prepare_codebook(qmap, prepared=None, stream=None):
         prepared = torch.empty(BQ_PREPARED_CODEBOOK_BYTES, dtype=torch.uint8, device=qmap.device)
     if prepared.numel() < BQ_PREPARED_CODEBOOK_BYTES:
         raise ValueError("prepared buffer too small")
-    _check(lib().bq_prepare_codebook(_dev_ptr(qmap, "qmap"), _dev_ptr(prepared, "prepared"),
+    _check(lib().bq_prepare_codebook(_map_ptr(qmap, "qmap"), _dev_ptr(prepared, "prepared"),
                                      _stream(stream)), "bq_prepare_codebook")
     return prepared
 
@@ -407,8 +426,8 @@ class StepPlan:
 
     def run(self, hp: dict, qmap1, qmap2=None, stream=None):
         h = _hparams(hp)
-        _check(lib().bq_step_plan_run(self._h, ctypes.byref(h), _dev_ptr(qmap1, "qmap1"),
-                                      None if qmap2 is None else _dev_ptr(qmap2, "qmap2"),
+        _check(lib().bq_step_plan_run(self._h, ctypes.byref(h), _map_ptr(qmap1, "qmap1"),
+                                      None if qmap2 is None else _map_ptr(qmap2, "qmap2"),
                                       _stream(stream)), "bq_step_plan_run")
 
     def run_prepared(self, hp: dict, prepared, stream=None):
