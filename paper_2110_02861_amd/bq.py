@@ -383,6 +383,8 @@ def bq_quantize_blockwise_prepared(prepared, x, blocksize: int, codes=None, absm
         raise TypeError("x fp32, codes uint8, absmax fp32")
     if codes.numel() < n or absmax.numel() < (n + blocksize - 1) // blocksize:
         raise ValueError("output buffers too small")
+    if prepared.numel() * prepared.element_size() < BQ_PREPARED_CODEBOOK_BYTES:
+        raise ValueError(f"prepared codebook: need {BQ_PREPARED_CODEBOOK_BYTES} bytes")
     _check(lib().bq_quantize_blockwise_prepared(_dev_ptr(prepared, "prepared"), _dev_ptr(x, "x"),
                                                 n, int(blocksize), _dev_ptr(codes, "codes"),
                                                 _dev_ptr(absmax, "absmax"), _stream(stream)),
