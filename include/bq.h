@@ -138,7 +138,8 @@ int64_t bq_quantile_workspace_bytes(int64_t n);
  * divided by max |q_i|, rounded to fp32, equal entries moved up by one ulp (an
  * all-zero x gives 0 and then successive subnormals).  Inputs must be finite.
  * Stream-ordered; three launches.
- *   x          device, n fp32 (read), 4-byte aligned
+ *   x          device, n fp32 (read), 4-byte aligned (a view such as x + 1
+ *              is accepted; 16-byte aligned x is read 16 bytes per lane)
  *   workspace  device, bq_quantile_workspace_bytes(n) bytes, 8-byte aligned,
  *              caller-owned
  *   out        device, 256 fp32 (written)

@@ -55,8 +55,7 @@ def lib() -> ctypes.CDLL:
         L.oracle_codebook.restype = I
         L.oracle_quantile_codebook.argtypes = [P, ctypes.c_int64, P]
         L.oracle_quantile_codebook.restype = I
-        L.oracle_chunked_quantile_codebook.argtypes = [P, ctypes.c_int64, ctypes.c_int64,
-                                                       ctypes.c_int64, P]
+        L.oracle_chunked_quantile_codebook.argtypes = [P, ctypes.c_int64, ctypes.c_int64, P]
         L.oracle_chunked_quantile_codebook.restype = I
         L.oracle_nearest_brute.argtypes = [P, F]
         L.oracle_nearest_brute.restype = I
@@ -112,12 +111,12 @@ def quantile_codebook(sample) -> np.ndarray:
     return out
 
 
-def chunked_quantile_codebook(sample, chunk: int = 4096, group: int = 64) -> np.ndarray:
-    """Quantile map from length-weighted averages of per-chunk quantiles (App. G),
-    summed within groups of `group` chunks, then over groups."""
+def chunked_quantile_codebook(sample, chunk: int = 4096) -> np.ndarray:
+    """Quantile map from the length-weighted average of per-chunk quantiles (App. G),
+    summed in chunk order."""
     x = np.ascontiguousarray(sample, dtype=np.float32).ravel()
     out = np.empty(256, np.float32)
-    if lib().oracle_chunked_quantile_codebook(x.ctypes.data, x.size, int(chunk), int(group),
+    if lib().oracle_chunked_quantile_codebook(x.ctypes.data, x.size, int(chunk),
                                               out.ctypes.data) != 0:
         raise ValueError("chunked quantile map: empty or non-finite sample")
     return out

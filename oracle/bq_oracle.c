@@ -202,24 +202,24 @@ ORACLE_API int oracle_quantile_codebook(const float *x, int64_t n, float out[256
  * Chunked quantile estimate (App. G): the sample is cut into chunks of
  * `chunk` values (the last one shorter, length L_c); each chunk's sample
  * quantiles Q_c(i / 257) = sorted_c[floor(i L_c / 257)], i = 0..256, are
- * averaged with weights L_c: summed in double within groups of `group`
- * consecutive chunks in chunk order, the group sums summed in order, divided
- * by n (the fixed order makes the estimate reproducible).
- * Reading: App. G averages the per-chunk quantiles; weighting by length makes
- * a short last chunk count for what it holds.  The map then follows Eq. 5 as
- * in oracle_quantile_codebook, except that an all-zero map is kept (0, then
+ * averaged over the chunks.
+ * Reading: App. G averages the per-chunk quantiles; weighting each by its
+ * length L_c makes a short last chunk count for what it holds.  The weighted
+ * sum is accumulated in double in plain chunk order and divided by n (App. G
+ * accumulates atomically, i.e. in no fixed order; any order is the same
+ * average up to rounding).  The map then follows Eq. 5 as in
+ * oracle_quantile_codebook, except that an all-zero map is kept (0, then
  * successive subnormals after the tie separation) instead of rejected.
  * Returns 0, or -1 for n < 1, chunk < 1 or a non-finite value.
  */
 ORACLE_API int oracle_chunked_quantile_codebook(const float *x, int64_t n, int64_t chunk,
-                                               int64_t group, float out[256])
+                                               float out[256])
 {
-    if (n < 1 || chunk < 1 || group < 1)
+    if (n < 1 || chunk < 1)
         return -1;
-    double S[257], Sg[257];
+    double S[257];
     for (int i = 0; i <= 256; ++i)
-        S[i] = Sg[i] = 0.0;
-    int64_t in_group = 0;
+        S[i] = 0.0;
     double *s = (double *)malloc(sizeof(double) * (size_t)chunk);
     if (!s)
         return -1;
@@ -234,14 +234,7 @@ ORACLE_API int oracle_chunked_quantile_codebook(const float *x, int64_t n, int64
         }
         qsort(s, (size_t)L, sizeof(double), cmp_double);
         for (int i = 0; i <= 256; ++i)
-            Sg[i] += (double)L * (double)(float)s[(int64_t)i * L / 257];
-        if (++in_group == group || c0 + chunk >= n) {
-            for (int i = 0; i <= 256; ++i) {
-                S[i] += Sg[i];
-                Sg[i] = 0.0;
-            }
-            in_group = 0;
-        }
+            S[i] += (double)L * s[(int64_t)i * L / 257];
     }
     free(s);
     double Q[257], q[256], amax = 0.0;

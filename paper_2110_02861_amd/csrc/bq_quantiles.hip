@@ -144,11 +144,14 @@ __global__ __launch_bounds__(kQThreads) void chunk_quantiles_kernel(const float 
     const int64_t rem = n - c0;
     const int L = rem >= kQChunk ? kQChunk : (int)rem;
     const int tid = threadIdx.x;
+    // 16-byte loads need x itself 16-byte aligned (c0 is a multiple of 4096
+    // values); a view that is only 4-byte aligned takes the scalar loads
+    const bool vec = L == kQChunk && (reinterpret_cast<uintptr_t>(x) & 15u) == 0;
     uint32_t a[kQPerThread];
 #pragma unroll
     for (int h = 0; h < kQPerThread / 4; ++h) {
         const int e = 4 * tid + 4 * kQThreads * h;
-        if (L == kQChunk) {
+        if (vec) {
             const vf4 v = ld_nt(reinterpret_cast<const vf4 *>(x + c0 + e));
             a[4 * h] = order_key(v.x);
             a[4 * h + 1] = order_key(v.y);

@@ -6,10 +6,16 @@ configuration bench.py times).
 The oracle cannot step 1.5B parameters in seconds, but blocks are independent
 (Section 3.1: each block is normalized by its own absmax), so it steps a sample
 of blocks: the first and last (often partial) block of every tensor plus
-random blocks.  Their inputs are copied to the host before each GPU step; the
-oracle steps each sampled block on its own, and the GPU's bytes for those
-blocks must match: codes and absmax bit-exact, params within 1e-6 |w_ref| plus
-1e-6 of each step's update and one rounding of w, summed over the steps.
+random blocks.  Their inputs are copied to the host before each GPU step and
+the oracle steps each sampled block on its own.
+
+Strict checks are teacher-forced: before every GPU step the sampled blocks of
+the device tensors are overwritten with the oracle's param, codes and absmax
+(oracle -> GPU only), so each step is compared from one state: codes and
+absmax bit-exact, params within 1e-6 |w_ref| + 1e-6 |update| (the one-step
+bound).  A free-running run (no forcing) is reported, not asserted on params:
+a single code that flips at a bucket boundary moves later updates by a code
+step, far beyond 1e-6.
 """
 import numpy as np
 import pytest
@@ -58,7 +64,17 @@ def sample_blocks(specs, nrandom, seed):
     return sorted(picks)
 
 
-def run_sampled(config, opt, steps, nrandom, path):
+def _load_block(T, i, b, n, hb):
+    """Sampled block b of tensor i on the device := the oracle's state."""
+    s = slice(b * B, min((b + 1) * B, n))
+    T[i]["w"][s].copy_(torch.from_numpy(hb["w"]))
+    T[i]["c1"][s].copy_(torch.from_numpy(hb["c1"]))
+    T[i]["c2"][s].copy_(torch.from_numpy(hb["c2"]))
+    T[i]["a1"][b:b + 1].copy_(torch.from_numpy(hb["a1"]))
+    T[i]["a2"][b:b + 1].copy_(torch.from_numpy(hb["a2"]))
+
+
+def run_sampled(config, opt, steps, nrandom, path, forced=True):
     hp = {k: getattr(workloads, config.upper())[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
     gdtype = workloads.GRADS[config][0]
     tdt = torch.float16 if gdtype == "float16" else torch.float32
@@ -79,6 +95,7 @@ def run_sampled(config, opt, steps, nrandom, path):
                              c2=np.zeros(s.stop - s.start, np.uint8),
                              a1=np.zeros(1, np.float32), a2=np.zeros(1, np.float32),
                              tol=np.zeros(s.stop - s.start, np.float64))
+    worst_free, flips = 0.0, 0
     for t in range(1, steps + 1):
         say(f"{config}: generating grads t={t}")
         for i, s in enumerate(specs):
@@ -87,7 +104,11 @@ def run_sampled(config, opt, steps, nrandom, path):
         for (i, b) in picks:
             s = slice(b * B, min((b + 1) * B, specs[i].numel))
             grads[(i, b)] = host(T[i]["g"][s]).copy()
-        say(f"{config}: {path} step t={t} over {len(specs)} tensors")
+        if forced and t > 1:
+            for (i, b), hb in hostb.items():
+                _load_block(T, i, b, specs[i].numel, hb)
+        say(f"{config}: {path} step t={t} over {len(specs)} tensors"
+            f"{' (teacher-forced)' if forced else ' (free-running)'}")
         if plan is not None:
             plan.run(dict(hp, step=t), qs_d, qu_d)
         else:
@@ -100,15 +121,35 @@ def run_sampled(config, opt, steps, nrandom, path):
                          hb["c2"], hb["a2"], qu, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
                          hp["wd"], t)
             w64 = hb["w"].astype(np.float64)
-            hb["tol"] += 1e-6 * np.abs(prev - w64) + 2.0 ** -23 * np.abs(w64)
+            step_tol = 1e-6 * np.abs(prev - w64)
+            hb["tol"] += step_tol + 2.0 ** -23 * np.abs(w64)
             s = slice(b * B, min((b + 1) * B, specs[i].numel))
-            ok, worst = param_close(host(T[i]["w"][s]), hb["w"], hb["tol"])
-            assert ok, (config, t, specs[i].name, b, worst)
-            np.testing.assert_array_equal(host(T[i]["c1"][s]), hb["c1"])
-            np.testing.assert_array_equal(host(T[i]["c2"][s]), hb["c2"])
-            assert host(T[i]["a1"][b:b + 1])[0] == hb["a1"][0], (config, t, specs[i].name, b)
-            assert host(T[i]["a2"][b:b + 1])[0] == hb["a2"][0], (config, t, specs[i].name, b)
-    say(f"{config}: {len(picks)} sampled blocks matched over {steps} steps")
+            got_w = host(T[i]["w"][s])
+            got_c1, got_c2 = host(T[i]["c1"][s]), host(T[i]["c2"][s])
+            got_a1, got_a2 = host(T[i]["a1"][b:b + 1])[0], host(T[i]["a2"][b:b + 1])[0]
+            if forced:
+                ok, worst = param_close(got_w, hb["w"], step_tol)
+                assert ok, (config, t, specs[i].name, b, worst)
+                np.testing.assert_array_equal(got_c1, hb["c1"])
+                np.testing.assert_array_equal(got_c2, hb["c2"])
+                assert got_a1 == hb["a1"][0], (config, t, specs[i].name, b)
+                assert got_a2 == hb["a2"][0], (config, t, specs[i].name, b)
+            else:
+                # reported: the worst param excess over the accumulated bound
+                # (relative to |w|) and the codes that differ
+                d = np.abs(got_w.astype(np.float64) - w64) - (1e-6 * np.abs(w64) + hb["tol"])
+                worst_free = max(worst_free, float(np.max(d / np.maximum(np.abs(w64), 1e-30))))
+                flips += int(np.count_nonzero(got_c1 != hb["c1"]) +
+                             np.count_nonzero(got_c2 != hb["c2"]))
+                for got_c, ref_c in ((got_c1, hb["c1"]), (got_c2, hb["c2"])):
+                    assert np.max(np.abs(got_c.astype(np.int32) - ref_c.astype(np.int32)),
+                                  initial=0) <= 1
+    if forced:
+        say(f"{config}: {len(picks)} sampled blocks matched over {steps} teacher-forced steps")
+    else:
+        say(f"{config}: free-running over {steps} steps, {len(picks)} blocks: codes differing "
+            f"{flips}, worst param excess over the accumulated bound {worst_free:.3g} |w|")
+    return worst_free, flips
 
 
 @pytest.mark.parametrize("path", ["call", "plan"])
@@ -120,3 +161,8 @@ def test_gpt2_medium_adamw_sampled(path):
 def test_lm_1p5b_adam_sampled(path):
     """The bench workload; "plan" is the launch configuration bench.py times."""
     run_sampled("c5", "adam", steps=3, nrandom=512, path=path)
+
+
+def test_gpt2_medium_adamw_free_running_report():
+    """Free-running drift, reported (codes stay within one index)."""
+    run_sampled("c4", "adamw", steps=3, nrandom=256, path="plan", forced=False)

@@ -221,3 +221,42 @@ def test_chunked_quantiles_converge_and_scale():
     np.testing.assert_array_equal(oracle.chunked_quantile_codebook(x * np.float32(4.0)), q)
     z = oracle.chunked_quantile_codebook(np.zeros(5000, np.float32))
     assert z[0] == 0.0 and np.all(np.diff(z) > 0) and z[-1] < 1e-42
+
+
+def _exact_chunked_map(x, chunk=4096):
+    """App. G's estimate with exact rationals: per chunk a numpy sort and the
+    sample quantiles sorted_c[floor(i L_c / 257)], their length-weighted
+    average, Eq. 5's midpoints and the division by the largest magnitude, all
+    as Fractions; one rounding to fp32 at the end (through double)."""
+    from fractions import Fraction
+    n = x.size
+    S = [Fraction(0)] * 257
+    for c0 in range(0, n, chunk):
+        s = np.sort(x[c0:c0 + chunk].astype(np.float64))
+        L = s.size
+        for i in range(257):
+            S[i] += L * Fraction(float(s[i * L // 257]))
+    Q = [v / n for v in S]
+    q = [(Q[i] + Q[i + 1]) / 2 for i in range(256)]
+    amax = max(abs(v) for v in q)
+    return np.array([float(v / amax) for v in q], np.float64).astype(np.float32)
+
+
+def test_chunked_quantiles_equal_exact_weighted_average():
+    """The double sums of the oracle equal App. G's average computed exactly,
+    within one fp32 ulp (the oracle rounds its double sums; the exact form
+    rounds once): a ragged last chunk, weighted by its length."""
+    x = workloads.student_t_host(5 * 4096 + 1234, seed=11)
+    q = oracle.chunked_quantile_codebook(x)
+    ref = _exact_chunked_map(x)
+    ulp = np.spacing(np.abs(ref))
+    assert np.all(np.abs(q.astype(np.float64) - ref) <= ulp), \
+        np.max(np.abs(q.astype(np.float64) - ref) / ulp)
+    # an unweighted mean of the chunk quantiles is a different estimate here
+    # (the short last chunk would count as much as a full one)
+    sorted_chunks = [np.sort(x[c0:c0 + 4096]) for c0 in range(0, x.size, 4096)]
+    unweighted = np.mean([[s[i * s.size // 257] for i in range(257)] for s in sorted_chunks],
+                         axis=0)
+    mid = (unweighted[:-1] + unweighted[1:]) / 2
+    alt = (mid / np.max(np.abs(mid))).astype(np.float32)
+    assert np.max(np.abs(alt.astype(np.float64) - ref) / ulp) > 4
