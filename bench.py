@@ -353,7 +353,7 @@ def run_list(args, torch, bq, workloads):
 
     stream = torch.cuda.current_stream()
     q2 = qu_d if nstates == 2 else None
-    if args.path == "call" and opt_name in ("lamb", "lars"):
+    if args.path in ("call", "static") and opt_name in ("lamb", "lars"):
         print("LAMB and LARS run through step plans only (--path plan or optim)",
               file=sys.stderr)
         sys.exit(2)
@@ -423,6 +423,12 @@ def run_list(args, torch, bq, workloads):
 
         def step(i):
             plans[i % 2].run_device(hp_dev, prepared, advance=True, stream=stream)
+    elif args.path == "static":
+        arrays = [(bq.make_tensor_array(r), len(r)) for r in rows]
+
+        def step(i):
+            bq.bq_optimizer8bit_step_static(opt, B, gdt, arrays[i % 2], dict(hp, step=i + 1),
+                                            q1, q2, stream=stream)
     else:
         arrays = [(bq.make_tensor_array(r), len(r)) for r in rows]
 
@@ -444,8 +450,10 @@ def run_list(args, torch, bq, workloads):
         {"workload": f"{desc}, blocksize {B}", "tensors": len(specs), "params": nparams,
          "blocksize": B, "grad_dtype": gname,
          "state_dtype": "u8", "path": args.path})
-    kname = (f"step_oneshot_kernel<{tag}, {gname} grad, {B}>"
-             if args.path != "call" else f"step_kernel<{tag}> (persistent, call path)")
+    kname = {"call": f"step_persistent_kernel<{tag}, {gname} grad, {B}> (call path)",
+             "static": f"step_static_kernel<{tag}, {gname} grad, {B}> (+ prepare_kernel and "
+                       f"{-(-len(specs) // 56)} descriptor uploads)"}.get(
+        args.path, f"step_oneshot_kernel<{tag}, {gname} grad, {B}>")
     if opt_name in ("lamb", "lars"):
         kname += " (+ norms_kernel and trust_ratio_kernel: the per-tensor norm pass)"
     if args.path == "optim":
@@ -484,7 +492,7 @@ def run_quant(args, torch, bq, workloads):
     """Standalone quantize or dequantize of 67,108,864 Student-t(3) x 1e-2
     values; four input / output buffer sets rotate so that no call finds its
     operands in the 256 MB last-level cache."""
-    if args.path in ("optim", "optim-graph", "prepared", "device"):
+    if args.path in ("optim", "optim-graph", "prepared", "device", "static"):
         print(f"--path {args.path} applies to the optimizer-step workloads (the quantize plan "
               "path already reads a codebook prepared once)", file=sys.stderr)
         sys.exit(2)
@@ -586,7 +594,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=16)
-    ap.add_argument("--path", choices=["plan", "prepared", "device", "call", "optim",
+    ap.add_argument("--path", choices=["plan", "prepared", "device", "call", "static", "optim",
                                        "optim-graph"],
                     default="plan",
                     help="plan: bq_step_plan_run (a prepare launch from the raw maps, then one "
@@ -595,7 +603,9 @@ def main():
                          "before the timed steps); device: bq_step_plan_run_device (as prepared, "
                          "the hyperparameters read and the step advanced in device memory); "
                          "call: bq_optimizer8bit_step "
-                         "(descriptor chunks of 56 tensors) or bq_quantize_blockwise; optim: "
+                         "(descriptor chunks of 56 tensors) or bq_quantize_blockwise; static: "
+                         "bq_optimizer8bit_step_static (no allocation: tables and descriptors "
+                         "in the library's static device array, one step launch); optim: "
                          "the drop-in torch optimizer (Adam8bit / AdamW8bit / SGD8bit) with "
                          "the grads of the ring assigned to .grad before each step; "
                          "optim-graph: the same optimizer built with capturable=True, its step() "

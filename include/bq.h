@@ -239,6 +239,30 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
                                 const bq_hparams *hp, const float *qmap1,
                                 const float *qmap2, hipStream_t stream);
 
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): bq_optimizer8bit_step with
+ * the same arguments, checks and results bit for bit as a step plan run
+ * (bq_step_plan_run) over the same list, without a plan.  The maps' decision
+ * tables and the list's descriptors go to a static device array of
+ * BQ_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on until
+ * the process ends; then one launch runs every tile of every tensor.
+ * Launches: one prepare, ceil(count / 56) descriptor uploads (count = the
+ * non-empty tensors, at most BQ_STATIC_MAX_TENSORS), one step.  Allocates
+ * nothing and calls no allocating routine.  Every call on one GPU shares that
+ * GPU's array: calls that overlap on one GPU (different streams, or different
+ * host threads) race and must be ordered by the caller.
+ * Errors: as bq_optimizer8bit_step, and BQ_ERR_SIZE for more than
+ * BQ_STATIC_MAX_TENSORS non-empty tensors or more than 8,388,607 tiles of
+ * 4096 elements in total.
+ */
+#define BQ_STATIC_MAX_TENSORS 4096
+#define BQ_STATIC_SCRATCH_BYTES 279808
+bq_status bq_optimizer8bit_step_static(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                                       const bq_tensor *tensors, int32_t ntensors,
+                                       const bq_hparams *hp, const float *qmap1,
+                                       const float *qmap2, hipStream_t stream);
+
 /* One tensor with 32-bit states; all pointers are device pointers. */
 typedef struct bq_tensor32 {
     float *param;       /* numel fp32, updated in place */

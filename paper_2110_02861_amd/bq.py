@@ -31,7 +31,8 @@ OPTIMIZERS = {"adam": BQ_ADAM, "adamw": BQ_ADAMW, "momentum": BQ_MOMENTUM,
 EXPORTS = ("bq_make_dynamic_codebook", "bq_make_codebook", "bq_make_quantile_codebook",
            "bq_estimate_quantile_codebook", "bq_quantile_workspace_bytes",
            "bq_quantize_blockwise", "bq_dequantize_blockwise",
-           "bq_optimizer8bit_step", "bq_optimizer32bit_step", "bq_prepare_codebook",
+           "bq_optimizer8bit_step", "bq_optimizer8bit_step_static", "bq_optimizer32bit_step",
+           "bq_prepare_codebook",
            "bq_quantize_blockwise_prepared",
            "bq_step_plan_create", "bq_step_plan_run", "bq_step_plan_run_prepared",
            "bq_step_plan_run_device", "bq_step_plan_destroy", "bq_status_string")
@@ -92,6 +93,8 @@ def lib() -> ctypes.CDLL:
         L.bq_dequantize_blockwise.restype = I
         L.bq_optimizer8bit_step.argtypes = [I, I32, I, P, I32, P, P, P, P]
         L.bq_optimizer8bit_step.restype = I
+        L.bq_optimizer8bit_step_static.argtypes = [I, I32, I, P, I32, P, P, P, P]
+        L.bq_optimizer8bit_step_static.restype = I
         L.bq_optimizer32bit_step.argtypes = [I, I, P, I32, P, P]
         L.bq_optimizer32bit_step.restype = I
         L.bq_prepare_codebook.argtypes = [P, P, P]
@@ -306,6 +309,24 @@ def bq_optimizer8bit_step(opt, blocksize: int, grad_dtype: int, tensors, hp: dic
                                        None if qmap2 is None else _map_ptr(qmap2, "qmap2"),
                                        _stream(stream)),
            "bq_optimizer8bit_step")
+
+
+def bq_optimizer8bit_step_static(opt, blocksize: int, grad_dtype: int, tensors, hp: dict,
+                                 qmap1, qmap2=None, stream=None):
+    """bq_optimizer8bit_step through the library's static device array (no
+    allocation; calls on one GPU must not overlap)."""
+    if isinstance(opt, str):
+        opt = OPTIMIZERS[opt]
+    if isinstance(tensors, tuple) and len(tensors) == 2 and isinstance(tensors[1], int):
+        arr, count = tensors  # prebuilt by the caller, who vouches for the sizes
+    else:
+        check_step_tensors(opt, blocksize, grad_dtype, tensors)
+        arr, count = make_tensor_array(tensors), len(tensors)
+    h = _hparams(hp)
+    _check(lib().bq_optimizer8bit_step_static(
+        int(opt), int(blocksize), int(grad_dtype), arr, count, ctypes.byref(h),
+        _map_ptr(qmap1, "qmap1"), None if qmap2 is None else _map_ptr(qmap2, "qmap2"),
+        _stream(stream)), "bq_optimizer8bit_step_static")
 
 
 def make_tensor32_array(tensors):

@@ -199,10 +199,14 @@ bq_status bq_dequantize_blockwise(const float *qmap, const uint8_t *codes, const
     return from_hip(bq::launch_dequantize(qmap, codes, absmax, n, blocksize, out, stream));
 }
 
-bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
-                                const bq_tensor *tensors, int32_t ntensors,
-                                const bq_hparams *hp, const float *qmap1, const float *qmap2,
-                                hipStream_t stream)
+}  // extern "C"
+
+namespace {
+
+// Checks of the two allocation-free step calls (no HIP call).
+bq_status check_step_call(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                          const bq_tensor *tensors, int32_t ntensors, const bq_hparams *hp,
+                          const float *qmap1, const float *qmap2)
 {
     if (!valid_opt(opt))
         return BQ_ERR_ENUM;
@@ -223,9 +227,23 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
         return BQ_ERR_ARG;
     if (!aligned(qmap1, 4) || (two && !aligned(qmap2, 4)))
         return BQ_ERR_ALIGN;
-    const bq_status st = check_tensors(tensors, ntensors, blocksize, two);
-    if (st != BQ_OK)
+    return check_tensors(tensors, ntensors, blocksize, two);
+}
+
+}  // namespace
+
+extern "C" {
+
+bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                                const bq_tensor *tensors, int32_t ntensors,
+                                const bq_hparams *hp, const float *qmap1, const float *qmap2,
+                                hipStream_t stream)
+{
+    const bq_status st =
+        check_step_call(opt, blocksize, grad_dtype, tensors, ntensors, hp, qmap1, qmap2);
+    if (st != BQ_OK || ntensors == 0)
         return st;
+    const bool two = two_states(opt);
 
     bq::StepArgs args;
     std::memset(&args, 0, sizeof(args));
@@ -261,6 +279,83 @@ bq_status bq_optimizer8bit_step(bq_optimizer opt, int32_t blocksize, bq_dtype gr
             return BQ_ERR_HIP;
     }
     return BQ_OK;
+}
+
+bq_status bq_optimizer8bit_step_static(bq_optimizer opt, int32_t blocksize, bq_dtype grad_dtype,
+                                       const bq_tensor *tensors, int32_t ntensors,
+                                       const bq_hparams *hp, const float *qmap1,
+                                       const float *qmap2, hipStream_t stream)
+{
+    const bq_status st =
+        check_step_call(opt, blocksize, grad_dtype, tensors, ntensors, hp, qmap1, qmap2);
+    if (st != BQ_OK || ntensors == 0)
+        return st;
+    const bool two = two_states(opt);
+    const int64_t tile = bq::step_tile(blocksize);
+    int64_t total = 0;
+    int32_t nonempty = 0;
+    for (int32_t i = 0; i < ntensors; ++i) {
+        if (tensors[i].numel == 0)
+            continue;
+        total += (tensors[i].numel + tile - 1) / tile;
+        if (++nonempty > bq::kStaticMaxTensors || total > kMaxOneShotTiles)
+            return BQ_ERR_SIZE;
+    }
+    if (nonempty == 0)
+        return BQ_OK;
+
+    uint8_t *scratch = nullptr;
+    hipError_t e = bq::static_scratch(&scratch);
+    if (e == hipSuccess)
+        e = bq::launch_prepare(qmap1, two ? qmap2 : nullptr, scratch + bq::kStaticOffTables,
+                               stream);
+    // descriptors of the non-empty tensors, in list order, kMaxDescPerLaunch
+    // per upload launch
+    bq::StaticUploadArgs up;
+    std::memset(&up, 0, sizeof(up));
+    up.scratch = scratch;
+    int64_t tiles = 0;
+    int32_t stored = 0;
+    for (int32_t i = 0; i < ntensors && e == hipSuccess; ++i) {
+        const bq_tensor &t = tensors[i];
+        if (t.numel == 0)
+            continue;
+        up.d[up.count++] = make_desc(t, two, tiles);
+        tiles += (t.numel + tile - 1) / tile;
+        if (up.count == bq::kMaxDescPerLaunch || stored + up.count == nonempty) {
+            up.first = stored;
+            e = bq::launch_static_upload(up, stream);
+            stored += up.count;
+            up.count = 0;
+        }
+    }
+    if (e == hipSuccess) {
+        bq::StaticArgs a;
+        std::memset(&a, 0, sizeof(a));
+        a.tables = scratch + bq::kStaticOffTables;
+        a.scratch = scratch;
+        a.sc = make_scalars(*hp, opt);
+        a.use_wd = bq::l2_on_grad(hp->weight_decay, static_cast<int>(opt));
+        a.ntensors = nonempty;
+        a.total_tiles = static_cast<int32_t>(total);
+        // first tile of every stride-th non-empty tensor
+        a.stride = (nonempty + bq::kStaticArgTiles - 1) / bq::kStaticArgTiles;
+        a.nfirst = (nonempty + a.stride - 1) / a.stride;
+        int64_t first = 0;
+        int32_t k = 0;
+        for (int32_t i = 0; i < ntensors; ++i) {
+            const bq_tensor &t = tensors[i];
+            if (t.numel == 0)
+                continue;
+            if (k % a.stride == 0)
+                a.first_tile[k / a.stride] = static_cast<int32_t>(first);
+            first += (t.numel + tile - 1) / tile;
+            ++k;
+        }
+        e = bq::launch_step_static(static_cast<int>(opt), static_cast<int>(grad_dtype), blocksize,
+                                   a, stream);
+    }
+    return from_hip(e);
 }
 
 bq_status bq_optimizer32bit_step(bq_optimizer opt, bq_dtype grad_dtype,

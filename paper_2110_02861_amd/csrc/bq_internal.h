@@ -6,6 +6,8 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include "bq.h"
+
 namespace bq {
 
 // Per-step fp32 scalars, each formed in double and rounded once (make_scalars
@@ -150,6 +152,56 @@ struct State32Args {
     Desc32 d[kMaxDesc32PerLaunch];
 };
 static_assert(sizeof(State32Args) <= 4096, "kernel argument block must stay below 4 KiB");
+
+// Allocation-free step from a static device array (bq_optimizer8bit_step_static):
+// the two prepared maps, then the descriptors of up to kStaticMaxTensors
+// non-empty tensors (tile_begin counted in step tiles over the whole list).
+constexpr int kStaticMaxTensors = 4096;
+constexpr int64_t kStaticOffTables = 0;
+constexpr int64_t kStaticOffDesc = 17664;  // 2 * kPreparedBytes, rounded up to 256
+constexpr int64_t kStaticScratchBytes = kStaticOffDesc + kStaticMaxTensors * 64;
+static_assert(2 * kPreparedBytes <= kStaticOffDesc, "static scratch layout");
+static_assert(kStaticScratchBytes == BQ_STATIC_SCRATCH_BYTES &&
+                  kStaticMaxTensors == BQ_STATIC_MAX_TENSORS, "bq.h limits");
+
+// One launch of the descriptor upload: count descriptors (kernel arguments)
+// written to entries [first, first + count) of the static array.
+struct StaticUploadArgs {
+    uint8_t *scratch;
+    int32_t first;
+    int32_t count;
+    TensorDesc d[kMaxDescPerLaunch];
+};
+static_assert(sizeof(StaticUploadArgs) <= 4096, "kernel argument block must stay below 4 KiB");
+
+// Arguments of the static step kernel (one workgroup per tile of the list).
+// The first tile of every stride-th non-empty tensor travels in the arguments
+// (stride = ceil(ntensors / kStaticArgTiles): 1 up to 992 tensors), so a
+// workgroup finds its tensor by a scalar search there, plus, for stride > 1,
+// one ballot over the first tiles of at most stride descriptors.
+constexpr int kStaticArgTiles = 992;
+struct StaticArgs {
+    const uint8_t *tables;   // scratch + kStaticOffTables
+    const uint8_t *scratch;  // the static array (device address)
+    StepScalars sc;
+    int32_t use_wd;
+    int32_t ntensors;
+    int32_t total_tiles;
+    int32_t stride;
+    int32_t nfirst;          // entries of first_tile: ceil(ntensors / stride)
+    int32_t pad;
+    int32_t first_tile[kStaticArgTiles];
+};
+static_assert(sizeof(StaticArgs) <= 4096, "kernel argument block must stay below 4 KiB");
+static_assert((kStaticMaxTensors + kStaticArgTiles - 1) / kStaticArgTiles <= 64,
+              "the fine search covers one wave");
+
+// Device address of the static array on the current device (looked up once
+// per device, then cached).
+hipError_t static_scratch(uint8_t **ptr);
+hipError_t launch_static_upload(const StaticUploadArgs &a, hipStream_t stream);
+hipError_t launch_step_static(int opt, int grad_dtype, int blocksize, const StaticArgs &a,
+                              hipStream_t stream);
 
 // Chunk length of the quantile estimator (values sorted per workgroup in LDS)
 // and chunks per first-level summation group.

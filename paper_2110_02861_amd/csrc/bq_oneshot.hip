@@ -16,6 +16,8 @@
 // maps): every workgroup builds the tables in its own LDS once and then runs
 // the same tile code (StepOS::tile, QuantOS::tile) over a grid-stride list of
 // tiles.
+#include <mutex>
+
 #include "bq.h"
 #include "bq_device.h"
 #include "bq_scalars.h"
@@ -54,6 +56,8 @@ __device__ inline int run_use_wd(const PlanArgs &a)
 }
 __device__ inline StepScalars run_scalars(const StepArgs &a) { return a.sc; }
 __device__ inline int run_use_wd(const StepArgs &a) { return a.use_wd; }
+__device__ inline StepScalars run_scalars(const StaticArgs &a) { return a.sc; }
+__device__ inline int run_use_wd(const StaticArgs &a) { return a.use_wd; }
 
 // ---------------------------------------------------------------------------
 // Scalars of a run from device-resident hyperparameters (one wave)
@@ -613,6 +617,80 @@ __global__ __launch_bounds__(kST) void step_persistent_kernel(const StepArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Fused 8-bit step from a static device array (the allocation-free call for
+// callers that cannot allocate): the maps' tables and the list's descriptors
+// live in `scratch`, and every tile is a one-shot workgroup as in a plan
+// ---------------------------------------------------------------------------
+
+// The array is reached from host code only through the device address that
+// hipGetSymbolAddress returns (static_scratch below); each GPU holds its own.
+static __device__ __attribute__((aligned(256))) uint8_t scratch[kStaticScratchBytes];
+
+// Descriptors of entries [first, first + count) from the kernel arguments.
+__global__ __launch_bounds__(64) void static_upload_kernel(const StaticUploadArgs a)
+{
+    const int i = threadIdx.x;
+    if (i < a.count)
+        reinterpret_cast<TensorDesc *>(a.scratch + kStaticOffDesc)[a.first + i] = a.d[i];
+}
+
+// One workgroup per tile.  Its tensor is the last one whose first tile is at
+// or below the tile index (empty tensors are left out, so first tiles rise
+// strictly): a scalar binary search over the first tiles in the kernel
+// arguments, then, when they hold only every stride-th tensor, one ballot over
+// the next stride descriptors' first tiles; then one scalar load of the
+// descriptor -- the one round trip to memory a plan's tile record also costs.
+template <int OPT, int GRAD, int B>
+__global__ __launch_bounds__(kST) void step_static_kernel(const StaticArgs a)
+{
+    using K = StepOS<OPT, GRAD, B>;
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
+    const int tid = threadIdx.x;
+
+    // decision-table granules first, as in the plan kernel
+    vu4 gran[K::kGPT];
+#pragma unroll
+    for (int k = 0; k < K::kGPT; ++k) {
+        const int gi = min(tid + k * kST, K::kGran - 1);
+        const int src = 16 * gi + (gi >= K::kGran1 ? kPreparedBytes - kPreparedSignedBytes : 0);
+        gran[k] = *G(reinterpret_cast<const vu4 *>(a.tables + src));
+    }
+
+    const int t = blockIdx.x;
+    int k = 0;
+#pragma unroll
+    for (int s = 512; s >= 1; s >>= 1)
+        if (k + s < a.nfirst && a.first_tile[k + s] <= t)
+            k += s;
+    const gptr<const TensorDesc> descs =
+        G(reinterpret_cast<const TensorDesc *>(a.scratch + kStaticOffDesc));
+    int idx = k * a.stride;
+    if (a.stride > 1) {
+        const int lane = tid & 63;
+        const int e = idx + lane;
+        // lane 0's tensor starts at or below t (the search above)
+        const uint64_t m =
+            __ballot(lane < a.stride && e < a.ntensors && descs[e].tile_begin <= t);
+        idx += 63 - __builtin_clzll(m);
+    }
+    idx = __builtin_amdgcn_readfirstlane(idx);
+    const gptr<const TensorDesc> dp = descs + idx;
+    const int64_t t0 = ((int64_t)t - dp->tile_begin) * K::TILE;
+    TensorDesc D;
+    D.param = dp->param + t0;
+    D.grad = static_cast<const char *>(dp->grad) + t0 * (GRAD == kF32 ? 4 : 2);
+    D.s1 = dp->s1 + t0;
+    D.s2 = K::kTwo ? dp->s2 + t0 : nullptr;
+    D.a1 = dp->a1 + t0 / B;
+    D.a2 = K::kTwo ? dp->a2 + t0 / B : nullptr;
+    D.numel = dp->numel - t0;
+    if (K::TILE <= D.numel)
+        K::template tile<true, true, StaticArgs>(a, D, 0, lds, gran, 0.0f);
+    else
+        K::template tile<false, true, StaticArgs>(a, D, 0, lds, gran, 0.0f);
+}
+
+// ---------------------------------------------------------------------------
 // LAMB / LARS: per-tile partial squared norms, then per-tensor lr * ratio
 // ---------------------------------------------------------------------------
 
@@ -1144,6 +1222,37 @@ hipError_t launch_os_g(int grad_dtype, int blocksize, const PlanArgs &a, hipStre
     }
 }
 
+template <int OPT, int GRAD>
+hipError_t launch_static_b(int blocksize, const StaticArgs &a, hipStream_t s)
+{
+    const dim3 grid((unsigned)a.total_tiles), block(kST);
+    switch (blocksize) {
+    case 256: hipLaunchKernelGGL((step_static_kernel<OPT, GRAD, 256>), grid, block, 0, s, a); break;
+    case 512: hipLaunchKernelGGL((step_static_kernel<OPT, GRAD, 512>), grid, block, 0, s, a); break;
+    case 1024:
+        hipLaunchKernelGGL((step_static_kernel<OPT, GRAD, 1024>), grid, block, 0, s, a);
+        break;
+    case 2048:
+        hipLaunchKernelGGL((step_static_kernel<OPT, GRAD, 2048>), grid, block, 0, s, a);
+        break;
+    case 4096:
+        hipLaunchKernelGGL((step_static_kernel<OPT, GRAD, 4096>), grid, block, 0, s, a);
+        break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int OPT>
+hipError_t launch_static_g(int grad_dtype, int blocksize, const StaticArgs &a, hipStream_t s)
+{
+    switch (grad_dtype) {
+    case kF16: return launch_static_b<OPT, kF16>(blocksize, a, s);
+    case kBF16: return launch_static_b<OPT, kBF16>(blocksize, a, s);
+    default: return launch_static_b<OPT, kF32>(blocksize, a, s);
+    }
+}
+
 template <int B>
 hipError_t launch_qr_t(const float *qmap, const float *x, int64_t n, uint8_t *codes,
                        float *absmax, hipStream_t s)
@@ -1254,6 +1363,50 @@ hipError_t launch_step_persistent(int opt, int grad_dtype, int blocksize, const 
     case kAdamW: return launch_persist_g<kAdamW>(grad_dtype, blocksize, a, stream);
     case kMomentum: return launch_persist_g<kMomentum>(grad_dtype, blocksize, a, stream);
     case kAdaGrad: return launch_persist_g<kAdaGrad>(grad_dtype, blocksize, a, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t static_scratch(uint8_t **ptr)
+{
+    // one device address per device, looked up with that device current
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static uint8_t *addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        if (!p)
+            return hipErrorInvalidSymbol;
+        addr[dev] = static_cast<uint8_t *>(p);
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_static_upload(const StaticUploadArgs &a, hipStream_t stream)
+{
+    hipLaunchKernelGGL(static_upload_kernel, dim3(1), dim3(64), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_step_static(int opt, int grad_dtype, int blocksize, const StaticArgs &a,
+                              hipStream_t stream)
+{
+    switch (opt) {
+    case kAdam: return launch_static_g<kAdam>(grad_dtype, blocksize, a, stream);
+    case kAdamW: return launch_static_g<kAdamW>(grad_dtype, blocksize, a, stream);
+    case kMomentum: return launch_static_g<kMomentum>(grad_dtype, blocksize, a, stream);
+    case kAdaGrad: return launch_static_g<kAdaGrad>(grad_dtype, blocksize, a, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -102,8 +102,9 @@ def _good_row(n=100, two=True):
                 absmax2=A16 if two else None, numel=n)
 
 
-def test_step_argument_checks(L):
-    s = L.bq_optimizer8bit_step
+@pytest.mark.parametrize("name", ["bq_optimizer8bit_step", "bq_optimizer8bit_step_static"])
+def test_step_argument_checks(L, name):
+    s = getattr(L, name)
     hp = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 1)
     hp0 = bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 0)
     good = _tensors(_good_row())
@@ -138,6 +139,17 @@ def test_step_argument_checks(L):
     assert s(0, 2048, 0, None, 0, None, None, None, None) == bq.BQ_OK
     empty = _tensors(dict(numel=0))
     assert s(0, 2048, 0, empty, 1, H, A16, A16, None) == bq.BQ_OK
+
+
+def test_static_step_limits(L):
+    """More non-empty tensors than the static array holds, or more tiles than
+    one launch covers, are refused before any HIP call."""
+    s = L.bq_optimizer8bit_step_static
+    H = ctypes.byref(bq.bq_hparams(1e-3, 0.9, 0.995, 1e-8, 0.0, 1))
+    many = _tensors(*[_good_row(10) for _ in range(4097)])
+    assert s(0, 2048, 1, many, 4097, H, A16, A16, None) == bq.BQ_ERR_SIZE
+    huge = _tensors(*[_good_row(1 << 34) for _ in range(3)])  # 3 * 2^22 tiles > 8,388,607
+    assert s(0, 2048, 1, huge, 3, H, A16, A16, None) == bq.BQ_ERR_SIZE
 
 
 def test_momentum_does_not_need_second_state(L):
