@@ -38,7 +38,8 @@ METRIC = "8-bit Adam step params/sec and achieved HBM GB/s (% of peak), 1.5B-par
 HBM_PEAK_GBS = 8000.0
 BLOCKSIZE = 2048
 
-# HBM traffic of one launch of the dominant kernel, from two rocprofv3 --pmc
+# HBM traffic of the dominant kernel per step (summed over its launches in one
+# step: 11 for the call path on the 1.5B list, else 1), from two rocprofv3 --pmc
 # runs of the bench command (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch),
 # FETCH_SIZE scaled by 2.0 and WRITE_SIZE by 1.0: the factors that make the
 # counters of kernels of known traffic (a plain fp32->fp16 copy, the
@@ -46,12 +47,20 @@ BLOCKSIZE = 2048
 # kernel sources the counters were taken on (sha256 below); otherwise the
 # bench reports traffic null.  Keys: (workload, blocksize, path).
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h", "bq_scalars.h"]
-TRAFFIC_SOURCES_SHA256 = "1ef25aa5acf915a9ecf1492ad1dcfafe7cbca3408fa2bb3d4142b2574d253fcb"
+TRAFFIC_SOURCES_SHA256 = "84f6b0fec646d604f22eabe2654f94399afa37940ac756f4d0727c7aa3d229f4"
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132447.781, "write_kib": 9150412.367},
-    ("quantize", 2048, "plan"): {"fetch_kib": 131136.489, "write_kib": 65792.0},
-    ("dequantize", 2048, "call"): {"fetch_kib": 33815.685, "write_kib": 262170.998},
+    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132451.375, "write_kib": 9150411.648},
+    ("lm1p5b-adam", 2048, "static"): {"fetch_kib": 6108645.500, "write_kib": 9150411.625},
+    # 11 launches per step: the mean per dispatch times 11
+    ("lm1p5b-adam", 2048, "call"): {"fetch_kib": 11 * 555518.016, "write_kib": 11 * 831860.055},
+    ("gpt2m-adamw", 2048, "plan"): {"fetch_kib": 1397108.734, "write_kib": 2084464.125},
+    # the plan and prepared paths run the same step kernel on the same list
+    ("resnet50-momentum", 2048, "prepared"): {"fetch_kib": 113027.094, "write_kib": 124988.211},
+    ("resnet50-momentum", 2048, "plan"): {"fetch_kib": 113027.094, "write_kib": 124988.211},
+    ("quantize", 2048, "plan"): {"fetch_kib": 131141.912, "write_kib": 65792.0},
+    ("quantize", 2048, "call"): {"fetch_kib": 131144.000, "write_kib": 65792.0},
+    ("dequantize", 2048, "call"): {"fetch_kib": 33808.756, "write_kib": 262169.973},
 }
 
 

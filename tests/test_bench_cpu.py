@@ -34,10 +34,19 @@ def test_recorded_counter_traffic_matches_the_byte_model():
     """The FETCH / WRITE counters recorded for each dominant kernel read within
     2 % of its algorithmic bytes (every byte moved once)."""
     c5 = [s.numel for s in workloads.lm_1p5b_specs()]
+    c4 = [s.numel for s in workloads.SPECS["c4"]()]
+    c3 = [s.numel for s in workloads.SPECS["c3"]()]
+    quant = bench.QUANT_N * 5 + bench.QUANT_N // 2048 * 4
     algorithmic = {
         ("lm1p5b-adam", 2048, "plan"): bench.step_bytes(c5, 2048, 2, 2),
-        ("quantize", 2048, "plan"): bench.QUANT_N * 5 + bench.QUANT_N // 2048 * 4,
-        ("dequantize", 2048, "call"): bench.QUANT_N * 5 + bench.QUANT_N // 2048 * 4,
+        ("lm1p5b-adam", 2048, "static"): bench.step_bytes(c5, 2048, 2, 2),
+        ("lm1p5b-adam", 2048, "call"): bench.step_bytes(c5, 2048, 2, 2),
+        ("gpt2m-adamw", 2048, "plan"): bench.step_bytes(c4, 2048, 2, 2),
+        ("resnet50-momentum", 2048, "prepared"): bench.step_bytes(c3, 2048, 4, 1),
+        ("resnet50-momentum", 2048, "plan"): bench.step_bytes(c3, 2048, 4, 1),
+        ("quantize", 2048, "plan"): quant,
+        ("quantize", 2048, "call"): quant,
+        ("dequantize", 2048, "call"): quant,
     }
     assert set(algorithmic) == set(bench.MEASURED_TRAFFIC)
     for key, m in bench.MEASURED_TRAFFIC.items():
