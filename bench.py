@@ -182,6 +182,18 @@ def setup_c5(torch, bq, workloads, seed=0):
     return setup_list(torch, bq, workloads, "c5", 2, BLOCKSIZE, seed)
 
 
+def cpu_model():
+    """The host CPU's model name (first processor in /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(specs, params, grads, layers, steps=6):
     """Time the oracle on the first `layers` transformer layers of the list
     (initial params, the first grad buffer, zero state): one warm-up step and
@@ -216,6 +228,7 @@ def cpu_baseline(specs, params, grads, layers, steps=6):
     dt = time.perf_counter() - t0
     return {
         "value": steps * n_sample / dt, "unit": "params/s", "cores": cores, "kind": "oracle",
+        "cpu_model": cpu_model(), "per_core": steps * n_sample / dt / cores,
         "sample": f"first {layers} transformer layers of the 1.5B list ({len(idx)} tensors, "
                   f"{n_sample} params), zero state, 1 warm-up + {steps} timed steps, "
                   f"OpenMP over blocks",
@@ -266,6 +279,72 @@ for _opt, _hp, _norms in (
         ("lars", dict(lr=0.1, beta1=0.9, beta2=0.0, eps=0.0, wd=1e-4, trust=1e-3), (4, 0))):
     LIST_WORKLOADS["paper1b-" + _opt] = dict(config="p1b", opt=_opt, hp=_hp, norms=_norms,
                                              desc=f"8-bit {_opt}, " + _P1B)
+
+
+def run_cpu_oracle(args):
+    """The oracle on one host thread: C1 (8-bit Adam, one 1,048,576-element
+    tensor, 10 steps from the zero state), C2 (block-wise quantize and
+    dequantize of 67,108,864 Student-t values, B = 2048) and C3 (8-bit Momentum
+    on the ResNet-50 list, 2 steps), all inputs from the host generators.  A
+    per-core reference for the GPU figures; no GPU is used."""
+    import oracle
+    from paper_2110_02861_amd import workloads
+    qs, qu = oracle.dynamic_codebook(0), oracle.dynamic_codebook(1)
+    B = BLOCKSIZE
+
+    def run_steps(config, opt, steps):
+        specs = workloads.SPECS[config]()
+        hp = getattr(workloads, config.upper())
+        two = opt in (oracle.ADAM, oracle.ADAMW)
+        st = []
+        for i, sp in enumerate(specs):
+            w = workloads.init_param_host(sp, workloads.host_rng(0, config, i, 0))
+            nb = (sp.numel + B - 1) // B
+            st.append([w, np.full(sp.numel, 127, np.uint8), np.zeros(nb, np.float32),
+                       np.zeros(sp.numel, np.uint8) if two else None,
+                       np.zeros(nb, np.float32) if two else None])
+        grads = [[workloads.grad_host(config, sp, workloads.host_rng(0, config, i, t))
+                  for i, sp in enumerate(specs)] for t in range(1, steps + 1)]
+        t0 = time.perf_counter()
+        for t in range(1, steps + 1):
+            for (w, c1, a1, c2, a2), g in zip(st, grads[t - 1]):
+                oracle.step8(opt, B, w, g, c1, a1, qs, c2, a2, qu, hp["lr"], hp["beta1"],
+                             hp["beta2"], hp["eps"], hp["wd"], t, nthreads=1)
+        dt = time.perf_counter() - t0
+        n = sum(sp.numel for sp in specs)
+        return n, steps, dt, [sp.numel for sp in specs]
+
+    log("C1 on one thread")
+    n1, k1, d1, e1 = run_steps("c1", oracle.ADAM, 10)
+    log("C3 on one thread")
+    n3, k3, d3, e3 = run_steps("c3", oracle.MOMENTUM, 2)
+    log("C2 on one thread")
+    x = workloads.student_t_host(QUANT_N, seed=0)
+    t0 = time.perf_counter()
+    codes, absmax = oracle.quantize_blockwise(qs, x, B, nthreads=1)
+    dq = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.dequantize_blockwise(qs, codes, absmax, B, nthreads=1)
+    dd = time.perf_counter() - t0
+    qbytes = QUANT_N * 5 + (QUANT_N + B - 1) // B * 4
+    c1 = {"params_per_s": n1 * k1 / d1, "gbs": k1 * step_bytes(e1, B, 2, 2) / d1 / 1e9,
+          "seconds": d1, "steps": k1}
+    c3 = {"params_per_s": n3 * k3 / d3, "gbs": k3 * step_bytes(e3, B, 4, 1) / d3 / 1e9,
+          "seconds": d3, "steps": k3}
+    c2 = {"quantize_elements_per_s": QUANT_N / dq, "quantize_gbs": qbytes / dq / 1e9,
+          "dequantize_elements_per_s": QUANT_N / dd, "dequantize_gbs": qbytes / dd / 1e9,
+          "seconds": dq + dd}
+    return {
+        "metric": "oracle (plain C, one host thread) 8-bit Adam step params/sec on C1",
+        "value": c1["params_per_s"], "unit": "params/s", "n_gpus": 0, "steps": k1, "warmup": 0,
+        "ms_per_step": d1 / k1 * 1e3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded numpy PCG64 on the host)",
+        "config": {"workload": "the CPU oracle on one thread: C1 (8-bit Adam, 1,048,576 params, "
+                               "10 steps), C2 (quantize + dequantize, 67,108,864 Student-t "
+                               "values, B 2048), C3 (8-bit Momentum, ResNet-50 list, 2 steps)",
+                   "threads": 1, "cpu_model": cpu_model()},
+        "c1_adam": c1, "c2_quantize": c2, "c3_momentum": c3,
+    }
 
 
 def workload_bytes(name, numels, blocksize, grad_bytes):
@@ -598,7 +677,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="lm1p5b-adam",
-                    choices=list(LIST_WORKLOADS) + ["quantize", "dequantize"])
+                    choices=list(LIST_WORKLOADS) + ["quantize", "dequantize", "cpu-oracle"])
     ap.add_argument("--blocksize", type=int, default=BLOCKSIZE)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true")
@@ -624,6 +703,10 @@ def main():
         print("bench.py measures one GPU only: the 8-bit step has no cross-GPU exchange, and "
               "the library runs on a single MI355X (use --gpus 1)", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "cpu-oracle":
+        print(json.dumps(run_cpu_oracle(args)), flush=True)
+        return
 
     import torch
     from paper_2110_02861_amd import bq, workloads

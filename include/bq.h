@@ -50,7 +50,11 @@ typedef enum bq_status {
     BQ_ERR_DTYPE = 5,     /* unknown gradient dtype */
     BQ_ERR_ALIGN = 6,     /* a pointer violates the alignment rule above */
     BQ_ERR_HIP = 7,       /* the HIP runtime reported an error at launch */
-    BQ_ERR_ARG = 8        /* a scalar argument is out of range (e.g. step < 1) */
+    BQ_ERR_ARG = 8,       /* a scalar argument is out of range (e.g. step < 1) */
+    /* not values: these two make the type span every int, so a call that
+     * receives any int in it has defined behavior (and rejects it) */
+    BQ_STATUS_RANGE_MIN = -2147483647 - 1,
+    BQ_STATUS_RANGE_MAX = 2147483647
 } bq_status;
 
 typedef enum bq_codebook_kind {
@@ -59,7 +63,11 @@ typedef enum bq_codebook_kind {
     BQ_INVERSE_SIGNED = 2,    /* inverse dynamic map, signed (App. F.1) */
     BQ_INVERSE_UNSIGNED = 3,  /* inverse dynamic map, unsigned (App. F.1) */
     BQ_LINEAR_SIGNED = 4,     /* 256 evenly spaced values in [-1, 1] */
-    BQ_LINEAR_UNSIGNED = 5    /* 256 evenly spaced values in [0, 1] */
+    BQ_LINEAR_UNSIGNED = 5,   /* 256 evenly spaced values in [0, 1] */
+    /* not values: these two make the type span every int, so a call that
+     * receives any int in it has defined behavior (and rejects it) */
+    BQ_CODEBOOK_RANGE_MIN = -2147483647 - 1,
+    BQ_CODEBOOK_RANGE_MAX = 2147483647
 } bq_codebook_kind;
 typedef enum bq_optimizer {
     BQ_ADAM = 0,
@@ -67,13 +75,25 @@ typedef enum bq_optimizer {
     BQ_MOMENTUM = 2,
     BQ_ADAGRAD = 3,
     BQ_LAMB = 4,  /* step plans only */
-    BQ_LARS = 5   /* step plans only */
+    BQ_LARS = 5,  /* step plans only */
+    /* not values: these two make the type span every int, so a call that
+     * receives any int in it has defined behavior (and rejects it) */
+    BQ_OPTIMIZER_RANGE_MIN = -2147483647 - 1,
+    BQ_OPTIMIZER_RANGE_MAX = 2147483647
 } bq_optimizer;
 /* Gradient element types.  Every grad is converted to fp32 exactly before the
  * update (Section 3: the update itself runs in 32 bit); the paper's setups use
  * fp16 (mixed precision) and fp32 grads, bfloat16 is the common mixed-precision
  * type on MI355X. */
-typedef enum bq_dtype { BQ_F32 = 0, BQ_F16 = 1, BQ_BF16 = 2 } bq_dtype;
+typedef enum bq_dtype {
+    BQ_F32 = 0,
+    BQ_F16 = 1,
+    BQ_BF16 = 2,
+    /* not values: these two make the type span every int, so a call that
+     * receives any int in it has defined behavior (and rejects it) */
+    BQ_DTYPE_RANGE_MIN = -2147483647 - 1,
+    BQ_DTYPE_RANGE_MAX = 2147483647
+} bq_dtype;
 
 /*
  * Build a 256-entry dynamic codebook on the host (synchronous, no GPU call).

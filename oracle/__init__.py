@@ -21,21 +21,37 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "bq_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# BQ_SANITIZE=1: the build with AddressSanitizer and UndefinedBehaviorSanitizer
+# (clang, to share the ASan runtime of the sanitized library; no OpenMP)
+SANITIZE = os.environ.get("BQ_SANITIZE") == "1"
+_LIB = os.path.join(_HERE, "liboracle_san.so" if SANITIZE else "liboracle.so")
 
 ADAM, ADAMW, MOMENTUM, ADAGRAD, LAMB, LARS = 0, 1, 2, 3, 4, 5
 TWO_STATES = (0, 1, 4)
 SIGNED, UNSIGNED = 0, 1
 
 
-def build() -> str:
-    """Compile the oracle with gcc (IEEE binary32, no contraction, OpenMP)."""
-    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
-           "-ffp-contract=off", "-fno-fast-math", "-fvisibility=hidden",
-           "-Wall", "-Wextra", "-o", _LIB + ".tmp", _SRC, "-lm"]
+def build(sanitize: bool = None) -> str:
+    """Compile the oracle with gcc (IEEE binary32, no contraction, OpenMP); with
+    sanitize (default: BQ_SANITIZE=1), with clang under AddressSanitizer and
+    UndefinedBehaviorSanitizer, single-threaded, to liboracle_san.so."""
+    if sanitize is None:
+        sanitize = SANITIZE
+    if sanitize:
+        rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+        out = os.path.join(_HERE, "liboracle_san.so")
+        cmd = [os.path.join(rocm, "llvm", "bin", "clang"), "-O1", "-g", "-std=c11", "-fPIC",
+               "-shared", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+               "-fno-omit-frame-pointer", "-ffp-contract=off", "-fno-fast-math",
+               "-fvisibility=hidden", "-Wall", "-Wextra", "-o", out + ".tmp", _SRC, "-lm"]
+    else:
+        out = os.path.join(_HERE, "liboracle.so")
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+               "-ffp-contract=off", "-fno-fast-math", "-fvisibility=hidden",
+               "-Wall", "-Wextra", "-o", out + ".tmp", _SRC, "-lm"]
     subprocess.run(cmd, check=True)
-    os.replace(_LIB + ".tmp", _LIB)
-    return _LIB
+    os.replace(out + ".tmp", out)
+    return out
 
 
 _lib = None

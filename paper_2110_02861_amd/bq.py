@@ -13,7 +13,10 @@ import os
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libbq.so")
+# BQ_SANITIZE=1 selects the host-sanitized build (build.py --sanitize), for the
+# CPU tests under AddressSanitizer / UndefinedBehaviorSanitizer only
+LIB_PATH = (os.path.join(_PKG, "_build", "san", "libbq.so") if os.environ.get("BQ_SANITIZE") == "1"
+            else os.path.join(_PKG, "libbq.so"))
 
 BQ_OK, BQ_ERR_NULL, BQ_ERR_SIZE, BQ_ERR_BLOCKSIZE, BQ_ERR_ENUM = 0, 1, 2, 3, 4
 BQ_ERR_DTYPE, BQ_ERR_ALIGN, BQ_ERR_HIP, BQ_ERR_ARG = 5, 6, 7, 8

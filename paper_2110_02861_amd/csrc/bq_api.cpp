@@ -115,6 +115,7 @@ const char *bq_status_string(bq_status s)
     case BQ_ERR_ALIGN: return "pointer misaligned (elements 16 B, absmax and codebook 4 B)";
     case BQ_ERR_HIP: return "HIP runtime error";
     case BQ_ERR_ARG: return "scalar argument out of range";
+    default: break;
     }
     return "unknown status";
 }

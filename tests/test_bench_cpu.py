@@ -77,3 +77,9 @@ def test_byte_model_of_the_paper_setup():
     assert bench.workload_bytes("paper1b-momentum", p, 2048, 4) == 14 * n + 8 * nb
     assert bench.workload_bytes("paper1b-lamb", p, 2048, 4) == (16 + 10) * n + 24 * nb
     assert bench.workload_bytes("paper1b-lars", p, 2048, 4) == (14 + 8) * n + 8 * nb
+
+
+def test_cpu_model_is_read_from_proc_cpuinfo():
+    m = bench.cpu_model()
+    if os.path.exists("/proc/cpuinfo"):
+        assert isinstance(m, str) and m

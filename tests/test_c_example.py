@@ -9,7 +9,8 @@ import pytest
 
 from tests.gpu_helpers import needs_gpu
 
-EXE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c", "bq_c_example")
+EXE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c",
+                   "bq_c_example_san" if os.environ.get("BQ_SANITIZE") == "1" else "bq_c_example")
 
 
 def _run(*args):
