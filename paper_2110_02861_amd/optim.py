@@ -28,6 +28,18 @@ Every update runs in the HIP kernels of libbq:
 Params must be fp32 CUDA tensors, contiguous and 16-byte aligned; grads fp32,
 fp16 or bf16 of the same shape.  ``state_dict`` / ``load_state_dict`` carry the codes,
 the absmax arrays and the step count of every tensor.
+
+Graphs (``capturable=True``): a captured ``step()`` reads device memory that
+the optimizer owns -- the step plans it ran, the device hyperparameters and
+the state tensors.  The optimizer therefore never frees what a capture used
+on its own: plans used under capture are never evicted, and
+``load_state_dict`` moves them, the device hyperparameters and the replaced
+state tensors to a retired list instead of freeing them.  A graph captured
+before ``load_state_dict`` keeps replaying harmlessly into that retired
+memory (it no longer updates the loaded states): capture again after a load.
+Each capture on new grad storages pins one more plan; once every graph that
+replays this optimizer's step has been dropped, ``release_graph_memory()``
+frees all of it.
 """
 from __future__ import annotations
 
@@ -94,6 +106,10 @@ class Optimizer8bit(torch.optim.Optimizer):
         self._override32: set = set()
         self._plans: dict = {}
         self._pinned: set = set()  # keys of plans used under graph capture: never evicted
+        # plans, device hyperparameters and state tensors that graphs captured
+        # before a load_state_dict may still read: freed by
+        # release_graph_memory() or with the optimizer
+        self._retired: list = []
         self._hp_dev: dict = {}  # (group, grad dtype, device) -> (device hparams, params)
         # group index -> the last two steps' params, grad storages, pointers
         # and launches; a step equal to one of them replays its launches
@@ -395,10 +411,20 @@ class Optimizer8bit(torch.optim.Optimizer):
         return plan
 
     def load_state_dict(self, state_dict):
-        for plan in self._plans.values():
-            plan.close()
+        """Load states; plans are made again.  Plans a captured graph used,
+        the device hyperparameters and (when anything was captured) the
+        replaced state tensors are retired, not freed: graphs captured
+        before the load replay into them and must be captured again."""
+        for key, plan in self._plans.items():
+            if key in self._pinned:
+                self._retired.append(plan)
+            else:
+                plan.close()
+        if self._pinned or self._hp_dev:
+            self._retired.extend(self._hp_dev.values())
+            self._retired.extend(dict(s) for s in self.state.values())
         self._plans = {}
-        self._pinned = set()  # graphs captured before a load must be captured again
+        self._pinned = set()
         self._hp_dev = {}  # made again from the loaded step counts
         self._fast = {}
         super().load_state_dict(state_dict)
@@ -408,6 +434,22 @@ class Optimizer8bit(torch.optim.Optimizer):
             for k in ("state1", "state2"):
                 if k in s:
                     s[k] = s[k].to(torch.uint8)
+
+    def release_graph_memory(self) -> None:
+        """Free every plan pinned by graph capture and everything retired by
+        ``load_state_dict``.  Call only once no captured graph that replays
+        this optimizer's step is left: a replay afterwards would read freed
+        device memory.  Later captures pin plans again."""
+        for key in list(self._pinned):
+            plan = self._plans.pop(key, None)
+            if plan is not None:
+                plan.close()
+        self._pinned = set()
+        for item in self._retired:
+            if hasattr(item, "close"):  # a plan; tensors are dropped with the list
+                item.close()
+        self._retired = []
+        self._fast = {}
 
 
 class Adam8bit(Optimizer8bit):

@@ -69,3 +69,50 @@ def test_hparams_per_group():
     sgd = optim.SGD8bit([a], lr=0.2, momentum=0.5, weight_decay=1e-4)
     assert sgd._hparams(sgd.param_groups[0], 1) == dict(lr=0.2, beta1=0.5, beta2=0.0, eps=0.0,
                                                         wd=1e-4, step=1)
+
+
+class _FakePlan:
+    """Stands in for a step plan: records whether it was closed."""
+
+    def __init__(self):
+        self.closed = False
+
+    def close(self):
+        self.closed = True
+
+
+def test_load_state_dict_retires_plans_a_graph_reads():
+    """Plans used under capture are not freed by load_state_dict (a graph
+    captured before it may still replay them); release_graph_memory() frees
+    them, and frees pinned plans still in the cache."""
+    p = torch.nn.Parameter(torch.zeros(4096))
+    opt = optim.Adam8bit([p], capturable=True)
+    pinned, free, pinned_later = _FakePlan(), _FakePlan(), _FakePlan()
+    opt._plans = {("a",): pinned, ("b",): free}
+    opt._pinned = {("a",)}
+    hp = torch.zeros(48, dtype=torch.uint8)
+    opt._hp_dev = {(0, 1, 0): (hp, [p])}
+    opt.state[p] = {"step": 3, "state1": torch.zeros(4096, dtype=torch.uint8)}
+    old_state1 = opt.state[p]["state1"]
+    sd = torch.optim.Optimizer.state_dict(opt)
+    opt.load_state_dict(sd)
+    assert free.closed and not pinned.closed
+    assert opt._plans == {} and opt._pinned == set() and opt._hp_dev == {}
+    assert pinned in opt._retired
+    assert any(isinstance(r, tuple) and r[0] is hp for r in opt._retired)
+    assert any(isinstance(r, dict) and r.get("state1") is old_state1 for r in opt._retired)
+    # a later capture pins another plan in the cache
+    opt._plans = {("c",): pinned_later}
+    opt._pinned = {("c",)}
+    opt.release_graph_memory()
+    assert pinned.closed and pinned_later.closed
+    assert opt._retired == [] and opt._pinned == set() and opt._plans == {}
+
+
+def test_load_state_dict_without_capture_closes_every_plan():
+    p = torch.nn.Parameter(torch.zeros(4096))
+    opt = optim.Adam8bit([p])
+    a, b = _FakePlan(), _FakePlan()
+    opt._plans = {("a",): a, ("b",): b}
+    opt.load_state_dict(torch.optim.Optimizer.state_dict(opt))
+    assert a.closed and b.closed and opt._retired == []
