@@ -9,7 +9,7 @@ bq_optimizer8bit_step, --path optim the drop-in torch optimizer.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
                     [--workload lm1p5b-adam|gpt2m-adamw|resnet50-momentum|
-                                quantize|dequantize] [--blocksize B]
+                                quantize|dequantize|stream-study] [--blocksize B]
 
 Prints one JSON line.  The CPU baseline is the oracle (plain C, OpenMP over
 blocks) timed on a bounded sample of the same workload on the host cores.
@@ -17,6 +17,9 @@ The other workloads are secondary measurements of the same kernels: the
 8-bit AdamW step on the GPT-2-medium list (fp16 grads), the 8-bit Momentum
 step on the ResNet-50 list (fp32 grads), and standalone block-wise quantize /
 dequantize of 67,108,864 Student-t values over four rotating buffers.
+--workload stream-study times the step's byte mix (and its reads and writes
+alone) under every launch shape, cache policy, tile order and occupancy of
+libbq_stream.so's access-shape study, beside the step itself.
 """
 from __future__ import annotations
 
@@ -142,6 +145,118 @@ def stream_ceiling(torch, nparams, steps=20):
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+STUDY_MODES = {0: "mix", 1: "reads", 2: "writes"}
+
+
+def run_stream_study(args, torch, bq, workloads):
+    """The access-shape study of libbq_stream.so (bq_stream_study): every
+    variant at the hardware's occupancy and at 2, 3 and 4 workgroups per CU,
+    over buffers of the 1.5B list's size, with the fused step itself (plan,
+    maps prepared once) on that list as one more case; `rounds` interleaved
+    rounds of 3 launches per case, median and best GB/s of algorithmic bytes
+    (mix 14 B per element + 16 B per block, reads 8 + 8, writes 6 + 8)."""
+    from paper_2110_02861_amd import build as pkg_build
+    L = ctypes.CDLL(pkg_build.STREAM_LIB)
+    P = ctypes.c_void_p
+    L.bq_stream_study_variants.restype = ctypes.c_int
+    L.bq_stream_study_info.restype = ctypes.c_char_p
+    L.bq_stream_study_info.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
+    L.bq_stream_study.restype = ctypes.c_int
+    L.bq_stream_study.argtypes = [ctypes.c_int, ctypes.POINTER(P), ctypes.POINTER(P),
+                                  ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, P, ctypes.c_int,
+                                  P]
+    log("allocating the lm1p5b-adam list and the study buffers")
+    specs, params, grads, states, rows = setup_c5(torch, bq, workloads)
+    nparams = sum(p.numel() for p in params)
+    n = nparams // 8192 * 8192
+    nb = n // BLOCKSIZE
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(12345)
+
+    def bufs():
+        return [torch.empty(n, dtype=torch.float32, device=dev).normal_(0, 0.02, generator=gen),
+                torch.empty(n, dtype=torch.float16, device=dev).normal_(0, 1e-4, generator=gen),
+                torch.randint(0, 256, (n,), dtype=torch.uint8, device=dev, generator=gen),
+                torch.randint(0, 256, (n,), dtype=torch.uint8, device=dev, generator=gen),
+                torch.rand(nb, device=dev, generator=gen), torch.rand(nb, device=dev, generator=gen)]
+    bi, bo = bufs(), bufs()
+    pin = (P * 6)(*[t.data_ptr() for t in bi])
+    pout = (P * 6)(*[t.data_ptr() for t in bo])
+    table = torch.randint(0, 2**31 - 1, (880 * 4,), dtype=torch.int32, device=dev, generator=gen)
+    stream = torch.cuda.current_stream()
+    mode_bytes = {0: 14 * n + 16 * nb, 1: 8 * n + 8 * nb, 2: 6 * n + 8 * nb}
+    cases = []
+    for v in range(L.bq_stream_study_variants()):
+        info = (ctypes.c_int * 3)()
+        name = L.bq_stream_study_info(v, info).decode()
+        for per_cu in (0, 2, 3, 4):
+            cases.append(dict(v=v, name=name, threads=info[0], chunks=info[1],
+                              mode=STUDY_MODES[info[2]], per_cu=per_cu,
+                              bytes=mode_bytes[info[2]]))
+
+    qs = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_SIGNED)).to(dev)
+    qu = torch.from_numpy(bq.bq_make_dynamic_codebook(bq.BQ_UNSIGNED)).to(dev)
+    prepared = bq.prepare_codebook_pair(qs, qu, stream=stream)
+    plans = [bq.StepPlan(bq.BQ_ADAM, BLOCKSIZE, bq.BQ_F16, r) for r in rows]
+    hp = {k: workloads.C5[k] for k in ("lr", "beta1", "beta2", "eps", "wd")}
+    t = [1]
+    cases.append(dict(v=-1, name="the fused step (plan, maps prepared once), lm1p5b-adam list",
+                      threads=512, chunks=2, mode="step", per_cu=0,
+                      bytes=step_bytes([p.numel() for p in params], BLOCKSIZE, 2, 2)))
+
+    def launch(c):
+        if c["v"] < 0:
+            plans[t[0] % 2].run_prepared(dict(hp, step=t[0]), prepared, stream=stream)
+            t[0] += 1
+            return 0
+        return L.bq_stream_study(c["v"], pin, pout, n, BLOCKSIZE, 0, P(table.data_ptr()),
+                                 c["per_cu"], P(stream.cuda_stream))
+
+    live = []
+    for c in cases:
+        rc = launch(c)
+        if rc == 0:
+            live.append(c)
+        elif rc != -1:
+            raise RuntimeError(f"bq_stream_study variant {c['v']} per_cu {c['per_cu']}: {rc}")
+    torch.cuda.synchronize()
+    log(f"{len(live)} cases, {args.rounds} rounds")
+    times = [[] for _ in live]
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    for r in range(args.rounds):
+        for i, c in enumerate(live):
+            e0.record(stream)
+            for _ in range(3):
+                launch(c)
+            e1.record(stream)
+            e1.synchronize()
+            times[i].append(e0.elapsed_time(e1) / 3)
+        log(f"round {r} done")
+    out = []
+    for c, ts in zip(live, times):
+        ts = sorted(ts)
+        med = ts[len(ts) // 2]
+        out.append(dict(c, ms_median=med, gbs_median=c["bytes"] / med / 1e6,
+                        gbs_best=c["bytes"] / ts[0] / 1e6))
+        log(f"{c['name']:48s} per CU {c['per_cu'] or 'hw'}: {out[-1]['gbs_median']:7.0f} GB/s "
+            f"(best {out[-1]['gbs_best']:7.0f})")
+    mix = [o for o in out if o["mode"] == "mix"]
+    best = max(mix, key=lambda o: o["gbs_median"])
+    step = [o for o in out if o["mode"] == "step"][0]
+    return {"metric": "access-shape study of the fused step's byte mix: algorithmic GB/s per "
+                      "launch shape (median of interleaved rounds)",
+            "value": best["gbs_median"], "unit": "GB/s", "n_gpus": 1, "rounds": args.rounds,
+            "higher_is_better": True, "data": "synthetic (seeded torch Philox on the GPU)",
+            "config": {"workload": f"flat buffers of {n} elements (the 1.5B list's size, "
+                                   f"rounded down to 8192), blocksize {BLOCKSIZE}"},
+            "best_mix": {k: best[k] for k in ("name", "per_cu", "gbs_median", "gbs_best")},
+            "step_gbs_median": step["gbs_median"],
+            "step_frac_of_best_mix": step["gbs_median"] / best["gbs_median"],
+            "peak_gbs": HBM_PEAK_GBS, "cases": out}
 
 
 def setup_list(torch, bq, workloads, config, nstates, blocksize=BLOCKSIZE, seed=0, zero1=127):
@@ -677,7 +792,10 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="lm1p5b-adam",
-                    choices=list(LIST_WORKLOADS) + ["quantize", "dequantize", "cpu-oracle"])
+                    choices=list(LIST_WORKLOADS) + ["quantize", "dequantize", "cpu-oracle",
+                                                    "stream-study"])
+    ap.add_argument("--rounds", type=int, default=5,
+                    help="stream-study: interleaved rounds over all cases")
     ap.add_argument("--blocksize", type=int, default=BLOCKSIZE)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream-ceiling", action="store_true")
@@ -711,7 +829,9 @@ def main():
     import torch
     from paper_2110_02861_amd import bq, workloads
 
-    if args.workload in LIST_WORKLOADS:
+    if args.workload == "stream-study":
+        res = run_stream_study(args, torch, bq, workloads)
+    elif args.workload in LIST_WORKLOADS:
         res = run_list(args, torch, bq, workloads)
     else:
         res = run_quant(args, torch, bq, workloads)
