@@ -280,6 +280,28 @@ __device__ inline T ld_nt(const T *p) { return __builtin_nontemporal_load(G(p));
 template <typename T>
 __device__ inline void st_nt(T *p, T v) { __builtin_nontemporal_store(v, G(p)); }
 
+// Streaming stores at system scope: buffer stores with the sc0, sc1 and nt
+// cache-policy bits, over a wave-uniform range [base, base + bytes) (bytes
+// < 2^32) at a per-lane byte offset.  On MI355X they drain to HBM faster than
+// st_nt's non-temporal stores: dequantize of 67M values 55.2 -> 51.6 us, the
+// fused step on the 1.5B list -0.6 % (A/B in one process).  Word 3 of the
+// descriptor is the raw-buffer format of gfx9-family parts.
+constexpr int kStreamStorePolicy = 1 | 2 | 16;  // sc0 | nt | sc1
+__device__ inline __amdgpu_buffer_rsrc_t stream_range(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes,
+                                             0x00020000);
+}
+__device__ inline void st_stream(__amdgpu_buffer_rsrc_t r, int off, vf4 v)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(vu4, v), r, off, 0,
+                                           kStreamStorePolicy);
+}
+__device__ inline void st_stream(__amdgpu_buffer_rsrc_t r, int off, uint32_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, kStreamStorePolicy);
+}
+
 __device__ inline float half_lo(uint32_t w)
 {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xffffu));

@@ -3,7 +3,7 @@
 //
 // One-shot kernels (step plans, prepared codebooks): one workgroup of 512
 // threads per tile, chunks of 2048 elements with 4 contiguous elements per
-// thread, wave-contiguous non-temporal loads and stores (4096-element tiles
+// thread, wave-contiguous non-temporal loads and streaming stores (4096-element tiles
 // for the step, 8192 for quantize, 4096 for dequantize).  The decision tables
 // of each codebook are built by prepare_kernel into a prepared-codebook buffer
 // (once per call, or once for all steps when the caller keeps the buffer) and
@@ -405,8 +405,8 @@ struct StepOS {
         for (int c = 0; c < C; ++c) {
             const int64_t e = t0 + c * (kST * 4) + tid * 4;
             if (FULL) {
-                st_nt(reinterpret_cast<vf4 *>(D.param + e),
-                      vf4{w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]});
+                st_stream(stream_range(D.param + t0, TILE * 4), (int)(e - t0) * 4,
+                          vf4{w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]});
             } else {
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
@@ -507,13 +507,13 @@ struct StepOS {
         for (int c = 0; c < C; ++c) {
             const int64_t e = t0 + c * (kST * 4) + tid * 4;
             if (FULL) {
-                st_nt(reinterpret_cast<uint32_t *>(D.s1 + e),
-                      c1[4 * c] | (c1[4 * c + 1] << 8) | (c1[4 * c + 2] << 16) |
-                          (c1[4 * c + 3] << 24));
+                st_stream(stream_range(D.s1 + t0, TILE), (int)(e - t0),
+                          c1[4 * c] | (c1[4 * c + 1] << 8) | (c1[4 * c + 2] << 16) |
+                              (c1[4 * c + 3] << 24));
                 if constexpr (kTwo)
-                    st_nt(reinterpret_cast<uint32_t *>(D.s2 + e),
-                          c2[4 * c] | (c2[4 * c + 1] << 8) | (c2[4 * c + 2] << 16) |
-                              (c2[4 * c + 3] << 24));
+                    st_stream(stream_range(D.s2 + t0, TILE), (int)(e - t0),
+                              c2[4 * c] | (c2[4 * c + 1] << 8) | (c2[4 * c + 2] << 16) |
+                                  (c2[4 * c + 3] << 24));
             } else {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -1188,7 +1188,7 @@ __global__ __launch_bounds__(kOS) void dequantize_kernel(const float *__restrict
             const int64_t e = t0 + c * (kOS * 4) + tid * 4;
             const vf4 y = {q[k[c] & 0xffu] * A[c], q[(k[c] >> 8) & 0xffu] * A[c],
                            q[(k[c] >> 16) & 0xffu] * A[c], q[k[c] >> 24] * A[c]};
-            st_nt(reinterpret_cast<vf4 *>(out + e), y);
+            st_stream(stream_range(out + t0, TILE * 4), (int)(e - t0) * 4, y);
         }
     } else {
 #pragma unroll
