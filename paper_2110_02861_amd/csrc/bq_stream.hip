@@ -254,15 +254,16 @@ constexpr int kNT = 2, kSC0 = 1, kSC1 = 16;
 // values from a hash of the element index).  T threads, CH chunks of 4 T
 // elements.  WC / WG: codes / grads 16 B per lane through LDS.  GLB: global
 // non-temporal loads and stores (the step's access); else buffer instructions
-// with load / store policy LP / SP.  ALU: dependent fma per element between
+// with load / store policy LP / SP; GLB 2: global non-temporal loads, buffer
+// stores with policy SP (the step's access).  ALU: dependent fma per element between
 // loads and stores; SLEEP: one s_sleep of that count there.  ORDER 1: params
 // stored first, codes after two barriers (the step's order).
-template <int T, int CH, int MODE, bool WC, bool WG, bool XCD, int LP, int SP, bool GLB, int ALU,
+template <int T, int CH, int MODE, bool WC, bool WG, bool XCD, int LP, int SP, int GLB, int ALU,
           int SLEEP, int ORDER>
 __global__ __launch_bounds__(T) void study_kernel(StudyBufs in, StudyBufs out, int64_t ntiles,
                                                   int lg_block, uint32_t key, const vu4 *table)
 {
-    static_assert(!GLB || (!WC && !WG), "wide accesses use buffer instructions");
+    static_assert(GLB == 0 || (!WC && !WG), "wide accesses use buffer instructions");
     constexpr int kTile = 4 * T * CH;
     constexpr int kGPT = (kGranules + T - 1) / T;
     constexpr int kHalf = kTile / 16;       // 16-byte lanes of one code array
@@ -293,7 +294,7 @@ __global__ __launch_bounds__(T) void study_kernel(StudyBufs in, StudyBufs out, i
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
             const int e = c * 4 * T + tid * 4;
-            if (GLB) {
+            if (GLB != 0) {
                 wv[c] = ld(reinterpret_cast<const vu4 *>(B.w + t0 + e));
                 gv[c] = ld(reinterpret_cast<const vu2 *>(B.g + t0 + e));
                 k1[c] = ld(reinterpret_cast<const uint32_t *>(B.c1 + t0 + e));
@@ -408,7 +409,7 @@ __global__ __launch_bounds__(T) void study_kernel(StudyBufs in, StudyBufs out, i
     for (int c = 0; c < CH; ++c) {
         const int e = c * 4 * T + tid * 4;
         const uint32_t gk = ((gv[c].x ^ gv[c].y) & key) ^ tk;
-        if (GLB)
+        if (GLB == 1)
             st(reinterpret_cast<vu4 *>(B.w + t0 + e), wv[c] ^ gk);
         else
             __builtin_amdgcn_raw_buffer_store_b128(wv[c] ^ gk, rw, e * 4, 0, SP);
@@ -421,7 +422,7 @@ __global__ __launch_bounds__(T) void study_kernel(StudyBufs in, StudyBufs out, i
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
             const int e = c * 4 * T + tid * 4;
-            if (GLB) {
+            if (GLB == 1) {
                 st(reinterpret_cast<uint32_t *>(B.c1 + t0 + e), k1[c] ^ key);
                 st(reinterpret_cast<uint32_t *>(B.c2 + t0 + e), k2[c] ^ key);
             } else {
@@ -464,6 +465,14 @@ struct StudyVariant {
 const StudyVariant kStudy[] = {
     SV(512, 2, 0, false, false, false, kNT, kNT, true, 0, 0, 0, "mix: the step's access (global, nt)"),
     SV(512, 2, 0, false, false, false, kNT, kNT, false, 0, 0, 0, "mix: buffer instructions, nt"),
+    SV(512, 2, 0, false, false, false, kNT, kSC0 | kSC1 | kNT, 2, 0, 0, 0,
+       "mix: global nt loads, stores sc0 sc1 nt (the step's)"),
+    SV(512, 2, 0, false, false, false, kSC0 | kNT, kNT, false, 0, 0, 0, "mix: loads sc0 nt"),
+    SV(512, 2, 0, false, false, false, kSC1 | kNT, kNT, false, 0, 0, 0, "mix: loads sc1 nt"),
+    SV(512, 2, 0, false, false, false, kSC0 | kSC1 | kNT, kNT, false, 0, 0, 0,
+       "mix: loads sc0 sc1 nt"),
+    SV(512, 2, 0, false, false, false, kSC0 | kSC1 | kNT, kSC0 | kSC1 | kNT, false, 0, 0, 0,
+       "mix: loads and stores sc0 sc1 nt"),
     SV(512, 2, 0, false, false, false, kNT, 0, false, 0, 0, 0, "mix: stores default policy"),
     SV(512, 2, 0, false, false, false, kNT, kSC1 | kNT, false, 0, 0, 0, "mix: stores sc1 nt"),
     SV(512, 2, 0, false, false, false, kNT, kSC0 | kSC1 | kNT, false, 0, 0, 0,
@@ -488,6 +497,9 @@ const StudyVariant kStudy[] = {
     SV(512, 2, 1, false, false, false, kNT, kNT, true, 0, 0, 0, "reads: global, nt"),
     SV(512, 2, 1, false, false, false, 0, kNT, false, 0, 0, 0, "reads: default policy"),
     SV(512, 2, 1, false, false, true, kNT, kNT, false, 0, 0, 0, "reads: XCD order"),
+    SV(512, 2, 1, false, false, false, kSC0 | kNT, kNT, false, 0, 0, 0, "reads: sc0 nt"),
+    SV(512, 2, 1, false, false, false, kSC1 | kNT, kNT, false, 0, 0, 0, "reads: sc1 nt"),
+    SV(512, 2, 1, false, false, false, kSC0 | kSC1 | kNT, kNT, false, 0, 0, 0, "reads: sc0 sc1 nt"),
     SV(512, 2, 2, false, false, false, kNT, kNT, true, 0, 0, 0, "writes: global, nt"),
     SV(512, 2, 2, false, false, false, kNT, 0, false, 0, 0, 0, "writes: default policy"),
     SV(512, 2, 2, false, false, false, kNT, kSC1 | kNT, false, 0, 0, 0, "writes: sc1 nt"),
