@@ -50,20 +50,20 @@ BLOCKSIZE = 2048
 # kernel sources the counters were taken on (sha256 below); otherwise the
 # bench reports traffic null.  Keys: (workload, blocksize, path).
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h", "bq_scalars.h"]
-TRAFFIC_SOURCES_SHA256 = "84f6b0fec646d604f22eabe2654f94399afa37940ac756f4d0727c7aa3d229f4"
+TRAFFIC_SOURCES_SHA256 = "8fa6f3e06a8d51817be118c736b0bad0a08fbd1acca8fcb435dea8fd6822aea0"
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132451.375, "write_kib": 9150411.648},
-    ("lm1p5b-adam", 2048, "static"): {"fetch_kib": 6108645.500, "write_kib": 9150411.625},
+    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6133023.000, "write_kib": 9150410.375},
+    ("lm1p5b-adam", 2048, "static"): {"fetch_kib": 6109145.781, "write_kib": 9150410.492},
     # 11 launches per step: the mean per dispatch times 11
-    ("lm1p5b-adam", 2048, "call"): {"fetch_kib": 11 * 555518.016, "write_kib": 11 * 831860.055},
-    ("gpt2m-adamw", 2048, "plan"): {"fetch_kib": 1397108.734, "write_kib": 2084464.125},
+    ("lm1p5b-adam", 2048, "call"): {"fetch_kib": 11 * 555789.783, "write_kib": 11 * 831893.744},
+    ("gpt2m-adamw", 2048, "plan"): {"fetch_kib": 1397266.750, "write_kib": 2084463.672},
     # the plan and prepared paths run the same step kernel on the same list
-    ("resnet50-momentum", 2048, "prepared"): {"fetch_kib": 113027.094, "write_kib": 124988.211},
-    ("resnet50-momentum", 2048, "plan"): {"fetch_kib": 113027.094, "write_kib": 124988.211},
-    ("quantize", 2048, "plan"): {"fetch_kib": 131141.912, "write_kib": 65792.0},
-    ("quantize", 2048, "call"): {"fetch_kib": 131144.000, "write_kib": 65792.0},
-    ("dequantize", 2048, "call"): {"fetch_kib": 33808.756, "write_kib": 262169.973},
+    ("resnet50-momentum", 2048, "prepared"): {"fetch_kib": 113029.578, "write_kib": 124988.250},
+    ("resnet50-momentum", 2048, "plan"): {"fetch_kib": 113029.578, "write_kib": 124988.250},
+    ("quantize", 2048, "plan"): {"fetch_kib": 131141.915, "write_kib": 65792.0},
+    ("quantize", 2048, "call"): {"fetch_kib": 131144.500, "write_kib": 65792.0},
+    ("dequantize", 2048, "call"): {"fetch_kib": 33808.749, "write_kib": 262144.0},
 }
 
 
