@@ -261,23 +261,69 @@ ORACLE_API int oracle_chunked_quantile_codebook(const float *x, int64_t n, int64
  * Exact sign of 2y - (a + b) for binary32 y, a, b.  For a < b,
  * |y - a| < |y - b|  <=>  (y - a)^2 < (y - b)^2  <=>  2y (b - a) < b^2 - a^2
  *                    <=>  2y < a + b,
- * so this decides which of two codes is nearer, with no rounding: a + b is
- * split exactly into s + e (Knuth's two-sum in double), t = 2y is exact, and
- * t - s is exact when t and s are within a factor 2 of each other (Sterbenz);
- * otherwise |t - s| exceeds |e| and decides alone.
+ * so this decides which of two codes is nearer.  It is evaluated in integers,
+ * with no rounding at all: every finite binary32 is an integer multiple of
+ * 2^-149 of magnitude below 2^128, so 2y, a and b are integers in units of
+ * 2^-149 below 2^279 and their signed sum fits a 320-bit two's-complement
+ * integer (five 64-bit limbs, least significant first).
  */
+enum { WIDE_LIMBS = 5 };
+
+/* acc += sign * m * 2^shift, for m < 2^24 and 0 <= shift <= 255 */
+static void wide_add(uint64_t acc[WIDE_LIMBS], int negative, uint64_t m, int shift)
+{
+    uint64_t t[WIDE_LIMBS] = {0, 0, 0, 0, 0};
+    const int limb = shift / 64, off = shift % 64;
+    t[limb] = m << off;
+    if (off > 40 && limb + 1 < WIDE_LIMBS)
+        t[limb + 1] = m >> (64 - off);
+    if (negative) { /* two's complement: invert, then add one below */
+        for (int i = 0; i < WIDE_LIMBS; ++i)
+            t[i] = ~t[i];
+    }
+    uint64_t carry = negative ? 1u : 0u;
+    for (int i = 0; i < WIDE_LIMBS; ++i) {
+        const uint64_t x = acc[i] + carry;
+        const uint64_t c1 = x < carry;
+        const uint64_t y = x + t[i];
+        const uint64_t c2 = y < x;
+        acc[i] = y;
+        carry = c1 + c2;
+    }
+}
+
+/* acc += (twice ? 2 : 1) * v in units of 2^-149, v finite */
+static void wide_add_float(uint64_t acc[WIDE_LIMBS], float v, int twice)
+{
+    uint32_t bits;
+    memcpy(&bits, &v, sizeof bits);
+    const int negative = (int)(bits >> 31);
+    const int biased = (int)((bits >> 23) & 0xffu);
+    uint64_t m = bits & 0x7fffffu;
+    int shift = 0; /* subnormal or zero: m * 2^-149 */
+    if (biased != 0) { /* normal: (2^23 + m) * 2^(biased - 150) */
+        m |= 0x800000u;
+        shift = biased - 1;
+    }
+    wide_add(acc, negative, m, shift + (twice ? 1 : 0));
+}
+
 static int sign_twice_y_minus_sum(float y, float a, float b)
 {
-    double A = a, B = b;
-    double s = A + B;
-    double bv = s - A;
-    double e = (A - (s - bv)) + (B - bv);
-    double t = 2.0 * (double)y;
-    if ((s > 0.0 && t >= 0.5 * s && t <= 2.0 * s) || (s < 0.0 && t <= 0.5 * s && t >= 2.0 * s)) {
-        double d = t - s;
-        return (d > e) - (d < e);
+    if (!isfinite(y) || !isfinite(a) || !isfinite(b)) { /* outside the contract */
+        const double t = 2.0 * (double)y, s = (double)a + (double)b;
+        return (t > s) - (t < s);
     }
-    return (t > s) - (t < s);
+    uint64_t acc[WIDE_LIMBS] = {0, 0, 0, 0, 0};
+    wide_add_float(acc, y, 1);
+    wide_add_float(acc, -a, 0);
+    wide_add_float(acc, -b, 0);
+    if (acc[WIDE_LIMBS - 1] >> 63)
+        return -1;
+    for (int i = 0; i < WIDE_LIMBS; ++i)
+        if (acc[i] != 0)
+            return 1;
+    return 0;
 }
 
 /*

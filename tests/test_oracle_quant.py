@@ -105,6 +105,26 @@ def test_random_values_exact_argmin(maps, name):
         assert oracle.nearest_bsearch(q, y) == e
 
 
+def test_nearest_exact_on_maps_spanning_the_binary32_range():
+    """The exact midpoint decision holds for any finite map, not only the
+    dynamic ones: strictly increasing maps whose magnitudes span 2^-149
+    (subnormal) to 2^100, with symmetric pairs (a + b == 0) and neighbours
+    many binades apart; probes at every binary32 midpoint +-2 ulps."""
+    rng = np.random.default_rng(7)
+    for trial in range(6):
+        mags = 2.0 ** rng.uniform(-149, 100, 300)
+        vals = np.concatenate([mags, -mags[:120], [0.0, 2.0 ** -149, -(2.0 ** -149)]])
+        q = np.unique(vals.astype(np.float32))
+        q = np.sort(rng.choice(q, 256, replace=False)).astype(np.float32)
+        assert np.all(np.diff(q.astype(np.float64)) > 0)
+        probes = midpoint_probes(q) + list(q) + [np.float32(0.0), np.float32(-0.0)]
+        ys = np.array(probes, np.float32)
+        exact = exact_nearest_many(q, ys)
+        for y, e in zip(ys, exact):
+            assert oracle.nearest_brute(q, y) == e, (trial, float(y))
+            assert oracle.nearest_bsearch(q, y) == e, (trial, float(y))
+
+
 @pytest.mark.parametrize("name", ["signed", "unsigned"])
 def test_nearest_property(maps, name):
     q = maps[name].astype(np.float64)
