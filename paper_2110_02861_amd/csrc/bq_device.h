@@ -75,16 +75,6 @@ __device__ inline bool above_midpoint(float y, float a, float b)
     return close ? (t - s) > e : t > s;
 }
 
-// #{j : t_j <= v} for finite v (at most 255 since t_255 = +inf).
-__device__ inline uint32_t count_le(const float *t, float v)
-{
-    uint32_t c = 0;
-#pragma unroll
-    for (uint32_t s = 128; s >= 1; s >>= 1)
-        c += (t[c + s - 1] <= v) ? s : 0u;
-    return c;
-}
-
 __device__ inline uint32_t bucket_lo_bits(uint32_t b)
 {
     return b == 0 ? 0u : (kBucketLo + b) << kBucketShift;
@@ -94,20 +84,81 @@ __device__ inline uint32_t bucket_hi_bits(uint32_t b)
     return b == kBuckets - 1 ? 0x7f7fffffu : ((kBucketLo + b + 1) << kBucketShift) - 1u;
 }
 
+// Where threshold v falls among the buckets.  Positive half: base[b] counts
+// the thresholds <= lo(b); v counts from bucket pos_pos(v) on (kBuckets: from
+// none).  Negative half: base[kBuckets + b] counts the thresholds <= -hi(b); v
+// counts for buckets b <= pos_neg(v) (-1: none).  inside_*: the bucket whose
+// interior (lo, hi] on the positive half, [-hi, -lo) mirrored (i.e. -hi < v <=
+// -lo) on the negative half, holds v, or -1.
+__device__ inline uint32_t bucket_clamped(uint32_t abs_bits)
+{
+    return min(max(abs_bits >> kBucketShift, kBucketLo), kBucketHi) - kBucketLo;
+}
+__device__ inline int pos_pos(float v)
+{
+    if (!(v > 0.0f))
+        return 0;  // v <= +0 <= lo(b) for every b
+    const uint32_t u = __float_as_uint(v);
+    const uint32_t b = bucket_clamped(u);
+    return (b >= 1 && u == bucket_lo_bits(b)) ? (int)b : (int)b + 1;
+}
+__device__ inline int inside_pos(float v)
+{
+    if (!(v > 0.0f))
+        return -1;
+    const uint32_t u = __float_as_uint(v);
+    const uint32_t b = bucket_clamped(u);
+    return (b >= 1 && u == bucket_lo_bits(b)) ? -1 : (int)b;
+}
+__device__ inline int pos_neg(float v)
+{
+    if (!(v < 0.0f))
+        return -1;  // -hi(b) < 0 <= v for every b
+    const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
+    const uint32_t b = bucket_clamped(a);
+    return a == bucket_hi_bits(b) ? (int)b : (int)b - 1;
+}
+__device__ inline int inside_neg(float v)
+{
+    if (v > 0.0f)
+        return -1;
+    if (!(v < 0.0f))
+        return 0;  // +-0: -hi(0) < v <= -lo(0) = -0
+    const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
+    const uint32_t b = bucket_clamped(a);
+    return a == bucket_hi_bits(b) ? -1 : (int)b;
+}
+
 // Build q, t, base and kmax for one map.  All NT threads of the workgroup take
-// part (NT >= 256); the function contains barriers.  q, t and base may live in
-// LDS or global memory; t must be readable by every thread after the first
-// barrier.  kmax_out is an LDS int, set to the maximum over the workgroup.
+// part (NT >= 512, a multiple of 64); the function contains barriers.  q and t
+// may live in LDS or global memory (t is read back after the first barrier);
+// base must be LDS, 4-byte aligned.  kmax_out is an LDS int, set to the maximum
+// over the workgroup.
+//
+// base is a prefix count over the buckets of a sorted threshold list, so it is
+// formed without any search: every threshold adds one to a byte histogram at
+// the first bucket it counts for (LDS atomics on the dword that holds the
+// byte; no byte exceeds 255 thresholds), then a workgroup scan turns the
+// histogram into counts, ascending over the positive half and descending over
+// the negative half.  Thresholds inside one bucket are consecutive, so kmax is
+// the longest run of equal inside_* buckets, counted from each run's start.
 template <int NT>
 __device__ void build_tables(const float *__restrict__ qmap, float *q, float *t, uint8_t *base,
                              int *kmax_out)
 {
-    static_assert(NT >= 256, "one thread per code");
+    static_assert(NT >= 512 && NT % 64 == 0, "two scan halves of at least 208 threads");
+    constexpr int kHalf = NT / 2;
+    constexpr int kPerThread = 16;                         // buckets scanned per thread
+    constexpr int kScanThreads = (int)kBuckets / kPerThread;  // per half
+    static_assert(kScanThreads * kPerThread == (int)kBuckets && kScanThreads <= kHalf,
+                  "scan layout");
+    __shared__ uint32_t wave_sums[NT / 64];
+    uint32_t *hist = reinterpret_cast<uint32_t *>(base);
     const uint32_t j = threadIdx.x;
+    float thr = __builtin_inff();
     if (j < 256) {
         const float qj = qmap[j];
         q[j] = qj;
-        float thr = __builtin_inff();
         if (j < 255) {
             // the smallest fp32 strictly above the exact midpoint: start from
             // the double midpoint (exact unless the codes are 2^29 apart in
@@ -125,47 +176,102 @@ __device__ void build_tables(const float *__restrict__ qmap, float *q, float *t,
         }
         t[j] = thr;
     }
+    for (uint32_t i = j; i < 2 * kBuckets / 4; i += NT)
+        hist[i] = 0u;
     if (j == 0)
         *kmax_out = 0;
     __syncthreads();
 
-    // Each thread walks a contiguous run of buckets on each side in ascending
-    // value order: one binary search, then a forward scan gives every count.
-    constexpr uint32_t kPer = (kBuckets + NT - 1) / NT;
-    const uint32_t b0 = j * kPer;
-    const uint32_t b1 = b0 + kPer < kBuckets ? b0 + kPer : kBuckets;
-    int kmax = 0;
-    if (b0 < b1) {
-        // positive side: values [lo, hi] rise with b
-        uint32_t c = count_le(t, __uint_as_float(bucket_lo_bits(b0)));
-        for (uint32_t b = b0; b < b1; ++b) {
-            const float lo = __uint_as_float(bucket_lo_bits(b));
-            const float hi = __uint_as_float(bucket_hi_bits(b));
-            while (t[c] <= lo)
-                ++c;
-            base[b] = (uint8_t)c;
-            uint32_t e = c;
-            while (t[e] <= hi)
-                ++e;
-            kmax = max(kmax, (int)(e - c));
-            c = e;
+    // histogram of first counting buckets; runs of thresholds inside a bucket
+    if (j < 255) {
+        const int pp = pos_pos(thr);
+        if (pp < (int)kBuckets)
+            atomicAdd(&hist[pp >> 2], 1u << (8 * (pp & 3)));
+        const int pn = pos_neg(thr);
+        if (pn >= 0) {
+            const uint32_t i = kBuckets + (uint32_t)pn;
+            atomicAdd(&hist[i >> 2], 1u << (8 * (i & 3)));
         }
-        // negative side: values [-hi, -lo] rise as b falls
-        c = count_le(t, -__uint_as_float(bucket_hi_bits(b1 - 1)));
-        for (uint32_t b = b1; b-- > b0;) {
-            const float lo = -__uint_as_float(bucket_hi_bits(b));
-            const float hi = -__uint_as_float(bucket_lo_bits(b));
-            while (t[c] <= lo)
-                ++c;
-            base[kBuckets + b] = (uint8_t)c;
-            uint32_t e = c;
-            while (t[e] <= hi)
-                ++e;
-            kmax = max(kmax, (int)(e - c));
-            c = e;
+        int run = 0;
+        const int ip = inside_pos(thr);
+        if (ip >= 0 && (j == 0 || inside_pos(t[j - 1]) != ip)) {
+            run = 1;
+            while (j + run < 255 && inside_pos(t[j + run]) == ip)
+                ++run;
         }
+        const int in = inside_neg(thr);
+        if (in >= 0 && (j == 0 || inside_neg(t[j - 1]) != in)) {
+            int r = 1;
+            while (j + r < 255 && inside_neg(t[j + r]) == in)
+                ++r;
+            run = max(run, r);
+        }
+        if (run > 0)
+            atomicMax(kmax_out, run);
     }
-    atomicMax(kmax_out, kmax);
+    __syncthreads();
+
+    // scan: thread k of a half takes 16 consecutive buckets (scan order: up
+    // the positive half, down the negative half); in-thread running sums, a
+    // wave scan of the thread totals, then the totals of the earlier waves
+    const int side = (int)j / kHalf;
+    const int k = (int)j % kHalf;
+    const bool active = k < kScanThreads;
+    const int b0 = side == 0 ? kPerThread * k : kPerThread * (kScanThreads - 1 - k);
+    const int d0 = (side == 0 ? 0 : (int)kBuckets / 4) + b0 / 4;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    if (active) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            w[i] = hist[d0 + i];
+    }
+    uint32_t total = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        total += (w[i] & 0xffu) + ((w[i] >> 8) & 0xffu) + ((w[i] >> 16) & 0xffu) + (w[i] >> 24);
+    const int lane = (int)j & 63;
+    uint32_t incl = total;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t v = __shfl_up(incl, off);
+        if (lane >= off)
+            incl += v;
+    }
+    if (lane == 63)
+        wave_sums[j >> 6] = incl;
+    __syncthreads();
+    uint32_t run_sum = incl - total;  // counts of the earlier threads of this wave
+    for (int wv = side * (kHalf / 64); wv < (int)(j >> 6); ++wv)
+        run_sum += wave_sums[wv];
+    if (active) {
+        uint32_t o[4];
+        if (side == 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                uint32_t packed = 0;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    run_sum += (w[i] >> (8 * r)) & 0xffu;
+                    packed |= run_sum << (8 * r);
+                }
+                o[i] = packed;
+            }
+        } else {
+#pragma unroll
+            for (int i = 3; i >= 0; --i) {
+                uint32_t packed = 0;
+#pragma unroll
+                for (int r = 3; r >= 0; --r) {
+                    run_sum += (w[i] >> (8 * r)) & 0xffu;
+                    packed |= run_sum << (8 * r);
+                }
+                o[i] = packed;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            hist[d0 + i] = o[i];
+    }
     __syncthreads();
 }
 
