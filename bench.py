@@ -50,20 +50,20 @@ BLOCKSIZE = 2048
 # kernel sources the counters were taken on (sha256 below); otherwise the
 # bench reports traffic null.  Keys: (workload, blocksize, path).
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h", "bq_scalars.h"]
-TRAFFIC_SOURCES_SHA256 = "8fa6f3e06a8d51817be118c736b0bad0a08fbd1acca8fcb435dea8fd6822aea0"
+TRAFFIC_SOURCES_SHA256 = "d388e8dc39dd29f1fc60b0d2376270c0d43652bcf81fb3868edc128a5896e482"
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6133023.000, "write_kib": 9150410.375},
-    ("lm1p5b-adam", 2048, "static"): {"fetch_kib": 6109145.781, "write_kib": 9150410.492},
+    ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132950.734, "write_kib": 9150410.344},
+    ("lm1p5b-adam", 2048, "static"): {"fetch_kib": 6109054.891, "write_kib": 9150410.578},
     # 11 launches per step: the mean per dispatch times 11
-    ("lm1p5b-adam", 2048, "call"): {"fetch_kib": 11 * 555789.783, "write_kib": 11 * 831893.744},
-    ("gpt2m-adamw", 2048, "plan"): {"fetch_kib": 1397266.750, "write_kib": 2084463.672},
+    ("lm1p5b-adam", 2048, "call"): {"fetch_kib": 11 * 555761.575, "write_kib": 11 * 831891.200},
+    ("gpt2m-adamw", 2048, "plan"): {"fetch_kib": 1397257.109, "write_kib": 2084463.539},
     # the plan and prepared paths run the same step kernel on the same list
-    ("resnet50-momentum", 2048, "prepared"): {"fetch_kib": 113029.578, "write_kib": 124988.250},
-    ("resnet50-momentum", 2048, "plan"): {"fetch_kib": 113029.578, "write_kib": 124988.250},
-    ("quantize", 2048, "plan"): {"fetch_kib": 131141.915, "write_kib": 65792.0},
-    ("quantize", 2048, "call"): {"fetch_kib": 131144.500, "write_kib": 65792.0},
-    ("dequantize", 2048, "call"): {"fetch_kib": 33808.749, "write_kib": 262144.0},
+    ("resnet50-momentum", 2048, "prepared"): {"fetch_kib": 113032.703, "write_kib": 124988.266},
+    ("resnet50-momentum", 2048, "plan"): {"fetch_kib": 113032.703, "write_kib": 124988.266},
+    ("quantize", 2048, "plan"): {"fetch_kib": 131141.926, "write_kib": 65792.0},
+    ("quantize", 2048, "call"): {"fetch_kib": 131174.500, "write_kib": 65792.0},
+    ("dequantize", 2048, "call"): {"fetch_kib": 33812.742, "write_kib": 262144.0},
 }
 
 
@@ -485,13 +485,17 @@ def timed(torch, stream, fn, steps, warmup, per_event):
     sorted per-call ms of each event segment)."""
     for i in range(warmup):
         fn(i)
+    # every event is created before the timed region: creating one inside it
+    # is a host call that can stall the enqueue of a short step
+    nev = 1 + (steps + per_event - 1) // per_event
+    pool = [torch.cuda.Event(enable_timing=True) for _ in range(nev)]
     torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True)]
+    evs = [pool[0]]
     evs[0].record(stream)
     for i in range(steps):
         fn(warmup + i)
         if (i + 1) % per_event == 0 or i + 1 == steps:
-            e = torch.cuda.Event(enable_timing=True)
+            e = pool[len(evs)]
             e.record(stream)
             evs.append(e)
     torch.cuda.synchronize()
