@@ -95,8 +95,8 @@ constexpr int kSTWaves = kST / 64;
 // Prepare: decision tables of 1 or 2 maps (one workgroup each)
 // ---------------------------------------------------------------------------
 
-// kPrepThreads threads per map: each walks ceil(3328 / kPrepThreads) buckets
-// of each sign, a chain of dependent LDS reads that sets the kernel's length.
+// kPrepThreads threads per map build its tables (build_tables: the thresholds,
+// a byte histogram of where each one starts counting, one workgroup scan).
 constexpr int kPrepThreads = 1024;
 
 __global__ __launch_bounds__(kPrepThreads) void prepare_kernel(const float *__restrict__ q1,
