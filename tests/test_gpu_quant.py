@@ -235,6 +235,28 @@ def test_exact_thresholds_for_uneven_maps():
         run_pair(qm, dev(qm), np.concatenate(blocks), B)
 
 
+def test_dense_bucket_map():
+    """150 codes one ulp apart inside one bucket (just above 0.5): the bucket
+    table leaves up to 149 thresholds to compare, so the search loop runs far
+    beyond the dynamic maps' single compare, in the per-workgroup tables of
+    the raw-map call and in the prepared tables alike."""
+    low = np.linspace(-1.0, 0.49, 105).astype(np.float32)
+    dense = np.float32(0.5) + np.arange(150, dtype=np.float32) * np.float32(2.0 ** -24)
+    q = np.concatenate([low, dense, [np.float32(1.0)]]).astype(np.float32)
+    assert q.size == 256 and np.all(np.diff(q.astype(np.float64)) > 0)
+    rng = np.random.default_rng(21)
+    B = 2048
+    nblk = 6
+    x = np.empty(nblk * B, np.float32)
+    for b in range(nblk):
+        blk = np.float32(0.5) + rng.integers(-5, 160, B).astype(np.float32) * np.float32(2.0 ** -24)
+        spread = rng.random(B) < 0.2
+        blk[spread] = rng.uniform(-1, 1, int(spread.sum())).astype(np.float32)
+        blk[0] = 1.0
+        x[b * B:(b + 1) * B] = blk * np.float32(2.0 ** (b - 3))
+    run_pair(q, dev(q), x, B)
+
+
 @pytest.mark.parametrize("B", [256, 2048])
 def test_block_isolation_on_gpu(B):
     """Changing one block's values changes only that block's codes and absmax
