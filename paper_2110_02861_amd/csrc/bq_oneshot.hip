@@ -1118,8 +1118,8 @@ __global__ __launch_bounds__(kOS) void quantize_persistent_kernel(const float *_
     __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsQuantBytes];
     __shared__ int kmax;
     // the first tile's loads are issued before the tables are built, so the
-    // build overlaps them (measured: 67.9 -> 66.7 us at 67M elements; loading
-    // every next tile ahead took 103 VGPRs, two workgroups per CU, 70.8 us)
+    // build overlaps them (loading every next tile ahead instead needed 103
+    // VGPRs, two workgroups per CU, and was slower)
     const int64_t tiles = (n + S::TILE - 1) / S::TILE;
     int64_t tile = blockIdx.x;
     bool full = (tile + 1) * S::TILE <= n;
