@@ -5,6 +5,8 @@ import os
 import subprocess
 import sys
 
+import pytest
+
 import bench
 from paper_2110_02861_amd import workloads
 
@@ -83,3 +85,50 @@ def test_cpu_model_is_read_from_proc_cpuinfo():
     m = bench.cpu_model()
     if os.path.exists("/proc/cpuinfo"):
         assert isinstance(m, str) and m
+
+
+def test_stream_library_describes_its_variants_and_refuses_bad_arguments():
+    """libbq_stream.so (the benchmark's stream ceilings and the access-shape
+    study): variant descriptions and argument checks, which return before any
+    HIP call."""
+    import ctypes
+    from paper_2110_02861_amd import build as pkg_build
+    if not os.path.exists(pkg_build.STREAM_LIB):
+        pytest.skip("libbq_stream.so is not built")
+    L = ctypes.CDLL(pkg_build.STREAM_LIB)
+    P = ctypes.c_void_p
+    L.bq_stream_study_info.restype = ctypes.c_char_p
+    L.bq_stream_study_info.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
+    L.bq_stream_study.argtypes = [ctypes.c_int, ctypes.POINTER(P), ctypes.POINTER(P),
+                                  ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, P, ctypes.c_int,
+                                  P]
+    L.bq_stream_ceiling.argtypes = [ctypes.c_int] + [P] * 6 + [ctypes.c_int64, ctypes.c_int32,
+                                                               ctypes.c_uint32, P, P]
+    assert L.bq_stream_variants() == 9
+    nv = L.bq_stream_study_variants()
+    assert nv >= 28
+    names = set()
+    for v in range(nv):
+        info = (ctypes.c_int * 3)()
+        name = L.bq_stream_study_info(v, info).decode()
+        assert name and name not in names
+        names.add(name)
+        assert info[0] in (256, 512, 1024) and info[1] in (1, 2, 4) and info[2] in (0, 1, 2)
+        assert info[0] * info[1] * 4 >= 2048
+    assert L.bq_stream_study_info(nv, None) == b"" and L.bq_stream_study_info(-1, None) == b""
+    fake = 1 << 20  # never dereferenced: every call below fails its argument checks
+    good = (P * 6)(*[fake] * 6)
+    n = 8192 * 4
+    assert L.bq_stream_study(-1, good, good, n, 2048, 0, P(fake), 0, None) == -1
+    assert L.bq_stream_study(nv, good, good, n, 2048, 0, P(fake), 0, None) == -1
+    assert L.bq_stream_study(0, good, good, n + 4096, 2048, 0, P(fake), 0, None) == -1
+    assert L.bq_stream_study(0, good, good, n, 3000, 0, P(fake), 0, None) == -1
+    assert L.bq_stream_study(0, good, good, n, 2048, 0, P(fake + 4), 0, None) == -1
+    assert L.bq_stream_study(0, good, good, n, 2048, 0, P(fake), 5, None) == -1
+    assert L.bq_stream_study(0, good, good, n, 2048, 0, P(fake), 1, None) == -1
+    bad = (P * 6)(*([fake] * 5 + [fake + 8]))
+    assert L.bq_stream_study(0, bad, good, n, 2048, 0, P(fake), 0, None) == -1
+    nul = (P * 6)(*([fake] * 5 + [None]))
+    assert L.bq_stream_study(0, good, nul, n, 2048, 0, P(fake), 0, None) == -1
+    assert L.bq_stream_ceiling(9, *[P(fake)] * 6, n, 2048, 0, P(fake), None) == -1
+    assert L.bq_stream_ceiling(0, *[P(fake)] * 6, n + 100, 2048, 0, P(fake), None) == -1
