@@ -252,19 +252,25 @@ def test_determinism_and_resume():
 def _map_families():
     normal = workloads.host_rng(0, "c2", 2, 0).standard_normal(100_001).astype(np.float32)
     heavy = np.abs(workloads.student_t_host(100_001, seed=13))
+    # 150 codes one ulp apart inside one bucket: 149 threshold compares
+    dense = np.float32(0.5) + np.arange(150, dtype=np.float32) * np.float32(2.0 ** -24)
+    one = np.array([1.0], np.float32)
     return {
         "inverse_dynamic": (oracle.codebook(2), oracle.codebook(3)),
         "linear": (oracle.codebook(4), oracle.codebook(5)),
         "quantile": (oracle.quantile_codebook(normal), oracle.quantile_codebook(heavy)),
+        "dense_bucket": (np.concatenate([np.linspace(-1.0, 0.49, 105).astype(np.float32), dense, one]),
+                         np.concatenate([np.linspace(0.0, 0.49, 105).astype(np.float32), dense, one])),
     }
 
 
 @pytest.mark.parametrize("path", PATHS)
-@pytest.mark.parametrize("family", ["inverse_dynamic", "linear", "quantile"])
+@pytest.mark.parametrize("family", ["inverse_dynamic", "linear", "quantile", "dense_bucket"])
 @pytest.mark.parametrize("opt", ["adam", "momentum"])
 def test_other_codebooks_step(opt, family, path):
     """The step with the App. F maps (the inverse unsigned map puts up to 28
-    thresholds in one bucket: the general search path)."""
+    thresholds in one bucket: the general search path) and with maps that put
+    149 thresholds in one bucket."""
     q1, q2 = _map_families()[family]
     run_lists(opt, 2048, bq.BQ_F16, [1, 2047, 4097, 3 * 4096 + 77], 3, seed=5, path=path,
               maps=(q1, q2))
