@@ -676,7 +676,7 @@ def run_list(args, torch, bq, workloads):
             "frac": gbs / HBM_PEAK_GBS,
             "traffic": measured_traffic(args.workload, B, args.path),
             "bytes_per_step": bytes_step,
-            "kernel": kname + {"plan": " (+ prepare_kernel, ~7 us, inside the timed launch pair)",
+            "kernel": kname + {"plan": " (+ prepare_kernel, ~6 us, inside the timed launch pair)",
                                "device": " (+ scalars_kernel: the step's scalars from device "
                                          "hyperparameters)"}.get(args.path, ""),
         },
