@@ -28,6 +28,11 @@ def _inputs():
         "abs_t": np.abs(workloads.student_t_host(200_000, seed=4)),
         "ties": np.round(rng.standard_normal(50_000) * 3).astype(np.float32),
         "zeros": np.zeros(9000, np.float32),
+        "constant": np.full(10_000, 3.0, np.float32),
+        "negative": -np.abs(rng.standard_normal(30_000)).astype(np.float32) - 1.0,
+        "wide_range": (np.sign(rng.standard_normal(40_000)) *
+                       10.0 ** rng.uniform(-30, 30, 40_000)).astype(np.float32),
+        "group_edge": rng.standard_normal(64 * 4096 + 1).astype(np.float32),
         "normal_1m": rng.standard_normal(1 << 20).astype(np.float32),
     }
 
