@@ -177,7 +177,8 @@ __global__ __launch_bounds__(kQThreads) void chunk_quantiles_kernel(const float 
 }
 
 // One workgroup per group of kQGroup chunks: length-weighted sums of the chunk
-// quantiles, in chunk order, in double.
+// quantiles, in chunk order, in double.  A full group's kQGroup loads are all
+// issued before the first add (the adds keep chunk order).
 __global__ __launch_bounds__(320) void group_sums_kernel(const float *__restrict__ partial,
                                                          int64_t n, int64_t nchunks,
                                                          double *__restrict__ gsum)
@@ -188,10 +189,23 @@ __global__ __launch_bounds__(320) void group_sums_kernel(const float *__restrict
     const int64_t c0 = (int64_t)blockIdx.x * kQGroup;
     const int64_t c1 = c0 + kQGroup < nchunks ? c0 + kQGroup : nchunks;
     double s = 0.0;
-    for (int64_t c = c0; c < c1; ++c) {
-        const int64_t rem = n - c * kQChunk;
-        const double L = (double)(rem >= kQChunk ? kQChunk : rem);
-        s += L * (double)G(partial)[c * 257 + tid];
+    if (c1 - c0 == kQGroup) {
+        float v[kQGroup];
+#pragma unroll
+        for (int k = 0; k < kQGroup; ++k)
+            v[k] = G(partial)[(c0 + k) * 257 + tid];
+#pragma unroll
+        for (int k = 0; k < kQGroup; ++k) {
+            const int64_t rem = n - (c0 + k) * kQChunk;
+            const double L = (double)(rem >= kQChunk ? kQChunk : rem);
+            s += L * (double)v[k];
+        }
+    } else {
+        for (int64_t c = c0; c < c1; ++c) {
+            const int64_t rem = n - c * kQChunk;
+            const double L = (double)(rem >= kQChunk ? kQChunk : rem);
+            s += L * (double)G(partial)[c * 257 + tid];
+        }
     }
     G(gsum)[(int64_t)blockIdx.x * 257 + tid] = s;
 }
@@ -204,7 +218,10 @@ __global__ __launch_bounds__(kCombineThreads) void combine_quantiles_kernel(
     __shared__ double q[256];
     __shared__ double red[256];
     __shared__ float map[256];
+    __shared__ int tie;
     const int tid = threadIdx.x;
+    if (tid == 0)
+        tie = 0;
     if (tid <= 256) {
         // in group order; loads issued 32 at a time
         double s = 0.0;
@@ -238,8 +255,13 @@ __global__ __launch_bounds__(kCombineThreads) void combine_quantiles_kernel(
     if (tid < 256)
         map[tid] = (float)(amax > 0.0 ? q[tid] / amax : q[tid]);
     __syncthreads();
-    // equal neighbours (ties in the sample) moved up by one ulp, in order
-    if (tid == 0) {
+    // equal neighbours (ties in the sample) moved up by one ulp, in order; the
+    // serial pass runs only when some neighbour is not strictly above its
+    // predecessor
+    if (tid >= 1 && tid < 256 && !(map[tid] > map[tid - 1]))
+        tie = 1;
+    __syncthreads();
+    if (tid == 0 && tie) {
         for (int i = 1; i < 256; ++i)
             if (!(map[i] > map[i - 1]))
                 map[i] = next_up(map[i - 1]);
